@@ -1,0 +1,303 @@
+/*
+ * ard.h - Approximate Random Dropout hot path for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Song et al., "Approximate Random Dropout for DNN training
+ * acceleration in GPGPU" (arXiv 1805.08939). Random dropout is replaced by
+ * regular patterns so that dropped neurons (row-based pattern, Sec. III-A) and
+ * dropped weight tiles (tile-based pattern, Sec. III-B) are skipped outright:
+ * the GEMMs below never load, multiply or store them. Each iteration a pattern
+ * is sampled from a distribution K (Sec. III-D) that the SGD-based search of
+ * Sec. III-C (Alg. 1) produces.
+ *
+ * Conventions shared by every call:
+ *  - Every function returns an ard_status (0 = ARD_OK). On failure a
+ *    thread-local message is available from ard_last_error(), and no device
+ *    work has been enqueued. Nothing aborts or throws across this boundary.
+ *  - Buffers are caller-owned. The library never allocates or frees device
+ *    memory; where a call needs scratch space its size is queried first and the
+ *    caller passes it in (ws, ws_bytes).
+ *  - "stream" is a hipStream_t passed as void* (NULL = the null stream). Device
+ *    calls are asynchronous and stream-ordered; the library never synchronises.
+ *  - Device pointers must be 16-byte aligned. Matrices are dense row-major
+ *    with the row lengths stated at each argument.
+ *  - Activations are stored feature-major: Xt[K][B] holds input feature k of
+ *    every sample in one contiguous row (the transpose of the math layout
+ *    X[B][K]), so that a dropped neuron is a skipped row. Weights are stored
+ *    output-major, W[N][K]: one row per output neuron.
+ *  - dtype ARD_BF16 means bf16 activations, weights and activation gradients
+ *    with fp32 accumulation; bias, weight and bias gradients are always fp32.
+ */
+#ifndef ARD_H
+#define ARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARD_VERSION 1
+
+typedef enum {
+  ARD_OK = 0,
+  ARD_ERR_INVALID_ARG = 1,   /* a size, pointer, pattern or option is invalid */
+  ARD_ERR_UNSUPPORTED = 2,   /* valid but not implemented (e.g. a dtype) */
+  ARD_ERR_HIP = 3,           /* the HIP runtime reported an error */
+  ARD_ERR_NOT_CONVERGED = 4, /* the search hit max_iters; its output is the last iterate */
+  ARD_ERR_WORKSPACE = 5      /* ws is NULL or smaller than the queried size */
+} ard_status;
+
+typedef enum { ARD_F32 = 0, ARD_BF16 = 1 } ard_dtype;
+
+/* Human-readable name of a status code (static string). */
+const char* ard_status_string(int status);
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* ard_last_error(void);
+/* ARD_VERSION of the built library. */
+int ard_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Pattern distribution search (host).                                      */
+/* ------------------------------------------------------------------------ */
+/*
+ * Alg. 1 (Sec. III-C): find K = softmax(v) over periods 1..n_max minimising
+ *     lambda1 * (K . p_u - p)^2 + (1 - lambda1) * (1/n_max) * sum_i K_i log K_i,
+ * p_u[i] = (i - 1) / i, by gradient descent on v from v = 0 until the change of
+ * the loss is below `threshold`.
+ *   mode ARD_SEARCH_PLAIN : v -= lr * dL/dv  (the paper's iteration)
+ *   mode ARD_SEARCH_MIRROR: v -= lr * dL/dK  (entropic mirror descent; same
+ *                           minimiser, far fewer iterations for large n_max)
+ */
+enum { ARD_SEARCH_PLAIN = 0, ARD_SEARCH_MIRROR = 1 };
+
+typedef struct {
+  int32_t n_max;      /* number of candidate periods, >= 1 */
+  int32_t mode;       /* ARD_SEARCH_PLAIN or ARD_SEARCH_MIRROR */
+  double lambda1;     /* weight of the rate term, in (0, 1); lambda2 = 1 - lambda1 */
+  double lr;          /* step size, > 0 */
+  double threshold;   /* stop when |loss_t - loss_{t-1}| < threshold, >= 0 */
+  int64_t max_iters;  /* >= 1 */
+} ard_search_opts;
+
+typedef struct {
+  int64_t iters;        /* iterations run */
+  double loss;          /* final loss */
+  double p_global;      /* Eq. 3: sum_i K_i (i - 1) / i */
+  double kkt_residual;  /* max_i dL/dK_i - min_i dL/dK_i (0 at the optimum) */
+  int32_t converged;    /* 1 if the stop rule fired */
+  int32_t reserved;
+} ard_search_info;
+
+/* Defaults: n_max 16, PLAIN, lambda1 0.99, lr 10, threshold 1e-15, max_iters 1e6. */
+void ard_search_opts_default(ard_search_opts* opts);
+
+/*
+ * Search K for target rate p. K_out: host array of opts->n_max doubles
+ * (caller-owned). info may be NULL. opts NULL = defaults.
+ * p = 0 returns K = e_1 exactly without iterating. p must satisfy
+ * 0 <= p < (n_max - 1) / n_max, else ARD_ERR_INVALID_ARG. If max_iters is
+ * reached K_out holds the last iterate and ARD_ERR_NOT_CONVERGED is returned.
+ */
+int ard_search_distribution(double p, const ard_search_opts* opts, double* K_out,
+                            ard_search_info* info);
+
+/* ------------------------------------------------------------------------ */
+/* Pattern sampling (host).                                                 */
+/* ------------------------------------------------------------------------ */
+/*
+ * A row pattern (Sec. III-A, Eq. 1): neuron j (0-based) is KEPT iff
+ * j % period == offset. The paper's (dp, b) is (period, offset + 1).
+ */
+typedef struct {
+  int32_t period;  /* >= 1; 1 = no dropout */
+  int32_t offset;  /* 0 <= offset < period */
+} ard_row_pattern;
+
+/*
+ * Sec. III-D: draw period ~ K (inverse CDF over sequential fp64 partial sums)
+ * and offset uniform in [0, period) from the counter-based SplitMix64 stream of
+ * (seed, stream, iter): initial state seed ^ ((stream << 40) | iter),
+ * stream < 2^24, iter < 2^40. Reproducible from any iteration; one stream per
+ * dropout layer. K: host, n_max entries, non-negative with a positive entry.
+ */
+int ard_sample_row_pattern(const double* K, int32_t n_max, uint64_t seed, uint32_t stream,
+                           uint64_t iter, ard_row_pattern* out);
+
+/* Kept count of n neurons under (period, offset): 0 if offset >= n, else
+ * ceil((n - offset) / period). Returns -1 on invalid arguments. */
+int32_t ard_row_kept(int32_t n, int32_t period, int32_t offset);
+
+/*
+ * Tile bitmaps over the tiles_n x tiles_k tile grid of W[N][K] (Sec. III-B).
+ * Tile t = tn * tiles_k + tk (row-major) is KEPT iff bit t is set, stored in
+ * word t / 32 at bit t % 32. bits: host, ceil(tiles_n * tiles_k / 32) words.
+ *   _tdp      : kept iff t % period == offset (the paper's tile pattern)
+ *   _bernoulli: tile t takes the t-th uniform of the (seed, stream, iter)
+ *               stream and is kept iff it is >= p (DropConnect-style tiles)
+ */
+int ard_tile_bitmap_tdp(int32_t tiles_n, int32_t tiles_k, int32_t period, int32_t offset,
+                        uint32_t* bits);
+int ard_tile_bitmap_bernoulli(int32_t tiles_n, int32_t tiles_k, double p, uint64_t seed,
+                              uint32_t stream, uint64_t iter, uint32_t* bits);
+/* Number of set bits among the first `total` bits (host). -1 on invalid args. */
+int32_t ard_bitmap_popcount(const uint32_t* bits, int32_t total);
+
+/* ------------------------------------------------------------------------ */
+/* Compaction: patterns -> gather lists (device kernels).                   */
+/* ------------------------------------------------------------------------ */
+/*
+ * The compact index list of a row pattern (Sec. III-A: the compact matrices are
+ * built from the kept rows only). Fills d_idx[0..kept) with the kept neuron
+ * indices in ascending order and the plan struct (host) with n, the pattern and
+ * the host-known kept count, so that later launches need no device readback.
+ * d_idx: device, capacity >= ard_row_kept(n, period, offset), caller-owned.
+ */
+typedef struct {
+  int32_t n;
+  int32_t period;
+  int32_t offset;
+  int32_t kept;
+  int32_t* d_idx;
+} ard_row_plan;
+
+int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard_row_plan* plan,
+                  void* stream);
+
+/*
+ * Tile plan (Sec. III-B: only non-dropped tiles are fetched). From the device
+ * bitmap d_bits of an N x K weight matrix in tile x tile tiles, a scan kernel
+ * writes into the workspace:
+ *   row_ptr[tiles_n + 1], row_cols[nnz]  kept tile columns per tile row (CSR)
+ *   col_ptr[tiles_k + 1], col_rows[nnz]  kept tile rows per tile column (CSC)
+ *   flat[nnz]                            kept linear tile indices
+ * all ascending. nnz must equal the popcount of the bitmap (host-known, see
+ * ard_bitmap_popcount). tile must be 32 or 64, and n, k multiples of it.
+ */
+typedef struct {
+  int32_t n, k, tile, tiles_n, tiles_k, nnz;
+  const uint32_t* d_bits;
+  int32_t* d_row_ptr;
+  int32_t* d_row_cols;
+  int32_t* d_col_ptr;
+  int32_t* d_col_rows;
+  int32_t* d_flat;
+} ard_tile_plan;
+
+size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k);
+int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, int32_t nnz,
+                   void* d_ws, size_t ws_bytes, ard_tile_plan* plan, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Fully connected layer under row patterns (device).                       */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. III-A with the dropout layer folded in (Sec. III-B, last paragraph):
+ * in_plan is the pattern of the layer's input neurons (the previous layer's
+ * output pattern), out_plan that of its outputs; NULL or period 1 = all kept.
+ * With S_in, S_out the kept sets and G = scale * act'(.) * dY on kept rows:
+ *   fwd       Yt[S_out,:] = scale * act(W[S_out,S_in] Xt[S_in,:] + bias[S_out])
+ *   bwd_data  dXt[S_in,:] = W[S_out,S_in]^T G[S_out,:]
+ *   bwd_weight dW[S_out,S_in] = G[S_out,:] Xt[S_in,:]^T,  dbias[S_out] = G 1
+ * Only kept rows/columns are read or computed. Entries outside the kept sets
+ * are written 0 (ARD_DROPPED_ZERO) or left untouched (ARD_DROPPED_SKIP).
+ * The ReLU derivative is taken from the stored forward output: [Yt > 0].
+ * Layouts: Xt[K][B], W[N][K], bias[N] fp32, Yt and dYt[N][B], dXt[K][B],
+ * dW[N][K] fp32, dbias[N] fp32 (K = in_features, N = out_features, B = batch).
+ */
+typedef enum { ARD_ACT_NONE = 0, ARD_ACT_RELU = 1 } ard_act;
+typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
+
+typedef struct {
+  int32_t dtype;        /* ard_dtype */
+  int32_t batch;        /* B >= 1 */
+  int32_t in_features;  /* K >= 1 */
+  int32_t out_features; /* N >= 1 */
+  const ard_row_plan* in_plan;   /* n == K, or NULL */
+  const ard_row_plan* out_plan;  /* n == N, or NULL */
+  float scale;          /* multiplies kept outputs (1 = pure mask) */
+  int32_t act;          /* ard_act */
+  int32_t dropped;      /* ard_dropped */
+  int32_t reserved;
+} ard_fc_desc;
+
+int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias,
+               void* Yt, void* stream);
+/* Yt: the forward output (for the ReLU gate), may be NULL when act == NONE. */
+int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
+                    void* dXt, void* stream);
+/* dbias may be NULL. */
+int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
+                      float* dW, float* dbias, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Layer under a tile pattern (device).                                     */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. III-B: with M the kept-tile mask of W expanded to tile x tile blocks,
+ *   fwd        Yt  = scale * (W * M) Xt
+ *   bwd_data   dXt = scale * (W * M)^T dYt
+ *   bwd_weight dW  = scale * M * (dYt Xt^T)
+ * Only kept tiles of W are read (fwd, bwd_data) or computed (bwd_weight).
+ * Every row of Yt and dXt is written (a row block with no kept tile gets 0);
+ * dW outside kept tiles is 0 (ZERO) or untouched (SKIP).
+ * Layouts as for the FC layer; in_features = plan->k, out_features = plan->n.
+ */
+typedef struct {
+  int32_t dtype;
+  int32_t batch;
+  int32_t in_features;
+  int32_t out_features;
+  float scale;
+  int32_t dropped;
+} ard_tile_desc;
+
+int ard_tile_fwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt,
+                 const void* W, void* Yt, void* stream);
+int ard_tile_bwd_data(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* dYt,
+                      const void* W, void* dXt, void* stream);
+int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt,
+                        const void* dYt, float* dW, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* LSTM layer with hidden-unit row pattern fixed per sequence (device).     */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. IV-C applies the method to LSTM as matrix multiplication. Dropped
+ * hidden units are removed for the whole sequence (their h and c stay 0), so
+ * the gate GEMMs run on the compact set S: inputs [x_t, h_{t-1}[S]], outputs
+ * the four gates of S. Gate order i, f, g, o; W = [W_ih | W_hh]:
+ *   z_t = W[:, :I] x_t + W[:, I:] (m * h_{t-1}) + bias
+ *   c_t = m * (f * c_{t-1} + i * g),  h_t = m * (o * tanh(c_t))
+ * Layouts: X[T][I][B], W[4H][I+H] (dtype), bias[4H] fp32, h0, c0, hT, cT
+ * [H][B], Hs[T][H][B]. h0/c0 NULL = zeros. Dropped rows of Hs, hT, cT are 0.
+ * The workspace carries the compact weights and the saved gates from fwd to
+ * bwd; it must not be modified in between.
+ * bwd: dHs[T][H][B] (derivative of the loss w.r.t. every h_t), dhT and dcT
+ * (extra derivatives of the final state, NULL = 0) -> dX[T][I][B], dW[4H][I+H]
+ * fp32, dbias[4H] fp32, dh0 and dc0 [H][B] (each output may be NULL). Entries
+ * of dropped units are written 0. Only ARD_F32 is supported.
+ */
+typedef struct {
+  int32_t dtype;
+  int32_t seq_len;     /* T >= 1 */
+  int32_t batch;       /* B >= 1 */
+  int32_t input_size;  /* I >= 1 */
+  int32_t hidden_size; /* H >= 1 */
+  int32_t reserved;
+  const ard_row_plan* hidden_plan;  /* n == H, or NULL = no dropout */
+} ard_lstm_desc;
+
+size_t ard_lstm_workspace_bytes(const ard_lstm_desc* desc);
+int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const float* bias,
+                 const void* h0, const void* c0, void* Hs, void* hT, void* cT, void* ws,
+                 size_t ws_bytes, void* stream);
+int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, const void* dhT,
+                 const void* dcT, void* ws, size_t ws_bytes, void* dX, float* dW, float* dbias,
+                 void* dh0, void* dc0, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARD_H */

@@ -1,0 +1,114 @@
+"""ctypes view of the C ABI in include/ard.h (structures and signatures).
+
+Loading fails loudly when libard.so has not been built: there is no fallback.
+"""
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libard.so")
+
+c_i32, c_i64, c_u32, c_u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
+c_f32, c_f64, c_vp, c_size = ctypes.c_float, ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t
+P_i32 = ctypes.POINTER(ctypes.c_int32)
+
+ARD_OK, ARD_ERR_INVALID_ARG, ARD_ERR_UNSUPPORTED, ARD_ERR_HIP, ARD_ERR_NOT_CONVERGED, ARD_ERR_WORKSPACE = range(6)
+ARD_F32, ARD_BF16 = 0, 1
+ARD_SEARCH_PLAIN, ARD_SEARCH_MIRROR = 0, 1
+ARD_ACT_NONE, ARD_ACT_RELU = 0, 1
+ARD_DROPPED_ZERO, ARD_DROPPED_SKIP = 0, 1
+
+
+class ard_search_opts(ctypes.Structure):
+    _fields_ = [("n_max", c_i32), ("mode", c_i32), ("lambda1", c_f64), ("lr", c_f64),
+                ("threshold", c_f64), ("max_iters", c_i64)]
+
+
+class ard_search_info(ctypes.Structure):
+    _fields_ = [("iters", c_i64), ("loss", c_f64), ("p_global", c_f64), ("kkt_residual", c_f64),
+                ("converged", c_i32), ("reserved", c_i32)]
+
+
+class ard_row_pattern(ctypes.Structure):
+    _fields_ = [("period", c_i32), ("offset", c_i32)]
+
+
+class ard_row_plan(ctypes.Structure):
+    _fields_ = [("n", c_i32), ("period", c_i32), ("offset", c_i32), ("kept", c_i32), ("d_idx", c_vp)]
+
+
+class ard_tile_plan(ctypes.Structure):
+    _fields_ = [("n", c_i32), ("k", c_i32), ("tile", c_i32), ("tiles_n", c_i32), ("tiles_k", c_i32),
+                ("nnz", c_i32), ("d_bits", c_vp), ("d_row_ptr", c_vp), ("d_row_cols", c_vp),
+                ("d_col_ptr", c_vp), ("d_col_rows", c_vp), ("d_flat", c_vp)]
+
+
+class ard_fc_desc(ctypes.Structure):
+    _fields_ = [("dtype", c_i32), ("batch", c_i32), ("in_features", c_i32), ("out_features", c_i32),
+                ("in_plan", ctypes.POINTER(ard_row_plan)), ("out_plan", ctypes.POINTER(ard_row_plan)),
+                ("scale", c_f32), ("act", c_i32), ("dropped", c_i32), ("reserved", c_i32)]
+
+
+class ard_tile_desc(ctypes.Structure):
+    _fields_ = [("dtype", c_i32), ("batch", c_i32), ("in_features", c_i32), ("out_features", c_i32),
+                ("scale", c_f32), ("dropped", c_i32)]
+
+
+class ard_lstm_desc(ctypes.Structure):
+    _fields_ = [("dtype", c_i32), ("seq_len", c_i32), ("batch", c_i32), ("input_size", c_i32),
+                ("hidden_size", c_i32), ("reserved", c_i32),
+                ("hidden_plan", ctypes.POINTER(ard_row_plan))]
+
+
+# name -> (restype, argtypes); every symbol the header declares.
+SIGNATURES = {
+    "ard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "ard_last_error": (ctypes.c_char_p, []),
+    "ard_version": (ctypes.c_int, []),
+    "ard_search_opts_default": (None, [ctypes.POINTER(ard_search_opts)]),
+    "ard_search_distribution": (ctypes.c_int, [c_f64, ctypes.POINTER(ard_search_opts),
+                                               ctypes.POINTER(c_f64), ctypes.POINTER(ard_search_info)]),
+    "ard_sample_row_pattern": (ctypes.c_int, [ctypes.POINTER(c_f64), c_i32, c_u64, c_u32, c_u64,
+                                              ctypes.POINTER(ard_row_pattern)]),
+    "ard_row_kept": (c_i32, [c_i32, c_i32, c_i32]),
+    "ard_tile_bitmap_tdp": (ctypes.c_int, [c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_u32)]),
+    "ard_tile_bitmap_bernoulli": (ctypes.c_int, [c_i32, c_i32, c_f64, c_u64, c_u32, c_u64,
+                                                 ctypes.POINTER(c_u32)]),
+    "ard_bitmap_popcount": (c_i32, [ctypes.POINTER(c_u32), c_i32]),
+    "ard_plan_rows": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, ctypes.POINTER(ard_row_plan), c_vp]),
+    "ard_tile_plan_workspace_bytes": (c_size, [c_i32, c_i32]),
+    "ard_plan_tiles": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, c_i32, c_vp, c_size,
+                                      ctypes.POINTER(ard_tile_plan), c_vp]),
+    "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "ard_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
+                                    c_vp, c_vp, c_vp, c_vp]),
+    "ard_tile_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
+                                         c_vp, c_vp, c_vp, c_vp]),
+    "ard_tile_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
+                                           c_vp, c_vp, c_vp, c_vp]),
+    "ard_lstm_workspace_bytes": (c_size, [ctypes.POINTER(ard_lstm_desc)]),
+    "ard_lstm_fwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_desc), c_vp, c_vp, c_vp, c_vp, c_vp,
+                                    c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "ard_lstm_bwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_desc), c_vp, c_vp, c_vp, c_vp, c_vp,
+                                    c_size, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded libard.so with every signature applied. Raises if not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+                               "(python -m paper_1805_08939_amd.build)")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib

@@ -1,0 +1,277 @@
+// Row-pattern compaction and the fully connected layer under row-based
+// dropout patterns (Sec. III-A), fwd / bwd_data / bwd_weight.
+//
+// The compact problem of each pass is handed to the gathered GEMM: kept output
+// neurons select rows of W and of the output, kept input neurons select rows
+// of the activations and columns of W. With feature-major activations every
+// neuron gather is a whole contiguous row.
+
+#include <hip/hip_runtime.h>
+
+#include "ard_gemm.hpp"
+#include "ard_internal.hpp"
+
+namespace ard {
+
+// d_idx[i] = offset + period * i for i < kept: the ascending kept list.
+__global__ void plan_rows_kernel(int32_t* __restrict__ idx, int32_t kept, int32_t period,
+                                 int32_t offset) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < kept) idx[i] = offset + period * i;
+}
+
+// ZERO mode: writes 0 to every row r of out[rows][cols] with r % period != offset.
+template <typename T>
+__global__ void zero_dropped_rows_kernel(T* __restrict__ out, int64_t ld, int32_t cols,
+                                         int32_t period, int32_t offset) {
+  const int r = blockIdx.x;
+  if (r % period == offset) return;
+  T* row = out + r * ld;
+  for (int c = threadIdx.x; c < cols; c += blockDim.x) row[c] = static_cast<T>(0.0f);
+}
+
+// ZERO mode for the weight gradient dW[N][K]: 0 wherever the output row or
+// the input column is dropped.
+__global__ void zero_dropped_weights_kernel(float* __restrict__ dW, int32_t K, int32_t out_period,
+                                            int32_t out_offset, int32_t in_period,
+                                            int32_t in_offset) {
+  const int r = blockIdx.x;
+  float* row = dW + static_cast<int64_t>(r) * K;
+  const bool row_kept = (r % out_period) == out_offset;
+  for (int c = threadIdx.x; c < K; c += blockDim.x)
+    if (!row_kept || (c % in_period) != in_offset) row[c] = 0.0f;
+}
+
+// dbias[idx[i]] = sum_b G[idx[i]][b] with G = scale * dY * [Y > 0] (or
+// scale * dY); one block per kept row, fixed-order reduction.
+template <typename T>
+__global__ void __launch_bounds__(256) dbias_kernel(const T* __restrict__ dYt,
+                                                    const T* __restrict__ Yt, int32_t B,
+                                                    const int32_t* __restrict__ idx, float scale,
+                                                    int32_t relu, float* __restrict__ dbias) {
+  __shared__ float part[256];
+  const int64_t row = idx ? idx[blockIdx.x] : blockIdx.x;
+  const T* dy = dYt + row * B;
+  const T* y = Yt ? Yt + row * B : nullptr;
+  float s = 0.0f;
+  for (int b = threadIdx.x; b < B; b += 256) {
+    float g = to_f32(dy[b]);
+    if (relu && !(to_f32(y[b]) > 0.0f)) g = 0.0f;
+    s += g;
+  }
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dbias[row] = scale * part[0];
+}
+
+namespace {
+
+struct FcShape {
+  int32_t B, K, N;
+  int32_t kin, kout;                 // kept counts
+  const int32_t* in_idx;             // NULL when every input is kept
+  const int32_t* out_idx;            // NULL when every output is kept
+  int32_t in_period, in_offset, out_period, out_offset;
+  size_t esize;
+};
+
+int check_desc(const ard_fc_desc* d, FcShape* s) {
+  if (!d) return fail(ARD_ERR_INVALID_ARG, "desc is NULL");
+  if (d->dtype != ARD_F32 && d->dtype != ARD_BF16)
+    return fail(ARD_ERR_UNSUPPORTED, "dtype %d not supported", d->dtype);
+  if (d->batch < 1 || d->in_features < 1 || d->out_features < 1)
+    return fail(ARD_ERR_INVALID_ARG, "sizes must be >= 1 (batch %d, in %d, out %d)", d->batch,
+                d->in_features, d->out_features);
+  if (d->act != ARD_ACT_NONE && d->act != ARD_ACT_RELU)
+    return fail(ARD_ERR_INVALID_ARG, "unknown activation %d", d->act);
+  if (d->dropped != ARD_DROPPED_ZERO && d->dropped != ARD_DROPPED_SKIP)
+    return fail(ARD_ERR_INVALID_ARG, "unknown dropped-output mode %d", d->dropped);
+  if (!(d->scale == d->scale) || d->scale == __builtin_inff() || d->scale == -__builtin_inff())
+    return fail(ARD_ERR_INVALID_ARG, "scale must be finite");
+  int st = check_row_plan(d->in_plan, d->in_features, "in_plan");
+  if (st != ARD_OK) return st;
+  st = check_row_plan(d->out_plan, d->out_features, "out_plan");
+  if (st != ARD_OK) return st;
+  s->B = d->batch;
+  s->K = d->in_features;
+  s->N = d->out_features;
+  const bool in_all = !d->in_plan || d->in_plan->period == 1;
+  const bool out_all = !d->out_plan || d->out_plan->period == 1;
+  s->kin = in_all ? s->K : d->in_plan->kept;
+  s->kout = out_all ? s->N : d->out_plan->kept;
+  s->in_idx = in_all ? nullptr : d->in_plan->d_idx;
+  s->out_idx = out_all ? nullptr : d->out_plan->d_idx;
+  s->in_period = in_all ? 1 : d->in_plan->period;
+  s->in_offset = in_all ? 0 : d->in_plan->offset;
+  s->out_period = out_all ? 1 : d->out_plan->period;
+  s->out_offset = out_all ? 0 : d->out_plan->offset;
+  s->esize = d->dtype == ARD_BF16 ? 2 : 4;
+  return ARD_OK;
+}
+
+int check_ptr(const void* p, const char* name) {
+  if (!p) return fail(ARD_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(p)) return fail(ARD_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return ARD_OK;
+}
+
+// Rows of `ld` elements start 16-byte aligned.
+inline bool vec_rows(int64_t ld, size_t esize) { return (ld * static_cast<int64_t>(esize)) % 16 == 0; }
+
+template <typename T>
+int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* W,
+                const float* bias, void* Yt, hipStream_t stream) {
+  GemmArgs g = {};
+  g.M = s.kout;
+  g.N = s.B;
+  g.K = s.kin;
+  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f};
+  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f};
+  g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
+  const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
+  const bool b_vec = vec_rows(s.B, sizeof(T));
+  ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+      g, 1, a_vec, b_vec, stream)));
+  if (d->dropped == ARD_DROPPED_ZERO && s.out_period > 1) {
+    hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.N), dim3(256), 0, stream,
+                       static_cast<T*>(Yt), static_cast<int64_t>(s.B), s.B, s.out_period,
+                       s.out_offset);
+    ARD_LAUNCH_CHECK();
+  }
+  return ARD_OK;
+}
+
+template <typename T>
+int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
+                     const void* W, void* dXt, hipStream_t stream) {
+  GemmArgs g = {};
+  g.M = s.kin;
+  g.N = s.B;
+  g.K = s.kout;
+  // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
+  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f};
+  // B(t, n) = G[out(t)][n], gated by the stored forward output.
+  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, d->scale};
+  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, 1.0f};
+  const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
+  const bool b_vec = vec_rows(s.B, sizeof(T));
+  ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_STORE>(
+      g, 1, a_vec, b_vec, stream)));
+  if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
+    hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
+                       static_cast<T*>(dXt), static_cast<int64_t>(s.B), s.B, s.in_period,
+                       s.in_offset);
+    ARD_LAUNCH_CHECK();
+  }
+  return ARD_OK;
+}
+
+template <typename T>
+int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
+                       const void* Yt, float* dW, float* dbias, hipStream_t stream) {
+  GemmArgs g = {};
+  g.M = s.kout;
+  g.N = s.kin;
+  g.K = s.B;
+  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, d->scale};
+  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f};
+  g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, 1.0f};
+  const bool v = vec_rows(s.B, sizeof(T));
+  ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_STORE>(
+      g, 1, v, v, stream)));
+  if (dbias && s.kout > 0) {
+    hipLaunchKernelGGL(dbias_kernel<T>, dim3(s.kout), dim3(256), 0, stream,
+                       static_cast<const T*>(dYt), static_cast<const T*>(Yt), s.B, s.out_idx,
+                       d->scale, d->act == ARD_ACT_RELU ? 1 : 0, dbias);
+    ARD_LAUNCH_CHECK();
+  }
+  if (d->dropped == ARD_DROPPED_ZERO && (s.out_period > 1 || s.in_period > 1)) {
+    hipLaunchKernelGGL(zero_dropped_weights_kernel, dim3(s.N), dim3(256), 0, stream, dW, s.K,
+                       s.out_period, s.out_offset, s.in_period, s.in_offset);
+    ARD_LAUNCH_CHECK();
+    if (dbias && s.out_period > 1) {
+      hipLaunchKernelGGL(zero_dropped_rows_kernel<float>, dim3(s.N), dim3(64), 0, stream, dbias,
+                         static_cast<int64_t>(1), 1, s.out_period, s.out_offset);
+      ARD_LAUNCH_CHECK();
+    }
+  }
+  return ARD_OK;
+}
+
+}  // namespace
+}  // namespace ard
+
+using namespace ard;
+
+extern "C" {
+
+int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard_row_plan* plan,
+                  void* stream) {
+  clear_error();
+  if (!plan) return fail(ARD_ERR_INVALID_ARG, "plan is NULL");
+  if (n < 1) return fail(ARD_ERR_INVALID_ARG, "n must be >= 1");
+  if (period < 1 || offset < 0 || offset >= period)
+    return fail(ARD_ERR_INVALID_ARG, "invalid pattern (period %d, offset %d)", period, offset);
+  const int32_t kept = kept_count(n, period, offset);
+  if (kept > 0 && !d_idx) return fail(ARD_ERR_INVALID_ARG, "d_idx is NULL");
+  plan->n = n;
+  plan->period = period;
+  plan->offset = offset;
+  plan->kept = kept;
+  plan->d_idx = d_idx;
+  if (kept > 0) {
+    hipLaunchKernelGGL(plan_rows_kernel, dim3((kept + 255) / 256), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), d_idx, kept, period, offset);
+    ARD_LAUNCH_CHECK();
+  }
+  return ARD_OK;
+}
+
+int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias, void* Yt,
+               void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(W, "W")) || (st = check_ptr(Yt, "Yt")))
+    return st;
+  if (bias && !aligned16(bias)) return fail(ARD_ERR_INVALID_ARG, "bias is not 16-byte aligned");
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) return fc_fwd_impl<bf16>(desc, s, Xt, W, bias, Yt, sm);
+  return fc_fwd_impl<float>(desc, s, Xt, W, bias, Yt, sm);
+}
+
+int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
+                    void* dXt, void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(dYt, "dYt")) || (st = check_ptr(W, "W")) || (st = check_ptr(dXt, "dXt")))
+    return st;
+  if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, sm);
+  return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, sm);
+}
+
+int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
+                      float* dW, float* dbias, void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(dYt, "dYt")) || (st = check_ptr(dW, "dW")))
+    return st;
+  if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
+  if (dbias && !aligned16(dbias)) return fail(ARD_ERR_INVALID_ARG, "dbias is not 16-byte aligned");
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) return fc_bwd_weight_impl<bf16>(desc, s, Xt, dYt, Yt, dW, dbias, sm);
+  return fc_bwd_weight_impl<float>(desc, s, Xt, dYt, Yt, dW, dbias, sm);
+}
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+"""Helpers for the GPU parity tests (imported only by tests marked gpu)."""
+import numpy as np
+import torch
+
+from oracle import patterns as opat
+from paper_1805_08939_amd import api, synth
+
+F32_TOL = 1e-4   # max relative error, fp32 paths
+BF16_TOL = 2e-2  # max relative error, bf16 paths (fp32 accumulation)
+
+
+def device():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    return torch.device("cuda:0")
+
+
+def tol(dtype_name):
+    return F32_TOL if dtype_name == "f32" else BF16_TOL
+
+
+def ard_dtype(dtype_name):
+    return api.ARD_F32 if dtype_name == "f32" else api.ARD_BF16
+
+
+def row_plan(n, period, offset, check=True):
+    """Builds a row plan on the device; checks its list against the oracle."""
+    kept = opat.row_kept_count(n, period, offset)
+    idx = torch.full((max(kept, 1),), -1, dtype=torch.int32, device=device())
+    plan = api.ard_plan_rows(n, period, offset, idx)
+    if check:
+        torch.cuda.synchronize()
+        assert plan.kept == kept
+        assert idx[:kept].cpu().tolist() == opat.row_kept_list(n, period, offset)
+    return plan
+
+
+def to_dev(t):
+    return t.contiguous().to(device())
+
+
+def f64(t):
+    return synth.as_f64(t).numpy()
+
+
+def compare(got, want, norm, rel_tol, what):
+    """Componentwise check |got - want| <= rel_tol * norm, where norm is the
+    GEMM error normaliser (|A| |B| of the masked operands, plus |bias|). Where
+    norm is 0 the result must be exactly 0. Also checks the normwise error
+    max|got - want| / max|want|. Returns (componentwise, normwise) errors."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    norm = np.asarray(norm, dtype=np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    assert np.isfinite(got).all(), f"{what}: non-finite values"
+    diff = np.abs(got - want)
+    zero = norm == 0.0
+    assert not diff[zero].any(), f"{what}: nonzero where the exact result is 0"
+    comp = float((diff[~zero] / norm[~zero]).max()) if (~zero).any() else 0.0
+    scale = float(np.abs(want).max())
+    normwise = float(diff.max() / scale) if scale > 0 else float(diff.max())
+    assert comp <= rel_tol, f"{what}: componentwise error {comp:.3e} > {rel_tol}"
+    assert normwise <= rel_tol, f"{what}: normwise error {normwise:.3e} > {rel_tol}"
+    return comp, normwise

@@ -1,0 +1,163 @@
+"""GPU parity of the FC layer under row patterns (fwd / bwd_data / bwd_weight)
+against the fp64 oracle, through the C ABI."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import compare, device, f64, row_plan, to_dev, tol, ard_dtype
+from oracle import fc as ofc
+from oracle import patterns as opat
+from oracle import prng as oprng
+from paper_1805_08939_amd import api, synth
+
+pytestmark = pytest.mark.gpu
+
+ACTS = {"none": api.ARD_ACT_NONE, "relu": api.ARD_ACT_RELU}
+
+
+def make_inputs(dtype, B, K, N, seed, w_std=0.05, bias=True):
+    g = synth.generator(seed)
+    X = synth.to_storage(synth.normal(g, (B, K)), dtype)
+    W = synth.to_storage(synth.normal(g, (N, K), w_std), dtype)
+    b = synth.normal(g, (N,), 0.1) if bias else None
+    dY = synth.to_storage(synth.normal(g, (B, N)), dtype)
+    return X, W, b, dY
+
+
+def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans=True,
+              sentinel=None, poison=False):
+    """Runs fwd, bwd_data and bwd_weight on the GPU and checks each against the
+    oracle. Returns the GPU outputs."""
+    B, K = X.shape
+    N = W.shape[0]
+    m_in, m_out = opat.row_mask(K, *pin), opat.row_mask(N, *pout)
+    b64 = f64(b) if b is not None else None
+    Y64 = ofc.fc_forward(f64(X), f64(W), b64, m_in, m_out, scale, act)
+    # the stored forward output feeds both sides' ReLU gate
+    Ys = synth.to_storage(torch.from_numpy(Y64).float(), dtype)
+    dX64, dW64, db64 = ofc.fc_backward(f64(X), f64(W), f64(Ys), f64(dY), m_in, m_out, scale, act)
+
+    in_plan = None if (use_null_plans and pin == (1, 0)) else row_plan(K, *pin)
+    out_plan = None if (use_null_plans and pout == (1, 0)) else row_plan(N, *pout)
+    desc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped)
+
+    Xt, Wd, dYt, Yst = to_dev(X.T), to_dev(W), to_dev(dY.T), to_dev(Ys.T)
+    if poison:  # dropped data must never enter the arithmetic
+        Xt[torch.from_numpy(m_in == 0).to(device())] = float("nan")
+        Wd[torch.from_numpy(m_out == 0).to(device())] = float("nan")
+        Wd[:, torch.from_numpy(m_in == 0).to(device())] = float("nan")
+        dYt[torch.from_numpy(m_out == 0).to(device())] = float("nan")
+        Yst[torch.from_numpy(m_out == 0).to(device())] = float("nan")
+    bd = to_dev(b) if b is not None else None
+    sdt = synth.storage_dtype(dtype)
+    fill = 0.0 if sentinel is None else sentinel
+    Yt = torch.full((N, B), fill, dtype=sdt, device=device())
+    dXt = torch.full((K, B), fill, dtype=sdt, device=device())
+    dW = torch.full((N, K), fill, dtype=torch.float32, device=device())
+    db = torch.full((N,), fill, dtype=torch.float32, device=device())
+
+    api.ard_fc_fwd(desc, Xt, Wd, bd, Yt)
+    api.ard_fc_bwd_data(desc, dYt, Yst, Wd, dXt)
+    api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dW, db)
+    torch.cuda.synchronize()
+
+    Xa, Wa = np.abs(f64(X) * m_in[None, :]), np.abs(f64(W))
+    G = ofc.fc_output_grad(f64(Ys), f64(dY), m_out, scale, act)
+    nY = abs(scale) * (Xa @ Wa.T + (np.abs(b64)[None, :] if b64 is not None else 0.0)) * m_out[None, :]
+    ndX = (np.abs(G) @ Wa) * m_in[None, :]
+    ndW = (np.abs(G).T @ Xa) * np.outer(m_out, m_in)
+    ndb = np.abs(G).sum(0)
+    t = tol(dtype)
+    got = {"Y": f64(Yt).T, "dX": f64(dXt).T, "dW": f64(dW), "db": f64(db)}
+    keep = {"Y": np.broadcast_to(m_out[None, :] > 0, Y64.shape),
+            "dX": np.broadcast_to(m_in[None, :] > 0, dX64.shape),
+            "dW": np.outer(m_out, m_in) > 0, "db": m_out > 0}
+    want = {"Y": Y64, "dX": dX64, "dW": dW64, "db": db64}
+    norm = {"Y": nY, "dX": ndX, "dW": ndW, "db": ndb}
+    for k in got:
+        if dropped == api.ARD_DROPPED_SKIP:
+            # untouched: bit-identical sentinel outside the kept sets
+            assert (got[k][~keep[k]] == fill).all(), f"{k}: dropped entries were written"
+            compare(got[k][keep[k]], want[k][keep[k]], norm[k][keep[k]], t, k)
+        else:
+            compare(got[k], want[k], norm[k], t, k)
+    return Yt, dXt, dW, db
+
+
+PATTERNS = [(1, 0), (2, 0), (2, 1), (3, 2), (5, 1), (16, 9), (40, 39)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_tiny_all_pattern_pairs(dtype):
+    X, W, b, dY = make_inputs(dtype, 5, 13, 11, seed=1805)
+    for pin, pout in itertools.product(PATTERNS, repeat=2):
+        for act in ("none", "relu"):
+            run_layer(dtype, X, W, b, dY, pin, pout, act, 1.0 / 0.7, api.ARD_DROPPED_ZERO)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(200, 300, 260), (130, 1000, 70), (64, 96, 520), (8, 4104, 36)])
+def test_multi_tile_ragged(dtype, shape):
+    B, K, N = shape
+    X, W, b, dY = make_inputs(dtype, B, K, N, seed=sum(shape))
+    for pin, pout, act in [((3, 1), (2, 0), "relu"), ((1, 0), (5, 4), "none"),
+                           ((4, 2), (1, 0), "relu"), ((7, 0), (3, 1), "none")]:
+        run_layer(dtype, X, W, b, dY, pin, pout, act, 1.25, api.ARD_DROPPED_ZERO,
+                  use_null_plans=False)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_skip_mode_leaves_dropped_entries_untouched(dtype):
+    X, W, b, dY = make_inputs(dtype, 96, 160, 144, seed=7)
+    run_layer(dtype, X, W, b, dY, (3, 0), (2, 1), "relu", 2.0, api.ARD_DROPPED_SKIP, sentinel=-7.5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dropped_data_never_enter_the_arithmetic(dtype):
+    X, W, b, dY = make_inputs(dtype, 80, 192, 176, seed=11)
+    run_layer(dtype, X, W, b, dY, (4, 3), (3, 1), "relu", 1.0, api.ARD_DROPPED_ZERO, poison=True)
+    run_layer(dtype, X, W, b, dY, (2, 0), (5, 2), "none", 1.0, api.ARD_DROPPED_SKIP, poison=True,
+              sentinel=3.0)
+
+
+def test_single_fc_layer_fp32_full_config():
+    """Single FC layer fp32: X[64x784] ~ N(0,1), W (512 outputs x 784) ~ N(0, 0.05^2),
+    row dropout of the 512 outputs with period 2 and a seeded offset, dY ~ N(0,1)."""
+    X, W, _, dY = make_inputs("f32", 64, 784, 512, seed=1805, w_std=0.05, bias=False)
+    K2 = np.zeros(16)
+    K2[1] = 1.0
+    per, off = oprng.sample_row_pattern(K2, 8939, 0, 0)
+    assert per == 2
+    run_layer("f32", X, W, None, dY, (1, 0), (per, off), "none", 1.0, api.ARD_DROPPED_ZERO)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bitwise_deterministic(dtype):
+    X, W, b, dY = make_inputs(dtype, 256, 384, 320, seed=3)
+    r1 = run_layer(dtype, X, W, b, dY, (3, 2), (2, 0), "relu", 1.0, api.ARD_DROPPED_ZERO)
+    r2 = run_layer(dtype, X, W, b, dY, (3, 2), (2, 0), "relu", 1.0, api.ARD_DROPPED_ZERO)
+    for a, c in zip(r1, r2):
+        assert torch.equal(a, c)
+
+
+def test_invalid_arguments_are_rejected_before_launch():
+    d = device()
+    X = torch.zeros(16, 8, device=d)
+    W = torch.zeros(8, 16, device=d)
+    Y = torch.zeros(8, 8, device=d)
+    plan_bad = row_plan(10, 2, 1)  # covers 10 neurons, the layer has 8 outputs
+    for desc in (api.fc_desc(api.ARD_F32, 0, 16, 8), api.fc_desc(7, 8, 16, 8),
+                 api.fc_desc(api.ARD_F32, 8, 16, 8, out_plan=plan_bad),
+                 api.fc_desc(api.ARD_F32, 8, 16, 8, act=5),
+                 api.fc_desc(api.ARD_F32, 8, 16, 8, scale=float("inf"))):
+        with pytest.raises(api.ArdError):
+            api.ard_fc_fwd(desc, X, W, None, Y)
+    good = api.fc_desc(api.ARD_F32, 8, 16, 8)
+    with pytest.raises(api.ArdError):
+        api.ard_fc_fwd(good, None, W, None, Y)
+    with pytest.raises(api.ArdError):
+        api.ard_fc_fwd(good, X[:, 1:].contiguous().view(-1)[1:], W, None, Y)  # misaligned
+    with pytest.raises(api.ArdError):
+        api.ard_fc_bwd_data(api.fc_desc(api.ARD_F32, 8, 16, 8, act=api.ARD_ACT_RELU), Y, None, W, X)
