@@ -154,12 +154,13 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
   g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f};
-  // B(t, n) = G[out(t)][n], gated by the stored forward output.
-  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, d->scale};
-  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, 1.0f};
+  // B(t, n) = dY[out(t)][n] * [Y > 0]: the 0/1 gate keeps bf16 operands exact;
+  // scale is applied to the fp32 accumulators in the epilogue.
+  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f};
+  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale};
   const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_STORE>(
+  ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
       g, 1, a_vec, b_vec, stream)));
   if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
     hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
@@ -177,11 +178,11 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.M = s.kout;
   g.N = s.kin;
   g.K = s.B;
-  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, d->scale};
+  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f};
   g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f};
-  g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, 1.0f};
+  g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
   const bool v = vec_rows(s.B, sizeof(T));
-  ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_STORE>(
+  ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
       g, 1, v, v, stream)));
   if (dbias && s.kout > 0) {
     hipLaunchKernelGGL(dbias_kernel<T>, dim3(s.kout), dim3(256), 0, stream,

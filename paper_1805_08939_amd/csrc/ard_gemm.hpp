@@ -60,7 +60,8 @@ struct GemmOutput {
   int64_t bstride;
   const float* bias;     // EPI_FWD: bias[ridx(m)], may be NULL
   int32_t relu;          // EPI_FWD: apply ReLU
-  float scale;           // EPI_FWD: multiply after the activation
+  float scale;           // EPI_FWD: multiply after the activation (also the
+                         // dropout scale of the backward passes)
 };
 
 struct GemmArgs {

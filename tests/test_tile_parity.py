@@ -1,0 +1,146 @@
+"""GPU parity of the tile-pattern layer (Sec. III-B) and its plan lists."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import compare, device, f64, to_dev, tol, ard_dtype
+from oracle import patterns as opat
+from oracle import prng as oprng
+from oracle import tdp as otdp
+from paper_1805_08939_amd import api, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def tile_plan(n, k, tile, words, check=True):
+    tn, tk = n // tile, k // tile
+    bits = torch.tensor(np.array(words, dtype=np.uint32).view(np.int32), device=device())
+    nnz = opat.bitmap_popcount(words, tn * tk)
+    ws = torch.zeros(api.ard_tile_plan_workspace_bytes(tn, tk) // 4, dtype=torch.int32, device=device())
+    plan = api.ard_plan_tiles(n, k, tile, bits, nnz, ws)
+    if check:
+        torch.cuda.synchronize()
+        L = opat.tile_lists(words, tn, tk)
+
+        def arr(ptr, count):
+            base = ptr - ws.data_ptr()
+            return ws[base // 4: base // 4 + count].cpu().tolist()
+
+        assert arr(plan.d_row_ptr, tn + 1) == L["row_ptr"]
+        assert arr(plan.d_col_ptr, tk + 1) == L["col_ptr"]
+        assert arr(plan.d_row_cols, nnz) == L["row_cols"]
+        assert arr(plan.d_col_rows, nnz) == L["col_rows"]
+        assert arr(plan.d_flat, nnz) == L["flat"]
+    return plan
+
+
+def run_tile(dtype, B, N, K, tile, words, scale=1.0, dropped=api.ARD_DROPPED_ZERO, seed=0,
+             sentinel=0.0, poison=False):
+    g = synth.generator(seed)
+    X = synth.to_storage(synth.normal(g, (B, K)), dtype)
+    W = synth.to_storage(synth.normal(g, (N, K), 0.02), dtype)
+    dY = synth.to_storage(synth.normal(g, (B, N)), dtype)
+    tn, tk = N // tile, K // tile
+    M = opat.tile_mask(words, tn, tk, tile)
+    Y64 = otdp.tdp_forward(f64(X), f64(W), M, scale)
+    dX64, dW64 = otdp.tdp_backward(f64(X), f64(W), f64(dY), M, scale)
+    plan = tile_plan(N, K, tile, words)
+    desc = api.tile_desc(ard_dtype(dtype), B, K, N, scale, dropped)
+    Xt, Wd, dYt = to_dev(X.T), to_dev(W), to_dev(dY.T)
+    if poison:
+        Wd[torch.from_numpy(M == 0).to(device())] = float("nan")
+    sdt = synth.storage_dtype(dtype)
+    Yt = torch.full((N, B), 5.0, dtype=sdt, device=device())
+    dXt = torch.full((K, B), 5.0, dtype=sdt, device=device())
+    dW = torch.full((N, K), sentinel, dtype=torch.float32, device=device())
+    api.ard_tile_fwd(desc, plan, Xt, Wd, Yt)
+    api.ard_tile_bwd_data(desc, plan, dYt, Wd, dXt)
+    api.ard_tile_bwd_weight(desc, plan, Xt, dYt, dW)
+    torch.cuda.synchronize()
+    Xa, Wm, dYa = np.abs(f64(X)), np.abs(f64(W)) * M, np.abs(f64(dY))
+    t = tol(dtype)
+    compare(f64(Yt).T, Y64, abs(scale) * Xa @ Wm.T, t, "Y")
+    compare(f64(dXt).T, dX64, abs(scale) * dYa @ Wm, t, "dX")
+    ndW = abs(scale) * M * (dYa.T @ Xa)
+    dWg = f64(dW)
+    if dropped == api.ARD_DROPPED_SKIP:
+        assert (dWg[M == 0] == sentinel).all()
+        compare(dWg[M > 0], dW64[M > 0], ndW[M > 0], t, "dW")
+    else:
+        compare(dWg, dW64, ndW, t, "dW")
+    return Yt, dXt, dW
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tile", [32, 64])
+def test_tdp_and_bernoulli_patterns(dtype, tile):
+    N, K, B = 4 * tile, 6 * tile, 72
+    tn, tk = N // tile, K // tile
+    for words in (oprng.tile_bitmap_tdp(tn, tk, 4, 1), oprng.tile_bitmap_tdp(tn, tk, 3, 2),
+                  oprng.tile_bitmap_bernoulli(tn, tk, 0.5, 8939, 0, 0),
+                  oprng.tile_bitmap_tdp(tn, tk, 1, 0), oprng.tile_bitmap_bernoulli(tn, tk, 1.0, 1, 0, 0)):
+        run_tile(dtype, B, N, K, tile, words, scale=1.5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ragged_batch_and_skip(dtype):
+    words = oprng.tile_bitmap_bernoulli(3, 5, 0.4, 3, 1, 2)
+    run_tile(dtype, 131, 3 * 64, 5 * 64, 64, words, dropped=api.ARD_DROPPED_SKIP, sentinel=-2.0)
+    run_tile(dtype, 12, 3 * 64, 5 * 64, 64, words)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dropped_tiles_never_read(dtype):
+    words = oprng.tile_bitmap_bernoulli(4, 4, 0.5, 8, 0, 0)
+    run_tile(dtype, 64, 256, 256, 64, words, poison=True)
+
+
+def test_full_config_bf16_4096():
+    """One 4096x4096 layer, batch 512, bf16, 64x64 tiles kept by a seeded
+    Bernoulli bitmap at p = 0.5: sampled output rows against the oracle."""
+    B, N, K, tile = 512, 4096, 4096, 64
+    words = oprng.tile_bitmap_bernoulli(64, 64, 0.5, 8939, 0, 0)
+    g = synth.generator(1805 + 2)
+    X = synth.to_storage(synth.normal(g, (B, K)), "bf16")
+    W = synth.to_storage(synth.normal(g, (N, K), 0.02), "bf16")
+    dY = synth.to_storage(synth.normal(g, (B, N)), "bf16")
+    plan = tile_plan(N, K, tile, words)
+    desc = api.tile_desc(api.ARD_BF16, B, K, N)
+    Xt, Wd, dYt = to_dev(X.T), to_dev(W), to_dev(dY.T)
+    Yt = torch.empty(N, B, dtype=torch.bfloat16, device=device())
+    dXt = torch.empty(K, B, dtype=torch.bfloat16, device=device())
+    dW = torch.empty(N, K, dtype=torch.float32, device=device())
+    api.ard_tile_fwd(desc, plan, Xt, Wd, Yt)
+    api.ard_tile_bwd_data(desc, plan, dYt, Wd, dXt)
+    api.ard_tile_bwd_weight(desc, plan, Xt, dYt, dW)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(N, 48, replace=False))
+    cols = np.sort(rng.choice(K, 48, replace=False))
+    grid = opat.bitmap_to_grid(words, 64, 64).astype(np.float64)
+    M_rows = np.kron(grid, np.ones((1, tile)))[rows // tile]      # mask rows `rows`: [48][K]
+    M_cols = np.kron(grid, np.ones((tile, 1)))[:, cols // tile]   # mask columns `cols`: [N][48]
+    Xf, Wf, dYf = f64(X), f64(W), f64(dY)
+    # Y columns (= output features) `rows`: Y[:, n] = X (W[n] * M[n])^T
+    Wr = Wf[rows] * M_rows
+    compare(f64(Yt)[rows].T, Xf @ Wr.T, np.abs(Xf) @ np.abs(Wr).T, 2e-2, "Y")
+    Wc = Wf[:, cols] * M_cols
+    compare(f64(dXt)[cols].T, dYf @ Wc, np.abs(dYf) @ np.abs(Wc), 2e-2, "dX")
+    sub = M_rows[:, cols]
+    want = sub * (dYf[:, rows].T @ Xf[:, cols])
+    compare(f64(dW)[np.ix_(rows, cols)], want, sub * (np.abs(dYf[:, rows]).T @ np.abs(Xf[:, cols])),
+            2e-2, "dW")
+
+
+def test_plan_validation():
+    words = oprng.tile_bitmap_tdp(2, 2, 2, 0)
+    bits = torch.tensor(np.array(words, dtype=np.uint32).view(np.int32), device=device())
+    ws = torch.zeros(api.ard_tile_plan_workspace_bytes(2, 2) // 4, dtype=torch.int32, device=device())
+    with pytest.raises(api.ArdError):
+        api.ard_plan_tiles(128, 128, 48, bits, 2, ws)      # tile size
+    with pytest.raises(api.ArdError):
+        api.ard_plan_tiles(100, 128, 64, bits, 2, ws)      # not a tile multiple
+    with pytest.raises(api.ArdError):
+        api.ard_plan_tiles(128, 128, 64, bits, 5, ws)      # nnz out of range
+    with pytest.raises(api.ArdError):
+        api.ard_plan_tiles(128, 128, 64, bits, 2, ws[:4])  # workspace too small
