@@ -1,0 +1,299 @@
+#!/usr/bin/env python3
+"""Benchmark of the Approximate Random Dropout hot path on one MI355X.
+
+Default workload: the paper's MLP 784-2048-2048-10 (fp32, batch 128, ReLU)
+with row-based dropout on both hidden layers. Each step samples a fresh
+pattern per hidden layer from the distribution K searched for p, compacts it
+on the device, and runs fwd, bwd_data and bwd_weight of all three layers
+(bwd_data of the first layer is not needed). The headline value is TFLOP/s
+counted on the work actually kept, at p = 0.5; the same steps at p = 0.3 and
+0.7 and at p = 0 (period 1: the same kernels with nothing dropped) give the
+speedups. Other workloads (--workload) are the single wide MLP layer set, the
+tile-pattern layer and the LSTM.
+
+Prints one JSON line. Inputs are synthetic and resident in HBM before timing.
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd layer TFLOP/s (kept work) & speedup vs p=0 at p=0.3/0.5/0.7"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # MI355X dense matrix peaks
+PEAK_HBM_GBS = 8000.0
+PATTERN_SEED = 8939
+
+
+class Mlp:
+    """An MLP whose hidden layers take row-based dropout patterns sampled per
+    step from K(p). Layers are FC: Xt[K][B] -> Yt[N][B]."""
+
+    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.dims, self.B, self.dtype = name, dims, batch, dtype
+        self.ard_dtype = api.ARD_F32 if dtype == "f32" else api.ARD_BF16
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        sdt = synth.storage_dtype(dtype)
+        L = len(dims) - 1
+        self.L = L
+        self.X0 = synth.to_storage(synth.normal(g, (dims[0], batch)), dtype).to(dev)
+        self.W = []
+        for l in range(L):
+            w = synth.xavier(g, dims[l + 1], dims[l]) if init == "xavier" else synth.he(g, dims[l + 1], dims[l])
+            self.W.append(synth.to_storage(w, dtype).to(dev))
+        self.bias = [torch.zeros(dims[l + 1], device=dev) for l in range(L)]
+        self.Y = [torch.zeros(dims[l + 1], batch, dtype=sdt, device=dev) for l in range(L)]
+        self.dY = [torch.zeros(dims[l + 1], batch, dtype=sdt, device=dev) for l in range(L)]
+        self.dY[-1].copy_(synth.to_storage(synth.normal(g, (dims[-1], batch)), dtype).to(dev))
+        self.dW = [torch.zeros(dims[l + 1], dims[l], device=dev) for l in range(L)]
+        self.db = [torch.zeros(dims[l + 1], device=dev) for l in range(L)]
+        self.idx = [torch.zeros(dims[l + 1], dtype=torch.int32, device=dev) for l in range(L - 1)]
+        self.plans = [api.ard_row_plan() for _ in range(L - 1)]
+        self.K = None
+
+    def set_rate(self, p):
+        api = self.api
+        self.p = p
+        self.K, _ = api.ard_search_distribution(p)
+        # descriptors point at the plan structs, which each step refills
+        self.descs = []
+        for l in range(self.L):
+            in_plan = self.plans[l - 1] if l > 0 else None
+            out_plan = self.plans[l] if l < self.L - 1 else None
+            act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
+            self.descs.append(api.fc_desc(self.ard_dtype, self.B, self.dims[l], self.dims[l + 1],
+                                          in_plan, out_plan, 1.0, act, api.ARD_DROPPED_SKIP))
+
+    def patterns(self, it):
+        return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
+
+    def kept(self, pats):
+        api = self.api
+        n = [self.dims[0]]
+        for l, (per, off) in enumerate(pats):
+            n.append(api.ard_row_kept(self.dims[l + 1], per, off))
+        n.append(self.dims[-1])
+        return n
+
+    def kept_flops(self, pats):
+        """(total, per-call dict): 2*B*K_kept*N_kept per GEMM; no bwd_data for layer 0."""
+        n = self.kept(pats)
+        per = {}
+        for l in range(self.L):
+            f = 2.0 * self.B * n[l] * n[l + 1]
+            per[("fwd", l)] = f
+            per[("bwd_weight", l)] = f
+            if l > 0:
+                per[("bwd_data", l)] = f
+        return sum(per.values()), per
+
+    def step(self, it, timed_call=None, events=None):
+        api = self.api
+        pats = self.patterns(it)
+        for l, (per, off) in enumerate(pats):
+            api.ard_plan_rows(self.dims[l + 1], per, off, self.idx[l], plan=self.plans[l])
+        acts = [self.X0] + self.Y
+
+        def call(kind, l, fn):
+            if timed_call == (kind, l):
+                events[0].record()
+                fn()
+                events[1].record()
+            else:
+                fn()
+
+        for l in range(self.L):
+            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.descs[l], acts[l], self.W[l], self.bias[l], self.Y[l]))
+        for l in reversed(range(self.L)):
+            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.descs[l], acts[l], self.dY[l],
+                                                                     self.Y[l], self.dW[l], self.db[l]))
+            if l > 0:
+                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.descs[l], self.dY[l], self.Y[l],
+                                                                     self.W[l], self.dY[l - 1]))
+        return pats
+
+    # ------------------------------------------------------------------ oracle
+    def oracle_step(self, pats):
+        """The same step through the fp64 oracle (masked dense layers)."""
+        import numpy as np
+        from oracle import fc as ofc
+        from oracle import patterns as opat
+        masks = [opat.row_mask(self.dims[0], 1, 0)]
+        for l, (per, off) in enumerate(pats):
+            masks.append(opat.row_mask(self.dims[l + 1], per, off))
+        masks.append(opat.row_mask(self.dims[-1], 1, 0))
+        X = self._host["X0"]
+        Ys = []
+        for l in range(self.L):
+            act = "relu" if l < self.L - 1 else "none"
+            X = ofc.fc_forward(X, self._host["W"][l], None, masks[l], masks[l + 1], 1.0, act)
+            Ys.append(X)
+        dY = self._host["dY"]
+        for l in reversed(range(self.L)):
+            act = "relu" if l < self.L - 1 else "none"
+            Xin = Ys[l - 1] if l > 0 else self._host["X0"]
+            dX, dW, db = ofc.fc_backward(Xin, self._host["W"][l], Ys[l], dY, masks[l], masks[l + 1], 1.0, act)
+            dY = dX
+        return np.abs(dW).sum()
+
+    def host_copies(self):
+        self._host = {"X0": self.X0.double().cpu().numpy().T.copy(),
+                      "W": [w.double().cpu().numpy() for w in self.W],
+                      "dY": self.dY[-1].double().cpu().numpy().T.copy()}
+
+
+WORKLOADS = {
+    "mlp784": dict(name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
+                   dtype="f32", init="xavier", seed=1805 + 1),
+    "mlp8192": dict(name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
+                    dtype="bf16", init="he", seed=1805 + 4),
+}
+
+
+def time_steps(wl, steps, warmup, it0, timed_call=None):
+    import torch
+    for i in range(warmup):
+        wl.step(it0 + i)
+    torch.cuda.synchronize()
+    ev = None
+    durs = []
+    total_flops = 0.0
+    call_flops = 0.0
+    if timed_call is not None:
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        pats = wl.step(it0 + warmup + i, timed_call, ev[i] if ev else None)
+        f, per = wl.kept_flops(pats)
+        total_flops += f
+        if timed_call is not None:
+            call_flops += per[timed_call]
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = start.elapsed_time(end)
+    if ev:
+        durs = [a.elapsed_time(b) for a, b in ev]
+    return {"ms": gpu_ms, "wall_s": wall, "flops": total_flops, "call_ms": durs, "call_flops": call_flops}
+
+
+def dominant_call(wl, it0):
+    """The (pass, layer) call with the largest summed event time over a few steps."""
+    import torch
+    totals = {}
+    for i in range(3):
+        pats = wl.patterns(it0 + i)
+        _, per = wl.kept_flops(pats)
+        for key in per:
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            wl.step(it0 + i, key, ev)
+            torch.cuda.synchronize()
+            totals[key] = totals.get(key, 0.0) + ev[0].elapsed_time(ev[1])
+    return max(totals, key=totals.get)
+
+
+def cpu_baseline(wl, p, budget_s):
+    """The oracle on the host cores: as many steps as fit in ~budget_s."""
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    wl.set_rate(p)
+    wl.host_copies()
+    n, flops, t = 0, 0.0, 0.0
+    while t < budget_s and n < 1000:
+        pats = wl.patterns(10_000 + n)
+        t0 = time.perf_counter()
+        wl.oracle_step(pats)
+        t += time.perf_counter() - t0
+        flops += wl.kept_flops(pats)[0]
+        n += 1
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} steps of the same workload at p={p} (fp64 masked dense layers, numpy), {t:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mlp784", choices=sorted(WORKLOADS))
+    ap.add_argument("--p", type=float, default=0.5, help="dropout rate of the headline value")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1805_08939_amd import _ffi
+    _ffi.lib()
+    torch.cuda.set_device(0)
+    spec = WORKLOADS[args.workload]
+    wl = Mlp(**spec)
+    dtype = spec["dtype"]
+
+    rates = sorted({0.0, 0.3, 0.5, 0.7, args.p})
+    results = {}
+    for i, p in enumerate(rates):
+        wl.set_rate(p)
+        it0 = 1_000_000 * (i + 1)
+        timed = None
+        if p == args.p:
+            timed = dominant_call(wl, it0)
+        r = time_steps(wl, args.steps, args.warmup, it0, timed)
+        r["timed_call"] = timed
+        results[p] = r
+        print(f"# p={p}: {r['ms'] / args.steps:.4f} ms/step, kept {r['flops'] / args.steps / 1e9:.3f} GFLOP/step, "
+              f"{r['flops'] / (r['ms'] * 1e-3) / 1e12:.3f} TFLOP/s", file=sys.stderr, flush=True)
+
+    head = results[args.p]
+    value = head["flops"] / (head["ms"] * 1e-3) / 1e12
+    t0 = results[0.0]["ms"]
+    speedup = {f"{p}": t0 / results[p]["ms"] for p in rates if p > 0}
+    kept_frac = {f"{p}": (results[p]["flops"] / results[0.0]["flops"]) for p in rates if p > 0}
+    kind, layer = head["timed_call"]
+    call_ms = sum(head["call_ms"]) / len(head["call_ms"])
+    call_flops = head["call_flops"] / args.steps
+    achieved = call_flops / (call_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                "frac": achieved / PEAK_TFLOPS[dtype], "traffic": None,
+                "kernel": f"gemm ({kind}, layer {layer})", "avg_launch_us": call_ms * 1e3,
+                "flops_per_launch": call_flops}
+    out = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": head["ms"] / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": spec["name"], "global_batch": spec["batch"], "layers": spec["dims"],
+                   "p": args.p, "patterns": "row-based, sampled per step from K(p), n_max 16",
+                   "dropped": "skip"},
+        "speedup_vs_p0": speedup,
+        "kept_flop_fraction": kept_frac,
+        "per_p": {f"{p}": {"ms_per_step": results[p]["ms"] / args.steps,
+                           "tflops_kept": results[p]["flops"] / (results[p]["ms"] * 1e-3) / 1e12}
+                  for p in rates},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.p, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

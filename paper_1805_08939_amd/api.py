@@ -128,10 +128,10 @@ def ard_bitmap_popcount(bits, total):
 
 # --------------------------------------------------------------------------- compaction
 
-def ard_plan_rows(n, period, offset, d_idx, stream=None):
-    """Fills the int32 device tensor d_idx with the kept list; returns the plan.
-    The plan keeps a reference to d_idx."""
-    plan = ard_row_plan()
+def ard_plan_rows(n, period, offset, d_idx, stream=None, plan=None):
+    """Fills the int32 device tensor d_idx with the kept list; returns the plan
+    (``plan`` if given, refilled in place). The plan keeps a reference to d_idx."""
+    plan = ard_row_plan() if plan is None else plan
     _check(_ffi.lib().ard_plan_rows(n, period, offset, _ptr(d_idx), ctypes.byref(plan), _stream(stream)))
     plan._keep = d_idx
     return plan

@@ -129,8 +129,8 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   g.M = s.kout;
   g.N = s.B;
   g.K = s.kin;
-  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f};
-  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f};
+  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f, 0};
+  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
   g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
   const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
@@ -153,10 +153,10 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   g.N = s.B;
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
-  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f};
+  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f, 0};
   // B(t, n) = dY[out(t)][n] * [Y > 0]: the 0/1 gate keeps bf16 operands exact;
   // scale is applied to the fp32 accumulators in the epilogue.
-  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f};
+  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f, 0};
   g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale};
   const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
@@ -178,8 +178,8 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.M = s.kout;
   g.N = s.kin;
   g.K = s.B;
-  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f};
-  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f};
+  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f, 0};
+  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
   g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
   const bool v = vec_rows(s.B, sizeof(T));
   ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(

@@ -50,6 +50,7 @@ struct GemmOperand {
   int64_t bstride;       // elements between batch entries (blockIdx.z)
   int32_t relu;          // gated operand: multiply by [Y > 0]
   float scale;           // gated operand: scale factor
+  int64_t kbstride;      // elements between K batches (see GemmArgs::kbatch)
 };
 
 struct GemmOutput {
@@ -64,10 +65,14 @@ struct GemmOutput {
                          // dropout scale of the backward passes)
 };
 
+// The contraction runs over kbatch x K: K batch kb reads both operands at
+// base + kb * kbstride (a sum over time steps of an LSTM, say). kbatch 0 or 1
+// is a plain GEMM.
 struct GemmArgs {
   int32_t M, N, K;
   GemmOperand a, b;
   GemmOutput c;
+  int32_t kbatch;
 };
 
 template <typename T>
@@ -339,12 +344,19 @@ __global__ void __launch_bounds__(Cfg::NT) gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  for (int k0 = 0; k0 < g.K; k0 += Cfg::BK) {
-    load_tile<T, AMODE, AGATE, Cfg::BM, Cfg::BK, LDK, Cfg::NT>(g.a, abase, aybase, As, m0, k0, g.M, g.K);
-    load_tile<T, BMODE, BGATE, Cfg::BN, Cfg::BK, LDK, Cfg::NT>(g.b, bbase, bybase, Bs, n0, k0, g.N, g.K);
-    __syncthreads();
-    mma_slab<T, Cfg, LDK>(As, Bs, acc, wm, wn);
-    __syncthreads();
+  const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
+  for (int kb = 0; kb < kbatch; ++kb) {
+    const T* ab = abase + kb * g.a.kbstride;
+    const T* aby = AGATE ? aybase + kb * g.a.kbstride : nullptr;
+    const T* bb = bbase + kb * g.b.kbstride;
+    const T* bby = BGATE ? bybase + kb * g.b.kbstride : nullptr;
+    for (int k0 = 0; k0 < g.K; k0 += Cfg::BK) {
+      load_tile<T, AMODE, AGATE, Cfg::BM, Cfg::BK, LDK, Cfg::NT>(g.a, ab, aby, As, m0, k0, g.M, g.K);
+      load_tile<T, BMODE, BGATE, Cfg::BN, Cfg::BK, LDK, Cfg::NT>(g.b, bb, bby, Bs, n0, k0, g.N, g.K);
+      __syncthreads();
+      mma_slab<T, Cfg, LDK>(As, Bs, acc, wm, wn);
+      __syncthreads();
+    }
   }
   store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz);
 }
