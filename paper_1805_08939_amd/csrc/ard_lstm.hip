@@ -1,19 +1,555 @@
-// LSTM layer with hidden-unit row pattern (Sec. IV-C). Placeholder entry points.
+// LSTM layer with a row-based dropout pattern on its hidden units, fixed for
+// the whole sequence (Sec. IV-C applies the method to LSTM's matrix products).
+//
+// Dropped units are removed from the layer: their h and c stay 0, so every
+// gate GEMM runs on the compact set S of kept units. The layer compacts its
+// weights once per sequence into the workspace:
+//   Wc[4u + g][c] = W[g*H + S(u)][c]          for input columns c < I
+//   Wc[4u + g][I + v] = W[g*H + S(u)][I + S(v)]  for recurrent columns
+// Rows are unit-major (4u + g, g = i, f, g, o), so in the 32x32 MFMA
+// accumulator layout each lane holds the four gates of one unit in four
+// consecutive registers, and the cell update runs in registers.
+//
+// fwd: one batched GEMM for the input projection of all steps (bias folded
+// in), then per step a kernel computing Wc_h h_{t-1} for a 32-row x 32-column
+// tile (four waves split the contraction and reduce through LDS) fused with
+// the gate nonlinearities and the state update.
+// bwd: per step a kernel computing dh = Wc_h^T dA_{t+1} fused with the
+// pointwise backward of step t; then K-batched GEMMs over all steps for the
+// weight gradients and one batched GEMM for dX.
+
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
+#include "ard_gemm.hpp"
 #include "ard_internal.hpp"
+
+namespace ard {
+
+namespace {
+
+struct Layout {
+  int64_t T, B, I, H, ns, G4, KW;
+  size_t wc, bc, rowmap, z, cc, hc, da, dc, total;
+};
+
+size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
+  Layout L;
+  L.T = d->seq_len;
+  L.B = d->batch;
+  L.I = d->input_size;
+  L.H = d->hidden_size;
+  L.ns = ns;
+  L.G4 = 4 * static_cast<int64_t>(ns);
+  L.KW = L.I + ns;
+  size_t off = 0;
+  L.wc = off;     off += al256(4 * L.G4 * L.KW);
+  L.bc = off;     off += al256(4 * L.G4 + 4);
+  L.rowmap = off; off += al256(4 * L.G4 + 4);
+  L.z = off;      off += al256(4 * L.T * L.G4 * L.B);
+  L.cc = off;     off += al256(4 * (L.T + 1) * ns * L.B);
+  L.hc = off;     off += al256(4 * (L.T + 1) * ns * L.B);
+  L.da = off;     off += al256(4 * L.T * L.G4 * L.B);
+  L.dc = off;     off += al256(4 * static_cast<int64_t>(ns) * L.B + 4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+__device__ __forceinline__ int64_t unit_row(const int32_t* idx, int64_t u) { return idx ? idx[u] : u; }
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
+
+// Compact weights, bias and row map; one block per compact row 4u + g.
+__global__ void lstm_prepare_kernel(const float* __restrict__ W, const float* __restrict__ bias,
+                                    const int32_t* __restrict__ idx, int32_t I, int32_t H, int32_t ns,
+                                    float* __restrict__ Wc, float* __restrict__ bc,
+                                    int32_t* __restrict__ rowmap) {
+  const int r = blockIdx.x;
+  const int u = r >> 2, g = r & 3;
+  const int64_t src = static_cast<int64_t>(g) * H + unit_row(idx, u);
+  const float* wrow = W + src * (I + H);
+  float* crow = Wc + static_cast<int64_t>(r) * (I + ns);
+  for (int c = threadIdx.x; c < I + ns; c += blockDim.x)
+    crow[c] = c < I ? wrow[c] : wrow[I + unit_row(idx, c - I)];
+  if (threadIdx.x == 0) {
+    bc[r] = bias ? bias[src] : 0.0f;
+    rowmap[r] = static_cast<int32_t>(src);
+  }
+}
+
+// Compact initial state: dst[u][b] = src ? src[S(u)][b] : 0.
+__global__ void lstm_gather_state_kernel(const float* __restrict__ src, const int32_t* __restrict__ idx,
+                                         int32_t ns, int32_t B, float* __restrict__ dst) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<int64_t>(ns) * B) return;
+  const int64_t u = e / B, b = e % B;
+  dst[e] = src ? src[unit_row(idx, u) * B + b] : 0.0f;
+}
+
+// Full state from compact: dst[j][b] = kept(j) ? src[u(j)][b] : 0 over H rows.
+__global__ void lstm_scatter_state_kernel(const float* __restrict__ src, int32_t H, int32_t B,
+                                          int32_t period, int32_t offset, float* __restrict__ dst) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<int64_t>(H) * B) return;
+  const int64_t j = e / B, b = e % B;
+  dst[e] = (j % period == offset) ? src[((j - offset) / period) * B + b] : 0.0f;
+}
+
+// Zeroes rows r of out[rows][cols] whose unit (r % H) is dropped.
+__global__ void lstm_zero_dropped_rows_kernel(float* __restrict__ out, int64_t rows, int32_t cols,
+                                              int32_t H, int32_t period, int32_t offset) {
+  const int64_t r = blockIdx.x;
+  if (r >= rows || ((r % H) % period) == offset) return;
+  for (int c = threadIdx.x; c < cols; c += blockDim.x) out[r * cols + c] = 0.0f;
+}
+
+// dW[4H][I+H]: zero the rows of dropped units and the recurrent columns of
+// dropped units; dbias entries of dropped units.
+__global__ void lstm_zero_dropped_dw_kernel(float* __restrict__ dW, float* __restrict__ dbias, int32_t I,
+                                            int32_t H, int32_t period, int32_t offset) {
+  const int r = blockIdx.x;
+  const bool row_kept = ((r % H) % period) == offset;
+  float* row = dW + static_cast<int64_t>(r) * (I + H);
+  for (int c = threadIdx.x; c < I + H; c += blockDim.x)
+    if (!row_kept || (c >= I && ((c - I) % period) != offset)) row[c] = 0.0f;
+  if (threadIdx.x == 0 && dbias && !row_kept) dbias[r] = 0.0f;
+}
+
+__global__ void fill_kernel(float* __restrict__ p, int64_t n, float v) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e < n) p[e] = v;
+}
+
+// dbias[rowmap[r]] = sum over t, b of dA[t][r][b]; one block per row r.
+__global__ void __launch_bounds__(256) lstm_dbias_kernel(const float* __restrict__ dA,
+                                                         const int32_t* __restrict__ rowmap, int32_t T,
+                                                         int32_t G4, int32_t B, float* __restrict__ dbias) {
+  __shared__ float part[256];
+  const int r = blockIdx.x;
+  float s = 0.0f;
+  for (int64_t e = threadIdx.x; e < static_cast<int64_t>(T) * B; e += 256) {
+    const int64_t t = e / B, b = e % B;
+    s += dA[(t * G4 + r) * B + b];
+  }
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dbias[rowmap[r]] = part[0];
+}
+
+struct LstmStep {
+  const float* Wc;      // compact weights [G4][KW]
+  const int32_t* idx;   // S list or NULL
+  float* Z;             // [T][G4][B]: input projection + bias, then activated gates
+  float* Cc;            // [T+1][ns][B]
+  float* Hc;            // [T+1][ns][B]
+  float* Hs;            // [T][H][B] output
+  float* dA;            // [T][G4][B]
+  float* dc;            // [ns][B] carry
+  const float* dHs;     // [T][H][B]
+  float* dh0;           // [H][B] or NULL (final backward step)
+  int32_t t, B, I, H, ns, G4, KW;
+};
+
+constexpr int kStepBK = 64;
+constexpr int kStepLDK = kStepBK + 4;
+
+// 32 x 32 output block over a contraction of length K held in two operand
+// views; the four waves of the block take disjoint quarters of each 64-wide
+// slab, then reduce through LDS. On return wave w holds, for its lane, the
+// full sums of accumulator registers 4w..4w+3 (rows 8w + 4*(lane/32) + q,
+// column lane % 32 of the block).
+template <int AMODE, int BMODE>
+__device__ __forceinline__ void splitk_32x32(const GemmOperand& a, const float* abase, const GemmOperand& b,
+                                             const float* bbase, int m0, int n0, int M, int N, int K,
+                                             float (&out)[4]) {
+  __shared__ __attribute__((aligned(16))) float As[32 * kStepLDK];
+  __shared__ __attribute__((aligned(16))) float Bs[32 * kStepLDK];
+  __shared__ float red[4 * 16 * 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lr = lane & 31, lh = lane >> 5;
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  for (int k0 = 0; k0 < K; k0 += kStepBK) {
+    load_tile<float, AMODE, false, 32, kStepBK, kStepLDK, 256>(a, abase, nullptr, As, m0, k0, M, K);
+    load_tile<float, BMODE, false, 32, kStepBK, kStepLDK, 256>(b, bbase, nullptr, Bs, n0, k0, N, K);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 16 * w; kk < 16 * w + 16; kk += 8) {
+      const f32x4 av = *reinterpret_cast<const f32x4*>(As + lr * kStepLDK + kk + 4 * lh);
+      const f32x4 bv = *reinterpret_cast<const f32x4*>(Bs + lr * kStepLDK + kk + 4 * lh);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], bv[e], acc, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) red[(w * 16 + r) * 64 + lane] = acc[r];
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float s = 0.0f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) s += red[(v * 16 + 4 * w + q) * 64 + lane];
+    out[q] = s;
+  }
+}
+
+// Forward step t: gates of 8 units x 32 samples.
+template <bool AVEC, bool BVEC>
+__global__ void __launch_bounds__(256) lstm_fwd_step_kernel(LstmStep s) {
+  const int r0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  GemmOperand a = {}, b = {};
+  a.ld = s.KW;
+  b.ld = s.B;
+  const float* hprev = s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B;
+  float z[4];
+  splitk_32x32<AVEC ? KC_VEC : KC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I, b, hprev, r0, n0, s.G4, s.B,
+                                                                  s.ns, z);
+  const int64_t u = r0 / 4 + 2 * w + (lane >> 5);
+  const int64_t col = n0 + (lane & 31);
+  if (u >= s.ns || col >= s.B) return;
+  float* Zt = s.Z + static_cast<int64_t>(s.t) * s.G4 * s.B;
+  float gate[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) gate[q] = z[q] + Zt[(4 * u + q) * s.B + col];
+  const float ig = sigm(gate[0]), fg = sigm(gate[1]), gg = tanhf(gate[2]), og = sigm(gate[3]);
+  const float cp = s.Cc[(static_cast<int64_t>(s.t) * s.ns + u) * s.B + col];
+  const float c = fg * cp + ig * gg;
+  const float h = og * tanhf(c);
+  Zt[(4 * u + 0) * s.B + col] = ig;
+  Zt[(4 * u + 1) * s.B + col] = fg;
+  Zt[(4 * u + 2) * s.B + col] = gg;
+  Zt[(4 * u + 3) * s.B + col] = og;
+  s.Cc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = c;
+  s.Hc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = h;
+  s.Hs[(static_cast<int64_t>(s.t) * s.H + unit_row(s.idx, u)) * s.B + col] = h;
+}
+
+// Pointwise backward of step t for unit u, sample b, given dL/dh_t.
+__device__ __forceinline__ void lstm_point_bwd(const LstmStep& s, int t, int64_t u, int64_t b, float dh) {
+  const float* Zt = s.Z + static_cast<int64_t>(t) * s.G4 * s.B;
+  const float ig = Zt[(4 * u + 0) * s.B + b], fg = Zt[(4 * u + 1) * s.B + b];
+  const float gg = Zt[(4 * u + 2) * s.B + b], og = Zt[(4 * u + 3) * s.B + b];
+  const float c = s.Cc[(static_cast<int64_t>(t + 1) * s.ns + u) * s.B + b];
+  const float cp = s.Cc[(static_cast<int64_t>(t) * s.ns + u) * s.B + b];
+  const float tc = tanhf(c);
+  const float d_o = dh * tc;
+  const float dcv = s.dc[u * s.B + b] + dh * og * (1.0f - tc * tc);
+  s.dc[u * s.B + b] = dcv * fg;
+  float* dAt = s.dA + static_cast<int64_t>(t) * s.G4 * s.B;
+  dAt[(4 * u + 0) * s.B + b] = dcv * gg * ig * (1.0f - ig);
+  dAt[(4 * u + 1) * s.B + b] = dcv * cp * fg * (1.0f - fg);
+  dAt[(4 * u + 2) * s.B + b] = dcv * ig * (1.0f - gg * gg);
+  dAt[(4 * u + 3) * s.B + b] = d_o * og * (1.0f - og);
+}
+
+// Last step: dh = dHs[T-1] + dhT, dc carry starts at dcT.
+__global__ void lstm_bwd_last_kernel(LstmStep s, const float* __restrict__ dhT, const float* __restrict__ dcT) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<int64_t>(s.ns) * s.B) return;
+  const int64_t u = e / s.B, b = e % s.B;
+  const int64_t j = unit_row(s.idx, u);
+  s.dc[e] = dcT ? dcT[j * s.B + b] : 0.0f;
+  float dh = s.dHs[(static_cast<int64_t>(s.t) * s.H + j) * s.B + b];
+  if (dhT) dh += dhT[j * s.B + b];
+  lstm_point_bwd(s, s.t, u, b, dh);
+}
+
+// dh_rec = Wc_h^T dA[t] for 32 units x 32 samples, then the pointwise backward
+// of step t - 1 (or, at t = 0, dh0).
+template <bool AVEC, bool BVEC, bool FINAL>
+__global__ void __launch_bounds__(256) lstm_bwd_step_kernel(LstmStep s) {
+  const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  GemmOperand a = {}, b = {};
+  a.ld = s.KW;
+  b.ld = s.B;
+  const float* dAt = s.dA + static_cast<int64_t>(s.t) * s.G4 * s.B;
+  float z[4];
+  splitk_32x32<AVEC ? MC_VEC : MC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I, b, dAt, m0, n0, s.ns, s.B,
+                                                                  s.G4, z);
+  const int64_t col = n0 + (lane & 31);
+  if (col >= s.B) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t u = m0 + 8 * w + 4 * (lane >> 5) + q;
+    if (u >= s.ns) continue;
+    const int64_t j = unit_row(s.idx, u);
+    if (FINAL) {
+      if (s.dh0) s.dh0[j * s.B + col] = z[q];
+    } else {
+      const float dh = s.dHs[(static_cast<int64_t>(s.t - 1) * s.H + j) * s.B + col] + z[q];
+      lstm_point_bwd(s, s.t - 1, u, col, dh);
+    }
+  }
+}
+
+namespace {
+
+int check_lstm(const ard_lstm_desc* d, int32_t* ns, int32_t* period, int32_t* offset, const int32_t** idx) {
+  if (!d) return fail(ARD_ERR_INVALID_ARG, "desc is NULL");
+  if (d->dtype != ARD_F32) return fail(ARD_ERR_UNSUPPORTED, "LSTM supports ARD_F32 only");
+  if (d->seq_len < 1 || d->batch < 1 || d->input_size < 1 || d->hidden_size < 1)
+    return fail(ARD_ERR_INVALID_ARG, "sizes must be >= 1");
+  int st = check_row_plan(d->hidden_plan, d->hidden_size, "hidden_plan");
+  if (st != ARD_OK) return st;
+  const bool all = !d->hidden_plan || d->hidden_plan->period == 1;
+  *ns = all ? d->hidden_size : d->hidden_plan->kept;
+  *period = all ? 1 : d->hidden_plan->period;
+  *offset = all ? 0 : d->hidden_plan->offset;
+  *idx = all ? nullptr : d->hidden_plan->d_idx;
+  return ARD_OK;
+}
+
+int check_ws(const Layout& L, void* ws, size_t ws_bytes) {
+  if (!ws || ws_bytes < L.total)
+    return fail(ARD_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", L.total, ws_bytes);
+  if (!aligned16(ws)) return fail(ARD_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  return ARD_OK;
+}
+
+int check_opt(const void* p, const char* name) {
+  if (p && !aligned16(p)) return fail(ARD_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return ARD_OK;
+}
+
+inline dim3 grid1d(int64_t n, int threads) { return dim3(static_cast<unsigned>((n + threads - 1) / threads)); }
+
+LstmStep step_args(const Layout& L, char* w, const int32_t* idx) {
+  LstmStep s = {};
+  s.Wc = reinterpret_cast<const float*>(w + L.wc);
+  s.idx = idx;
+  s.Z = reinterpret_cast<float*>(w + L.z);
+  s.Cc = reinterpret_cast<float*>(w + L.cc);
+  s.Hc = reinterpret_cast<float*>(w + L.hc);
+  s.dA = reinterpret_cast<float*>(w + L.da);
+  s.dc = reinterpret_cast<float*>(w + L.dc);
+  s.B = static_cast<int32_t>(L.B);
+  s.I = static_cast<int32_t>(L.I);
+  s.H = static_cast<int32_t>(L.H);
+  s.ns = static_cast<int32_t>(L.ns);
+  s.G4 = static_cast<int32_t>(L.G4);
+  s.KW = static_cast<int32_t>(L.KW);
+  return s;
+}
+
+}  // namespace
+}  // namespace ard
 
 using namespace ard;
 
 extern "C" {
 
-size_t ard_lstm_workspace_bytes(const ard_lstm_desc*) { return 0; }
-int ard_lstm_fwd(const ard_lstm_desc*, const void*, const void*, const float*, const void*,
-                 const void*, void*, void*, void*, void*, size_t, void*) {
-  return fail(ARD_ERR_UNSUPPORTED, "LSTM layer is not built yet");
+size_t ard_lstm_workspace_bytes(const ard_lstm_desc* desc) {
+  int32_t ns, period, offset;
+  const int32_t* idx;
+  if (check_lstm(desc, &ns, &period, &offset, &idx) != ARD_OK) return 0;
+  return make_layout(desc, ns).total;
 }
-int ard_lstm_bwd(const ard_lstm_desc*, const void*, const void*, const void*, const void*, void*,
-                 size_t, void*, float*, float*, void*, void*, void*) {
-  return fail(ARD_ERR_UNSUPPORTED, "LSTM layer is not built yet");
+
+int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const float* bias, const void* h0,
+                 const void* c0, void* Hs, void* hT, void* cT, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  int32_t ns, period, offset;
+  const int32_t* idx;
+  int st = check_lstm(desc, &ns, &period, &offset, &idx);
+  if (st != ARD_OK) return st;
+  if (!X || !W || !Hs) return fail(ARD_ERR_INVALID_ARG, "X, W and Hs must not be NULL");
+  if ((st = check_opt(X, "X")) || (st = check_opt(W, "W")) || (st = check_opt(Hs, "Hs")) ||
+      (st = check_opt(bias, "bias")) || (st = check_opt(h0, "h0")) || (st = check_opt(c0, "c0")) ||
+      (st = check_opt(hT, "hT")) || (st = check_opt(cT, "cT")))
+    return st;
+  const Layout L = make_layout(desc, ns);
+  if ((st = check_ws(L, ws, ws_bytes))) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  LstmStep s = step_args(L, w, idx);
+  float* Hsf = static_cast<float*>(Hs);
+  s.Hs = Hsf;
+  const int64_t HB = L.H * L.B;
+
+  if (ns == 0) {  // every unit dropped: the layer outputs zeros
+    hipLaunchKernelGGL(fill_kernel, grid1d(L.T * HB, 256), dim3(256), 0, sm, Hsf, L.T * HB, 0.0f);
+    if (hT) hipLaunchKernelGGL(fill_kernel, grid1d(HB, 256), dim3(256), 0, sm, static_cast<float*>(hT), HB, 0.0f);
+    if (cT) hipLaunchKernelGGL(fill_kernel, grid1d(HB, 256), dim3(256), 0, sm, static_cast<float*>(cT), HB, 0.0f);
+    ARD_LAUNCH_CHECK();
+    return ARD_OK;
+  }
+
+  hipLaunchKernelGGL(lstm_prepare_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm,
+                     static_cast<const float*>(W), bias, idx, s.I, s.H, ns, const_cast<float*>(s.Wc),
+                     reinterpret_cast<float*>(w + L.bc), reinterpret_cast<int32_t*>(w + L.rowmap));
+  ARD_LAUNCH_CHECK();
+  const int64_t nsB = static_cast<int64_t>(ns) * L.B;
+  hipLaunchKernelGGL(lstm_gather_state_kernel, grid1d(nsB, 256), dim3(256), 0, sm,
+                     static_cast<const float*>(h0), idx, ns, s.B, s.Hc);
+  hipLaunchKernelGGL(lstm_gather_state_kernel, grid1d(nsB, 256), dim3(256), 0, sm,
+                     static_cast<const float*>(c0), idx, ns, s.B, s.Cc);
+  ARD_LAUNCH_CHECK();
+
+  // input projection of every step, bias folded in: Z[t] = Wc_x X[t] + bc
+  GemmArgs g = {};
+  g.M = static_cast<int32_t>(L.G4);
+  g.N = s.B;
+  g.K = s.I;
+  g.a = {s.Wc, nullptr, L.KW, nullptr, nullptr, 0, 0, 1.0f, 0};
+  g.b = {X, nullptr, L.B, nullptr, nullptr, L.I * L.B, 0, 1.0f, 0};
+  g.c = {s.Z, L.B, nullptr, nullptr, L.G4 * L.B, reinterpret_cast<const float*>(w + L.bc), 0, 1.0f};
+  const bool kw_vec = L.KW % 4 == 0;
+  const bool b_vec = L.B % 4 == 0 && L.I % 4 == 0;
+  ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+      g, static_cast<int>(L.T), kw_vec, b_vec, sm)));
+
+  const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((L.G4 + 31) / 32));
+  const bool avec = kw_vec && L.I % 4 == 0, bvec = L.B % 4 == 0;
+  for (int t = 0; t < L.T; ++t) {
+    s.t = t;
+    if (avec && bvec)
+      hipLaunchKernelGGL((lstm_fwd_step_kernel<true, true>), sgrid, dim3(256), 0, sm, s);
+    else
+      hipLaunchKernelGGL((lstm_fwd_step_kernel<false, false>), sgrid, dim3(256), 0, sm, s);
+    ARD_LAUNCH_CHECK();
+  }
+  if (period > 1) {
+    hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(L.T * L.H)), dim3(256), 0, sm,
+                       Hsf, L.T * L.H, s.B, s.H, period, offset);
+    ARD_LAUNCH_CHECK();
+  }
+  if (hT)
+    hipLaunchKernelGGL(lstm_scatter_state_kernel, grid1d(HB, 256), dim3(256), 0, sm,
+                       s.Hc + L.T * nsB, s.H, s.B, period, offset, static_cast<float*>(hT));
+  if (cT)
+    hipLaunchKernelGGL(lstm_scatter_state_kernel, grid1d(HB, 256), dim3(256), 0, sm,
+                       s.Cc + L.T * nsB, s.H, s.B, period, offset, static_cast<float*>(cT));
+  ARD_LAUNCH_CHECK();
+  return ARD_OK;
 }
+
+int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, const void* dhT, const void* dcT,
+                 void* ws, size_t ws_bytes, void* dX, float* dW, float* dbias, void* dh0, void* dc0,
+                 void* stream) {
+  clear_error();
+  int32_t ns, period, offset;
+  const int32_t* idx;
+  int st = check_lstm(desc, &ns, &period, &offset, &idx);
+  if (st != ARD_OK) return st;
+  if (!X || !dHs) return fail(ARD_ERR_INVALID_ARG, "X and dHs must not be NULL");
+  if ((st = check_opt(X, "X")) || (st = check_opt(dHs, "dHs")) || (st = check_opt(dhT, "dhT")) ||
+      (st = check_opt(dcT, "dcT")) || (st = check_opt(dX, "dX")) || (st = check_opt(dW, "dW")) ||
+      (st = check_opt(dbias, "dbias")) || (st = check_opt(dh0, "dh0")) || (st = check_opt(dc0, "dc0")))
+    return st;
+  const Layout L = make_layout(desc, ns);
+  if ((st = check_ws(L, ws, ws_bytes))) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  LstmStep s = step_args(L, w, idx);
+  s.dHs = static_cast<const float*>(dHs);
+  const int64_t HB = L.H * L.B;
+  const int64_t rowsW = 4 * L.H, colsW = L.I + L.H;
+
+  if (ns == 0) {
+    if (dX) hipLaunchKernelGGL(fill_kernel, grid1d(L.T * L.I * L.B, 256), dim3(256), 0, sm, static_cast<float*>(dX), L.T * L.I * L.B, 0.0f);
+    if (dW) hipLaunchKernelGGL(fill_kernel, grid1d(rowsW * colsW, 256), dim3(256), 0, sm, dW, rowsW * colsW, 0.0f);
+    if (dbias) hipLaunchKernelGGL(fill_kernel, grid1d(rowsW, 256), dim3(256), 0, sm, dbias, rowsW, 0.0f);
+    if (dh0) hipLaunchKernelGGL(fill_kernel, grid1d(HB, 256), dim3(256), 0, sm, static_cast<float*>(dh0), HB, 0.0f);
+    if (dc0) hipLaunchKernelGGL(fill_kernel, grid1d(HB, 256), dim3(256), 0, sm, static_cast<float*>(dc0), HB, 0.0f);
+    ARD_LAUNCH_CHECK();
+    return ARD_OK;
+  }
+
+  const int64_t nsB = static_cast<int64_t>(ns) * L.B;
+  s.t = static_cast<int32_t>(L.T - 1);
+  hipLaunchKernelGGL(lstm_bwd_last_kernel, grid1d(nsB, 256), dim3(256), 0, sm, s,
+                     static_cast<const float*>(dhT), static_cast<const float*>(dcT));
+  ARD_LAUNCH_CHECK();
+  const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32));
+  const bool vec = L.KW % 4 == 0 && L.I % 4 == 0 && L.B % 4 == 0;
+  for (int t = static_cast<int>(L.T) - 1; t >= 1; --t) {
+    s.t = t;
+    if (vec)
+      hipLaunchKernelGGL((lstm_bwd_step_kernel<true, true, false>), sgrid, dim3(256), 0, sm, s);
+    else
+      hipLaunchKernelGGL((lstm_bwd_step_kernel<false, false, false>), sgrid, dim3(256), 0, sm, s);
+    ARD_LAUNCH_CHECK();
+  }
+  if (dh0) {
+    s.t = 0;
+    s.dh0 = static_cast<float*>(dh0);
+    if (vec)
+      hipLaunchKernelGGL((lstm_bwd_step_kernel<true, true, true>), sgrid, dim3(256), 0, sm, s);
+    else
+      hipLaunchKernelGGL((lstm_bwd_step_kernel<false, false, true>), sgrid, dim3(256), 0, sm, s);
+    ARD_LAUNCH_CHECK();
+    if (period > 1) {
+      hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(L.H)), dim3(256), 0, sm,
+                         static_cast<float*>(dh0), L.H, s.B, s.H, period, offset);
+      ARD_LAUNCH_CHECK();
+    }
+  }
+  if (dc0) {
+    hipLaunchKernelGGL(lstm_scatter_state_kernel, grid1d(HB, 256), dim3(256), 0, sm, s.dc, s.H, s.B, period,
+                       offset, static_cast<float*>(dc0));
+    ARD_LAUNCH_CHECK();
+  }
+
+  const int32_t* rowmap = reinterpret_cast<const int32_t*>(w + L.rowmap);
+  const bool bv = L.B % 4 == 0;
+  if (dW) {
+    // dW[rowmap][:I] = sum_t dA[t] X[t]^T ; dW[rowmap][I + S] = sum_t dA[t] Hc[t]^T
+    GemmArgs g = {};
+    g.M = static_cast<int32_t>(L.G4);
+    g.N = s.I;
+    g.K = s.B;
+    g.kbatch = static_cast<int32_t>(L.T);
+    g.a = {s.dA, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.G4 * L.B};
+    g.b = {X, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
+    g.c = {dW, colsW, rowmap, nullptr, 0, nullptr, 0, 1.0f};
+    ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
+        g, 1, bv, bv && L.I % 4 == 0, sm)));
+    g.N = ns;
+    g.b = {s.Hc, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, nsB};
+    g.c = {dW + L.I, colsW, rowmap, idx, 0, nullptr, 0, 1.0f};
+    ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
+        g, 1, bv, bv, sm)));
+  }
+  if (dbias) {
+    hipLaunchKernelGGL(lstm_dbias_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm, s.dA, rowmap,
+                       static_cast<int32_t>(L.T), static_cast<int32_t>(L.G4), s.B, dbias);
+    ARD_LAUNCH_CHECK();
+  }
+  if (period > 1 && (dW || dbias)) {
+    if (dW) {
+      hipLaunchKernelGGL(lstm_zero_dropped_dw_kernel, dim3(static_cast<unsigned>(rowsW)), dim3(256), 0, sm, dW,
+                         dbias, s.I, s.H, period, offset);
+    } else {
+      hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(rowsW)), dim3(64), 0, sm,
+                         dbias, rowsW, 1, s.H, period, offset);
+    }
+    ARD_LAUNCH_CHECK();
+  }
+  if (dX) {
+    // dX[t] = Wc_x^T dA[t] for every step
+    GemmArgs g = {};
+    g.M = s.I;
+    g.N = s.B;
+    g.K = static_cast<int32_t>(L.G4);
+    g.a = {s.Wc, nullptr, L.KW, nullptr, nullptr, 0, 0, 1.0f, 0};
+    g.b = {s.dA, nullptr, L.B, nullptr, nullptr, L.G4 * L.B, 0, 1.0f, 0};
+    g.c = {dX, L.B, nullptr, nullptr, L.I * L.B, nullptr, 0, 1.0f};
+    ARD_HIP_CHECK((run_gemm<float, float, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+        g, static_cast<int>(L.T), L.KW % 4 == 0 && L.I % 4 == 0, bv, sm)));
+  }
+  return ARD_OK;
 }
+
+}  // extern "C"

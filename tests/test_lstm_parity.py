@@ -1,0 +1,116 @@
+"""GPU parity of the LSTM layer with hidden-unit row dropout (Sec. IV-C)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import device, f64, row_plan, to_dev
+from oracle import lstm as olstm
+from oracle import patterns as opat
+from oracle import prng as oprng
+from paper_1805_08939_amd import api, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4  # normwise per tensor, fp32
+
+
+def check(got, want, what, tol=TOL):
+    got, want = np.asarray(got, np.float64), np.asarray(want, np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    assert np.isfinite(got).all(), what
+    scale = np.abs(want).max()
+    err = np.abs(got - want).max() / (scale if scale > 0 else 1.0)
+    assert err <= tol, f"{what}: normwise error {err:.3e}"
+    return err
+
+
+def run_lstm(T, B, I, H, pattern, seed, with_state=True, with_final_grads=True, a=0.1):
+    g = synth.generator(seed)
+    X = synth.uniform(g, (T, B, I), a)
+    W = synth.uniform(g, (4 * H, I + H), a)
+    b = synth.uniform(g, (4 * H,), a)
+    h0 = synth.uniform(g, (B, H), 0.5) if with_state else None
+    c0 = synth.uniform(g, (B, H), 0.5) if with_state else None
+    dHs = synth.normal(g, (T, B, H))
+    dhT = synth.normal(g, (B, H)) if with_final_grads else None
+    dcT = synth.normal(g, (B, H)) if with_final_grads else None
+    m = opat.row_mask(H, *pattern)
+    Hs64, hT64, cT64, cache = olstm.lstm_forward(f64(X), f64(W), f64(b), m,
+                                                 None if h0 is None else f64(h0), None if c0 is None else f64(c0))
+    dX64, dW64, db64, dh064, dc064 = olstm.lstm_backward(
+        f64(X), f64(W), m, cache, f64(dHs), None if dhT is None else f64(dhT), None if dcT is None else f64(dcT))
+
+    plan = None if pattern == (1, 0) else row_plan(H, *pattern)
+    desc = api.lstm_desc(api.ARD_F32, T, B, I, H, plan)
+    ws = torch.empty(api.ard_lstm_workspace_bytes(desc) // 4 + 1, dtype=torch.float32, device=device())
+    Xd = to_dev(X.permute(0, 2, 1))      # [T][I][B]
+    Wd, bd = to_dev(W), to_dev(b)
+    h0d = to_dev(h0.T) if h0 is not None else None
+    c0d = to_dev(c0.T) if c0 is not None else None
+    Hs = torch.full((T, H, B), 9.0, device=device())
+    hT = torch.full((H, B), 9.0, device=device())
+    cT = torch.full((H, B), 9.0, device=device())
+    api.ard_lstm_fwd(desc, Xd, Wd, bd, h0d, c0d, Hs, hT, cT, ws)
+    dHsd = to_dev(dHs.permute(0, 2, 1))
+    dhTd = to_dev(dhT.T) if dhT is not None else None
+    dcTd = to_dev(dcT.T) if dcT is not None else None
+    dX = torch.full((T, I, B), 9.0, device=device())
+    dW = torch.full((4 * H, I + H), 9.0, device=device())
+    db = torch.full((4 * H,), 9.0, device=device())
+    dh0 = torch.full((H, B), 9.0, device=device())
+    dc0 = torch.full((H, B), 9.0, device=device())
+    api.ard_lstm_bwd(desc, Xd, dHsd, dhTd, dcTd, ws, dX, dW, db, dh0, dc0)
+    torch.cuda.synchronize()
+    check(f64(Hs).transpose(0, 2, 1), Hs64, "Hs")
+    check(f64(hT).T, hT64, "hT")
+    check(f64(cT).T, cT64, "cT")
+    check(f64(dX).transpose(0, 2, 1), dX64, "dX")
+    check(f64(dW), dW64, "dW")
+    check(f64(db), db64, "db")
+    check(f64(dh0).T, dh064, "dh0")
+    check(f64(dc0).T, dc064, "dc0")
+    dropped = m == 0
+    assert not f64(Hs)[:, dropped].any() and not f64(dW)[np.tile(dropped, 4)].any()
+    return Hs
+
+
+@pytest.mark.parametrize("pattern", [(1, 0), (2, 1), (3, 0), (7, 6), (16, 12)])
+def test_tiny_patterns(pattern):
+    run_lstm(3, 5, 6, 10, pattern, seed=sum(pattern))
+    run_lstm(2, 4, 8, 10, pattern, seed=7, with_state=False, with_final_grads=False)
+
+
+@pytest.mark.parametrize("shape,pattern", [((4, 40, 68, 100), (3, 1)), ((3, 37, 33, 70), (2, 0)),
+                                           ((5, 96, 128, 160), (4, 3)), ((1, 8, 12, 64), (5, 2))])
+def test_multi_tile_and_unaligned(shape, pattern):
+    T, B, I, H = shape
+    run_lstm(T, B, I, H, pattern, seed=B)
+
+
+def test_full_config_lstm_1024():
+    """Single LSTM layer fp32, input 1024, hidden 1024, 35 steps, batch 64, hidden
+    units dropped with period 2 (seeded offset), inputs ~ U(-0.1, 0.1)."""
+    K2 = np.zeros(16)
+    K2[1] = 1.0
+    per, off = oprng.sample_row_pattern(K2, 8939, 0, 0)
+    run_lstm(35, 64, 1024, 1024, (per, off), seed=1805 + 3, with_state=False, with_final_grads=False)
+
+
+def test_deterministic():
+    a = run_lstm(4, 64, 64, 96, (2, 1), seed=5)
+    b = run_lstm(4, 64, 64, 96, (2, 1), seed=5)
+    assert torch.equal(a, b)
+
+
+def test_invalid():
+    d = device()
+    desc = api.lstm_desc(api.ARD_BF16, 2, 4, 8, 8)
+    with pytest.raises(api.ArdError):
+        api.ard_lstm_fwd(desc, torch.zeros(1, device=d), torch.zeros(1, device=d), None, None, None,
+                         torch.zeros(1, device=d), None, None, torch.zeros(1, device=d))
+    desc = api.lstm_desc(api.ARD_F32, 2, 4, 8, 8)
+    small = torch.zeros(4, device=d)
+    with pytest.raises(api.ArdError) as e:
+        api.ard_lstm_fwd(desc, torch.zeros(64, device=d), torch.zeros(512, device=d), None, None, None,
+                         torch.zeros(64, device=d), None, None, small)
+    assert e.value.status == 5
