@@ -59,6 +59,12 @@ class Mlp:
         self.db = [torch.zeros(dims[l + 1], device=dev) for l in range(L)]
         self.idx = [torch.zeros(dims[l + 1], dtype=torch.int32, device=dev) for l in range(L - 1)]
         self.plans = [api.ard_row_plan() for _ in range(L - 1)]
+        # compact weights of the layers whose inputs are dropped (built once per
+        # step, shared by fwd and bwd_data) and one workspace for split-K sums:
+        # at most 256 output tiles of 128 x 128 fp32
+        self.Wc = [None] + [torch.zeros(dims[l + 1] * ((dims[l] + 7) // 8 * 8), dtype=sdt, device=dev)
+                            for l in range(1, L)]
+        self.ws = torch.empty(256 * 128 * 128, dtype=torch.float32, device=dev)
         self.K = None
 
     def set_rate(self, p):
@@ -66,13 +72,15 @@ class Mlp:
         self.p = p
         self.K, _ = api.ard_search_distribution(p)
         # descriptors point at the plan structs, which each step refills
-        self.descs = []
+        self.descs, self.cdescs = [], []
         for l in range(self.L):
             in_plan = self.plans[l - 1] if l > 0 else None
             out_plan = self.plans[l] if l < self.L - 1 else None
             act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
-            self.descs.append(api.fc_desc(self.ard_dtype, self.B, self.dims[l], self.dims[l + 1],
-                                          in_plan, out_plan, 1.0, act, api.ARD_DROPPED_SKIP))
+            args = (self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], in_plan, out_plan, 1.0, act,
+                    api.ARD_DROPPED_SKIP)
+            self.descs.append(api.fc_desc(*args))
+            self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT) if l > 0 else self.descs[-1])
 
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
@@ -102,7 +110,11 @@ class Mlp:
         pats = self.patterns(it)
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, self.idx[l], plan=self.plans[l])
+        for l in range(1, self.L):
+            api.ard_fc_compact_weights(self.cdescs[l], self.W[l], self.Wc[l])
+        Wf = [self.W[0]] + self.Wc[1:]
         acts = [self.X0] + self.Y
+        ws = self.ws
 
         def call(kind, l, fn):
             if timed_call == (kind, l):
@@ -113,13 +125,13 @@ class Mlp:
                 fn()
 
         for l in range(self.L):
-            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.descs[l], acts[l], self.W[l], self.bias[l], self.Y[l]))
+            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.cdescs[l], acts[l], Wf[l], self.bias[l], self.Y[l], ws))
         for l in reversed(range(self.L)):
             call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.descs[l], acts[l], self.dY[l],
-                                                                     self.Y[l], self.dW[l], self.db[l]))
+                                                                     self.Y[l], self.dW[l], self.db[l], ws))
             if l > 0:
-                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.descs[l], self.dY[l], self.Y[l],
-                                                                     self.W[l], self.dY[l - 1]))
+                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], self.dY[l], self.Y[l],
+                                                                     Wf[l], self.dY[l - 1], ws))
         return pats
 
     # ------------------------------------------------------------------ oracle

@@ -207,6 +207,18 @@ int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, i
  */
 typedef enum { ARD_ACT_NONE = 0, ARD_ACT_RELU = 1 } ard_act;
 typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
+/*
+ * How the W argument of fwd / bwd_data is stored:
+ *   ARD_WEIGHTS_FULL   : the full W[N][K];
+ *   ARD_WEIGHTS_COMPACT: the compact Wc[kept_out][ldc] written by
+ *                        ard_fc_compact_weights for this descriptor's patterns,
+ *                        Wc[i][j] = W[S_out(i)][S_in(j)] (Sec. III-A's compact
+ *                        weight matrix), ldc = ard_fc_compact_ld(desc).
+ * With FULL weights and a gathered input side, fwd and bwd_data build the
+ * compact copy in their workspace themselves; a training step that compacts
+ * once and passes COMPACT to both saves one pass over W.
+ */
+typedef enum { ARD_WEIGHTS_FULL = 0, ARD_WEIGHTS_COMPACT = 1 } ard_weight_layout;
 
 typedef struct {
   int32_t dtype;        /* ard_dtype */
@@ -218,17 +230,33 @@ typedef struct {
   float scale;          /* multiplies kept outputs (1 = pure mask) */
   int32_t act;          /* ard_act */
   int32_t dropped;      /* ard_dropped */
-  int32_t reserved;
+  int32_t weight_layout;/* ard_weight_layout of the W argument */
 } ard_fc_desc;
 
+/* Row length (elements) of the compact weight matrix: kept inputs rounded up
+ * to a multiple of 8. -1 on an invalid descriptor. */
+int32_t ard_fc_compact_ld(const ard_fc_desc* desc);
+/* Bytes of the compact weight matrix (kept_out * ldc * element size). */
+size_t ard_fc_compact_bytes(const ard_fc_desc* desc);
+/* Gathers W[S_out][S_in] (W full, [N][K]) into Wc (device, compact bytes,
+ * caller-owned); padding columns are written 0. */
+int ard_fc_compact_weights(const ard_fc_desc* desc, const void* W, void* Wc, void* stream);
+
+/* Workspace (bytes) that fwd, bwd_data and bwd_weight of this descriptor need:
+ * split-contraction partial sums for small output grids and, for FULL weights
+ * with a gathered input side, the compact weight copy. Depends on the kept
+ * counts, so query it per pattern (or once for the dense pattern, which bounds
+ * every other one of the same layer). ws may be NULL when this is 0. */
+size_t ard_fc_workspace_bytes(const ard_fc_desc* desc);
+
 int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias,
-               void* Yt, void* stream);
+               void* Yt, void* ws, size_t ws_bytes, void* stream);
 /* Yt: the forward output (for the ReLU gate), may be NULL when act == NONE. */
 int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
-                    void* dXt, void* stream);
+                    void* dXt, void* ws, size_t ws_bytes, void* stream);
 /* dbias may be NULL. */
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
-                      float* dW, float* dbias, void* stream);
+                      float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Layer under a tile pattern (device).                                     */

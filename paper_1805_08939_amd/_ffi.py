@@ -17,6 +17,7 @@ ARD_F32, ARD_BF16 = 0, 1
 ARD_SEARCH_PLAIN, ARD_SEARCH_MIRROR = 0, 1
 ARD_ACT_NONE, ARD_ACT_RELU = 0, 1
 ARD_DROPPED_ZERO, ARD_DROPPED_SKIP = 0, 1
+ARD_WEIGHTS_FULL, ARD_WEIGHTS_COMPACT = 0, 1
 
 
 class ard_search_opts(ctypes.Structure):
@@ -46,7 +47,7 @@ class ard_tile_plan(ctypes.Structure):
 class ard_fc_desc(ctypes.Structure):
     _fields_ = [("dtype", c_i32), ("batch", c_i32), ("in_features", c_i32), ("out_features", c_i32),
                 ("in_plan", ctypes.POINTER(ard_row_plan)), ("out_plan", ctypes.POINTER(ard_row_plan)),
-                ("scale", c_f32), ("act", c_i32), ("dropped", c_i32), ("reserved", c_i32)]
+                ("scale", c_f32), ("act", c_i32), ("dropped", c_i32), ("weight_layout", c_i32)]
 
 
 class ard_tile_desc(ctypes.Structure):
@@ -79,9 +80,15 @@ SIGNATURES = {
     "ard_tile_plan_workspace_bytes": (c_size, [c_i32, c_i32]),
     "ard_plan_tiles": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, c_i32, c_vp, c_size,
                                       ctypes.POINTER(ard_tile_plan), c_vp]),
-    "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp]),
-    "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp]),
-    "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "ard_fc_compact_ld": (c_i32, [ctypes.POINTER(ard_fc_desc)]),
+    "ard_fc_compact_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
+    "ard_fc_compact_weights": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp]),
+    "ard_fc_workspace_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
+    "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size,
+                                       c_vp]),
+    "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                         c_size, c_vp]),
     "ard_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
                                     c_vp, c_vp, c_vp, c_vp]),
     "ard_tile_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),

@@ -12,6 +12,7 @@ import numpy as np
 from . import _ffi
 from ._ffi import (ARD_ACT_NONE, ARD_ACT_RELU, ARD_BF16, ARD_DROPPED_SKIP, ARD_DROPPED_ZERO,  # noqa: F401
                    ARD_ERR_NOT_CONVERGED, ARD_F32, ARD_SEARCH_MIRROR, ARD_SEARCH_PLAIN,
+                   ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_FULL,
                    ard_fc_desc, ard_lstm_desc, ard_row_plan, ard_search_info, ard_search_opts,
                    ard_tile_desc, ard_tile_plan)
 
@@ -154,26 +155,49 @@ def ard_plan_tiles(n, k, tile, d_bits, nnz, ws, stream=None):
 # --------------------------------------------------------------------------- FC layer
 
 def fc_desc(dtype, batch, in_features, out_features, in_plan=None, out_plan=None, scale=1.0,
-            act=ARD_ACT_NONE, dropped=ARD_DROPPED_ZERO):
+            act=ARD_ACT_NONE, dropped=ARD_DROPPED_ZERO, weight_layout=ARD_WEIGHTS_FULL):
     d = ard_fc_desc(dtype, batch, in_features, out_features, _plan_ptr(in_plan), _plan_ptr(out_plan),
-                    scale, act, dropped, 0)
+                    scale, act, dropped, weight_layout)
     d._keep = (in_plan, out_plan)
     return d
 
 
-def ard_fc_fwd(desc, Xt, W, bias, Yt, stream=None):
-    _check(_ffi.lib().ard_fc_fwd(ctypes.byref(desc), _ptr(Xt), _ptr(W), _ptr(bias), _ptr(Yt),
+def _ws(ws):
+    return (_ptr(ws), ws.numel() * ws.element_size()) if ws is not None else (None, 0)
+
+
+def ard_fc_compact_ld(desc):
+    return _ffi.lib().ard_fc_compact_ld(ctypes.byref(desc))
+
+
+def ard_fc_compact_bytes(desc):
+    return _ffi.lib().ard_fc_compact_bytes(ctypes.byref(desc))
+
+
+def ard_fc_compact_weights(desc, W, Wc, stream=None):
+    _check(_ffi.lib().ard_fc_compact_weights(ctypes.byref(desc), _ptr(W), _ptr(Wc), _stream(stream)))
+
+
+def ard_fc_workspace_bytes(desc):
+    return _ffi.lib().ard_fc_workspace_bytes(ctypes.byref(desc))
+
+
+def ard_fc_fwd(desc, Xt, W, bias, Yt, ws=None, stream=None):
+    p, n = _ws(ws)
+    _check(_ffi.lib().ard_fc_fwd(ctypes.byref(desc), _ptr(Xt), _ptr(W), _ptr(bias), _ptr(Yt), p, n,
                                  _stream(stream)))
 
 
-def ard_fc_bwd_data(desc, dYt, Yt, W, dXt, stream=None):
-    _check(_ffi.lib().ard_fc_bwd_data(ctypes.byref(desc), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt),
+def ard_fc_bwd_data(desc, dYt, Yt, W, dXt, ws=None, stream=None):
+    p, n = _ws(ws)
+    _check(_ffi.lib().ard_fc_bwd_data(ctypes.byref(desc), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt), p, n,
                                       _stream(stream)))
 
 
-def ard_fc_bwd_weight(desc, Xt, dYt, Yt, dW, dbias, stream=None):
+def ard_fc_bwd_weight(desc, Xt, dYt, Yt, dW, dbias, ws=None, stream=None):
+    p, n = _ws(ws)
     _check(_ffi.lib().ard_fc_bwd_weight(ctypes.byref(desc), _ptr(Xt), _ptr(dYt), _ptr(Yt), _ptr(dW),
-                                        _ptr(dbias), _stream(stream)))
+                                        _ptr(dbias), p, n, _stream(stream)))
 
 
 # --------------------------------------------------------------------------- tile layer

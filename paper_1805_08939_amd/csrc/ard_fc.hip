@@ -70,6 +70,18 @@ __global__ void __launch_bounds__(256) dbias_kernel(const T* __restrict__ dYt,
 
 namespace {
 
+// Gathers W[S_out][S_in] into Wc[kout][ldc]; padding columns are 0.
+template <typename T>
+__global__ void compact_weights_kernel(const T* __restrict__ W, int64_t K, const int32_t* __restrict__ out_idx,
+                                       const int32_t* __restrict__ in_idx, int32_t kin, int64_t ldc,
+                                       T* __restrict__ Wc) {
+  const int64_t i = blockIdx.x;
+  const T* row = W + gather(out_idx, i) * K;
+  T* crow = Wc + i * ldc;
+  for (int64_t j = threadIdx.x; j < ldc; j += blockDim.x)
+    crow[j] = j < kin ? row[gather(in_idx, j)] : from_f32<T>(0.0f);
+}
+
 struct FcShape {
   int32_t B, K, N;
   int32_t kin, kout;                 // kept counts
@@ -77,6 +89,9 @@ struct FcShape {
   const int32_t* out_idx;            // NULL when every output is kept
   int32_t in_period, in_offset, out_period, out_offset;
   size_t esize;
+  int64_t ldc;                       // compact weight row length
+  bool compact_given;                // W argument is the compact matrix
+  bool needs_compact;                // fwd / bwd_data gather W through a compact copy
 };
 
 int check_desc(const ard_fc_desc* d, FcShape* s) {
@@ -90,6 +105,8 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
     return fail(ARD_ERR_INVALID_ARG, "unknown activation %d", d->act);
   if (d->dropped != ARD_DROPPED_ZERO && d->dropped != ARD_DROPPED_SKIP)
     return fail(ARD_ERR_INVALID_ARG, "unknown dropped-output mode %d", d->dropped);
+  if (d->weight_layout != ARD_WEIGHTS_FULL && d->weight_layout != ARD_WEIGHTS_COMPACT)
+    return fail(ARD_ERR_INVALID_ARG, "unknown weight layout %d", d->weight_layout);
   if (!(d->scale == d->scale) || d->scale == __builtin_inff() || d->scale == -__builtin_inff())
     return fail(ARD_ERR_INVALID_ARG, "scale must be finite");
   int st = check_row_plan(d->in_plan, d->in_features, "in_plan");
@@ -110,7 +127,27 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   s->out_period = out_all ? 1 : d->out_plan->period;
   s->out_offset = out_all ? 0 : d->out_plan->offset;
   s->esize = d->dtype == ARD_BF16 ? 2 : 4;
+  s->ldc = (static_cast<int64_t>(s->kin) + 7) / 8 * 8;
+  s->compact_given = d->weight_layout == ARD_WEIGHTS_COMPACT;
+  s->needs_compact = !s->compact_given && s->in_idx != nullptr;
   return ARD_OK;
+}
+
+size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+size_t compact_bytes(const FcShape& s) { return static_cast<size_t>(s.kout) * s.ldc * s.esize; }
+
+template <typename T>
+size_t partial_bytes(const FcShape& s) {
+  size_t f = gemm_partial_floats<T>(s.kout, s.B, s.kin, 1, 1);                  // fwd
+  f = f > gemm_partial_floats<T>(s.kin, s.B, s.kout, 1, 1) ? f : gemm_partial_floats<T>(s.kin, s.B, s.kout, 1, 1);
+  f = f > gemm_partial_floats<T>(s.kout, s.kin, s.B, 1, 1) ? f : gemm_partial_floats<T>(s.kout, s.kin, s.B, 1, 1);
+  return 4 * f;
+}
+
+size_t workspace_bytes(const FcShape& s, int dtype) {
+  const size_t part = dtype == ARD_BF16 ? partial_bytes<bf16>(s) : partial_bytes<float>(s);
+  return (s.needs_compact ? al256(compact_bytes(s)) : 0) + al256(part);
 }
 
 int check_ptr(const void* p, const char* name) {
@@ -119,23 +156,68 @@ int check_ptr(const void* p, const char* name) {
   return ARD_OK;
 }
 
+int check_ws(const FcShape& s, int dtype, void* ws, size_t ws_bytes) {
+  const size_t need = workspace_bytes(s, dtype);
+  if (need == 0) return ARD_OK;
+  if (!ws || ws_bytes < need)
+    return fail(ARD_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (!aligned16(ws)) return fail(ARD_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+  return ARD_OK;
+}
+
 // Rows of `ld` elements start 16-byte aligned.
 inline bool vec_rows(int64_t ld, size_t esize) { return (ld * static_cast<int64_t>(esize)) % 16 == 0; }
 
 template <typename T>
+hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t stream) {
+  if (s.kout == 0) return hipSuccess;
+  hipLaunchKernelGGL(compact_weights_kernel<T>, dim3(s.kout), dim3(256), 0, stream, static_cast<const T*>(W),
+                     static_cast<int64_t>(s.K), s.out_idx, s.in_idx, s.kin, s.ldc, static_cast<T*>(Wc));
+  return hipGetLastError();
+}
+
+// The view of W used by fwd / bwd_data: either the full matrix gathered by
+// rows (no input gather), or a compact copy (given, or built into ws).
+struct WeightView {
+  const void* p;
+  int64_t ld;
+  const int32_t* ridx;
+  float* partial;  // split-K partial sums in ws, or NULL
+};
+
+template <typename T>
+int weight_view(const FcShape& s, const void* W, void* ws, hipStream_t stream, WeightView* v) {
+  char* w = static_cast<char*>(ws);
+  if (s.compact_given) {
+    *v = {W, s.ldc, nullptr, nullptr};
+  } else if (s.needs_compact) {
+    ARD_HIP_CHECK(launch_compact<T>(s, W, w, stream));
+    *v = {w, s.ldc, nullptr, nullptr};
+    w += al256(compact_bytes(s));
+  } else {
+    *v = {W, s.K, s.out_idx, nullptr};
+  }
+  v->partial = ws ? reinterpret_cast<float*>(w) : nullptr;
+  return ARD_OK;
+}
+
+template <typename T>
 int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* W,
-                const float* bias, void* Yt, hipStream_t stream) {
+                const float* bias, void* Yt, void* ws, hipStream_t stream) {
+  WeightView wv;
+  int st = weight_view<T>(s, W, ws, stream, &wv);
+  if (st != ARD_OK) return st;
   GemmArgs g = {};
   g.M = s.kout;
   g.N = s.B;
   g.K = s.kin;
-  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f, 0};
+  g.a = {wv.p, nullptr, wv.ld, wv.ridx, nullptr, 0, 0, 1.0f, 0};
   g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
   g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
-  const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
+  const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-      g, 1, a_vec, b_vec, stream)));
+      g, 1, a_vec, b_vec, stream, wv.partial)));
   if (d->dropped == ARD_DROPPED_ZERO && s.out_period > 1) {
     hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.N), dim3(256), 0, stream,
                        static_cast<T*>(Yt), static_cast<int64_t>(s.B), s.B, s.out_period,
@@ -147,21 +229,24 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
 
 template <typename T>
 int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
-                     const void* W, void* dXt, hipStream_t stream) {
+                     const void* W, void* dXt, void* ws, hipStream_t stream) {
+  WeightView wv;
+  int st = weight_view<T>(s, W, ws, stream, &wv);
+  if (st != ARD_OK) return st;
   GemmArgs g = {};
   g.M = s.kin;
   g.N = s.B;
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
-  g.a = {W, nullptr, s.K, s.out_idx, s.in_idx, 0, 0, 1.0f, 0};
+  g.a = {wv.p, nullptr, wv.ld, wv.ridx, nullptr, 0, 0, 1.0f, 0};
   // B(t, n) = dY[out(t)][n] * [Y > 0]: the 0/1 gate keeps bf16 operands exact;
   // scale is applied to the fp32 accumulators in the epilogue.
   g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f, 0};
   g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale};
-  const bool a_vec = s.in_idx == nullptr && vec_rows(s.K, sizeof(T));
+  const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
-      g, 1, a_vec, b_vec, stream)));
+      g, 1, a_vec, b_vec, stream, wv.partial)));
   if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
     hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
                        static_cast<T*>(dXt), static_cast<int64_t>(s.B), s.B, s.in_period,
@@ -173,7 +258,7 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
 
 template <typename T>
 int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
-                       const void* Yt, float* dW, float* dbias, hipStream_t stream) {
+                       const void* Yt, float* dW, float* dbias, void* ws, hipStream_t stream) {
   GemmArgs g = {};
   g.M = s.kout;
   g.N = s.kin;
@@ -182,8 +267,11 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
   g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
   const bool v = vec_rows(s.B, sizeof(T));
+  float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                 (s.needs_compact ? al256(compact_bytes(s)) : 0))
+                      : nullptr;
   ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
-      g, 1, v, v, stream)));
+      g, 1, v, v, stream, partial)));
   if (dbias && s.kout > 0) {
     hipLaunchKernelGGL(dbias_kernel<T>, dim3(s.kout), dim3(256), 0, stream,
                        static_cast<const T*>(dYt), static_cast<const T*>(Yt), s.B, s.out_idx,
@@ -232,8 +320,41 @@ int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard
   return ARD_OK;
 }
 
+int32_t ard_fc_compact_ld(const ard_fc_desc* desc) {
+  FcShape s;
+  if (check_desc(desc, &s) != ARD_OK) return -1;
+  return static_cast<int32_t>(s.ldc);
+}
+
+size_t ard_fc_compact_bytes(const ard_fc_desc* desc) {
+  FcShape s;
+  if (check_desc(desc, &s) != ARD_OK) return 0;
+  return compact_bytes(s);
+}
+
+int ard_fc_compact_weights(const ard_fc_desc* desc, const void* W, void* Wc, void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(W, "W")) || (st = check_ptr(Wc, "Wc"))) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) {
+    ARD_HIP_CHECK(launch_compact<bf16>(s, W, Wc, sm));
+  } else {
+    ARD_HIP_CHECK(launch_compact<float>(s, W, Wc, sm));
+  }
+  return ARD_OK;
+}
+
+size_t ard_fc_workspace_bytes(const ard_fc_desc* desc) {
+  FcShape s;
+  if (check_desc(desc, &s) != ARD_OK) return 0;
+  return workspace_bytes(s, desc->dtype);
+}
+
 int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias, void* Yt,
-               void* stream) {
+               void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   FcShape s;
   int st = check_desc(desc, &s);
@@ -241,13 +362,14 @@ int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const flo
   if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(W, "W")) || (st = check_ptr(Yt, "Yt")))
     return st;
   if (bias && !aligned16(bias)) return fail(ARD_ERR_INVALID_ARG, "bias is not 16-byte aligned");
+  if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);
-  if (desc->dtype == ARD_BF16) return fc_fwd_impl<bf16>(desc, s, Xt, W, bias, Yt, sm);
-  return fc_fwd_impl<float>(desc, s, Xt, W, bias, Yt, sm);
+  if (desc->dtype == ARD_BF16) return fc_fwd_impl<bf16>(desc, s, Xt, W, bias, Yt, ws, sm);
+  return fc_fwd_impl<float>(desc, s, Xt, W, bias, Yt, ws, sm);
 }
 
 int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
-                    void* dXt, void* stream) {
+                    void* dXt, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   FcShape s;
   int st = check_desc(desc, &s);
@@ -255,13 +377,14 @@ int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, co
   if ((st = check_ptr(dYt, "dYt")) || (st = check_ptr(W, "W")) || (st = check_ptr(dXt, "dXt")))
     return st;
   if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
+  if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);
-  if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, sm);
-  return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, sm);
+  if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, ws, sm);
+  return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, ws, sm);
 }
 
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
-                      float* dW, float* dbias, void* stream) {
+                      float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   FcShape s;
   int st = check_desc(desc, &s);
@@ -270,9 +393,11 @@ int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, 
     return st;
   if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
   if (dbias && !aligned16(dbias)) return fail(ARD_ERR_INVALID_ARG, "dbias is not 16-byte aligned");
+  if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);
-  if (desc->dtype == ARD_BF16) return fc_bwd_weight_impl<bf16>(desc, s, Xt, dYt, Yt, dW, dbias, sm);
-  return fc_bwd_weight_impl<float>(desc, s, Xt, dYt, Yt, dW, dbias, sm);
+  if (desc->dtype == ARD_BF16)
+    return fc_bwd_weight_impl<bf16>(desc, s, Xt, dYt, Yt, dW, dbias, ws, sm);
+  return fc_bwd_weight_impl<float>(desc, s, Xt, dYt, Yt, dW, dbias, ws, sm);
 }
 
 }  // extern "C"

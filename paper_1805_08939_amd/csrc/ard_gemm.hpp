@@ -1,11 +1,11 @@
 // Gathered GEMM on CDNA4 matrix cores (gfx950).
 //
-// Every GEMM of the hot path multiplies COMPACT matrices whose rows (and, for
-// a weight matrix under two patterns, columns) are picked from a larger matrix
-// by an ascending index list. Sec. III-A builds these compact matrices from the
-// kept rows only; here they are never materialised in HBM: the loaders fetch
-// kept rows straight from the full matrices into LDS, and the epilogue scatters
-// the compact result back. Dropped rows are never read.
+// Every GEMM of the hot path multiplies COMPACT matrices whose rows are picked
+// from a larger matrix by an ascending index list. Sec. III-A builds these
+// compact matrices from the kept rows only; here the row gathers happen in the
+// loaders, which fetch kept rows straight from the full matrices into LDS, and
+// in the epilogue, which scatters the compact result back. Dropped rows are
+// never read or written.
 //
 // C(m, n) = sum_k A(m, k) B(k, n) over compact extents M, N, K.
 //
@@ -17,13 +17,20 @@
 //             16-byte loads, transposed in registers on the way into LDS
 //   MC_ELEM : the same with element loads
 // LDS always holds [rows of the tile][k] so that each MFMA operand fragment is
-// one 16-byte LDS read. A "gated" operand computes scale * dY * [Y > 0] (or
-// scale * dY) on load, fusing the dropout/activation derivative of the
-// backward pass (Sec. II-C: the derivative is masked by the forward mask).
+// one 16-byte LDS read. A "gated" operand multiplies by [Y > 0] on load: the
+// activation derivative of the backward pass (Sec. II-C: the derivative is
+// masked by the forward mask), exact in any dtype because the gate is 0/1.
+//
+// Main loop: each thread loads its share of the next K slab into registers
+// while the waves run MFMA on the current slab from LDS; LDS is double
+// buffered, so one barrier per slab suffices. Small output grids split the
+// contraction over workgroups (grid z); each split writes fp32 partial tiles
+// to a workspace and a second kernel sums them in fixed order (deterministic)
+// and applies the epilogue.
 //
 // Matrix cores: bf16 uses v_mfma_f32_32x32x16_bf16 (8 k per lane); fp32 uses
 // v_mfma_f32_32x32x2_f32 with each lane reading 4 consecutive k from LDS and
-// issuing four MFMAs, so that both operands stay k-contiguous.
+// issuing four MFMAs, so that both operands stay k-contiguous in LDS.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -49,7 +56,7 @@ struct GemmOperand {
   const int32_t* cidx;   // gather list of view columns, NULL = identity
   int64_t bstride;       // elements between batch entries (blockIdx.z)
   int32_t relu;          // gated operand: multiply by [Y > 0]
-  float scale;           // gated operand: scale factor
+  float scale;           // unused by the loaders (kept for layout stability)
   int64_t kbstride;      // elements between K batches (see GemmArgs::kbatch)
 };
 
@@ -67,12 +74,16 @@ struct GemmOutput {
 
 // The contraction runs over kbatch x K: K batch kb reads both operands at
 // base + kb * kbstride (a sum over time steps of an LSTM, say). kbatch 0 or 1
-// is a plain GEMM.
+// is a plain GEMM. splits > 1 divides the kbatch x ceil(K / BK) slabs over
+// that many workgroups per output tile; `partial` then receives
+// [batch][splits][M][N] fp32 sums for the reduction kernel.
 struct GemmArgs {
   int32_t M, N, K;
   GemmOperand a, b;
   GemmOutput c;
   int32_t kbatch;
+  int32_t splits;
+  float* partial;
 };
 
 template <typename T>
@@ -108,9 +119,9 @@ __device__ __forceinline__ T load_elem(const GemmOperand& op, const T* base, con
   if constexpr (!GATED) {
     return base[off];
   } else {
-    float g = op.scale * to_f32(base[off]);
-    if (op.relu && !(to_f32(ybase[off]) > 0.0f)) g = 0.0f;
-    return from_f32<T>(g);
+    T v = base[off];
+    if (op.relu && !(to_f32(ybase[off]) > 0.0f)) v = from_f32<T>(0.0f);
+    return v;
   }
 }
 
@@ -119,118 +130,130 @@ template <typename T, bool GATED>
 __device__ __forceinline__ u32x4 load_vec(const GemmOperand& op, const T* base, const T* ybase,
                                           int64_t off) {
   u32x4 raw = *reinterpret_cast<const u32x4*>(base + off);
-  if constexpr (!GATED) {
-    return raw;
-  } else {
-    constexpr int VE = TypeTraits<T>::VE;
-    u32x4 yr = raw;
-    if (op.relu) yr = *reinterpret_cast<const u32x4*>(ybase + off);
-    const T* xv = reinterpret_cast<const T*>(&raw);
-    const T* yv = reinterpret_cast<const T*>(&yr);
-    u32x4 out;
-    T* ov = reinterpret_cast<T*>(&out);
+  if constexpr (GATED) {
+    if (op.relu) {
+      constexpr int VE = TypeTraits<T>::VE;
+      const u32x4 yr = *reinterpret_cast<const u32x4*>(ybase + off);
+      T* xv = reinterpret_cast<T*>(&raw);
+      const T* yv = reinterpret_cast<const T*>(&yr);
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      float g = op.scale * to_f32(xv[e]);
-      if (op.relu && !(to_f32(yv[e]) > 0.0f)) g = 0.0f;
-      ov[e] = from_f32<T>(g);
+      for (int e = 0; e < VE; ++e)
+        if (!(to_f32(yv[e]) > 0.0f)) xv[e] = from_f32<T>(0.0f);
     }
-    return out;
   }
+  return raw;
 }
 
-// Loads the R x BK tile (tile rows r0.., compact k k0..) of an operand into LDS
-// laid out [R][LDK] (k contiguous). rext / kext are the compact extents.
+// Per-thread share of one R x BK operand tile: global -> registers (load)
+// and registers -> LDS [R][LDK] (store). rext / kext are the compact extents;
+// out-of-range elements are zero.
 template <typename T, int MODE, bool GATED, int R, int BK, int LDK, int NT>
-__device__ __forceinline__ void load_tile(const GemmOperand& op, const T* base, const T* ybase,
-                                          T* lds, int r0, int k0, int rext, int kext) {
-  constexpr int VE = TypeTraits<T>::VE;
-  constexpr int KP = TypeTraits<T>::KP;
-  const int tid = threadIdx.x;
-  if constexpr (MODE == KC_VEC || MODE == KC_ELEM) {
-    // view row = tile row, view column = k
-    constexpr int CPR = BK / VE;  // 16-byte chunks per tile row
-    constexpr int CHUNKS = R * CPR;
+struct TileLoader {
+  static constexpr int VE = TypeTraits<T>::VE;
+  static constexpr int KP = TypeTraits<T>::KP;
+  static constexpr bool MCV = MODE == MC_VEC;
+  // KC_* and MC_ELEM: one 16-byte vector per unit; MC_VEC: KP vectors per unit
+  static constexpr int UNITS = MCV ? (BK / KP) * (R / VE) : R * (BK / VE);
+  static constexpr int PER = (UNITS + NT - 1) / NT;
+  static constexpr int RPU = MCV ? KP : 1;
+  u32x4 v[PER * RPU];
+
+  __device__ __forceinline__ void load(const GemmOperand& op, const T* base, const T* ybase, int r0,
+                                       int k0, int rext, int kext) {
+    const int tid = threadIdx.x;
 #pragma unroll
-    for (int c = tid; c < CHUNKS; c += NT) {
-      const int r = c / CPR;
-      const int kc = (c % CPR) * VE;
-      const int gr = r0 + r, gk = k0 + kc;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (gr < rext) {
-        const int64_t rowoff = gather(op.ridx, gr) * op.ld;
-        if (MODE == KC_VEC && gk + VE <= kext) {
-          v = load_vec<T, GATED>(op, base, ybase, rowoff + gk);
-        } else {
-          T* vv = reinterpret_cast<T*>(&v);
+    for (int p = 0; p < PER; ++p) {
+      const int u = tid + p * NT;
 #pragma unroll
-          for (int e = 0; e < VE; ++e)
-            if (gk + e < kext) vv[e] = load_elem<T, GATED>(op, base, ybase, rowoff + gather(op.cidx, gk + e));
-        }
-      }
-      *reinterpret_cast<u32x4*>(lds + r * LDK + kc) = v;
-    }
-  } else if constexpr (MODE == MC_VEC) {
-    // view row = k, view column = tile row; KP k-rows x VE columns per unit,
-    // transposed into VE 32-bit LDS words. k runs fastest across threads so
-    // that one wave's LDS writes of a column land in distinct banks.
-    constexpr int KU = BK / KP;     // k units per column chunk
-    constexpr int CC = R / VE;      // column chunks
-    constexpr int UNITS = KU * CC;
-#pragma unroll
-    for (int u = tid; u < UNITS; u += NT) {
-      const int kp = (u % KU) * KP;
-      const int rc = (u / KU) * VE;
-      const int gk = k0 + kp, gr = r0 + rc;
-      u32x4 rows[KP];
-#pragma unroll
-      for (int q = 0; q < KP; ++q) {
-        rows[q] = u32x4{0u, 0u, 0u, 0u};
-        if (gk + q < kext) {
-          const int64_t rowoff = gather(op.ridx, gk + q) * op.ld;
-          if (gr + VE <= rext) {
-            rows[q] = load_vec<T, GATED>(op, base, ybase, rowoff + gr);
+      for (int q = 0; q < RPU; ++q) v[p * RPU + q] = u32x4{0u, 0u, 0u, 0u};
+      if (UNITS % NT != 0 && u >= UNITS) continue;
+      if constexpr (MODE == KC_VEC || MODE == KC_ELEM) {
+        constexpr int CPR = BK / VE;
+        const int r = u / CPR, kc = (u % CPR) * VE;
+        const int gr = r0 + r, gk = k0 + kc;
+        if (gr < rext) {
+          const int64_t rowoff = gather(op.ridx, gr) * op.ld;
+          if (MODE == KC_VEC && gk + VE <= kext) {
+            v[p] = load_vec<T, GATED>(op, base, ybase, rowoff + gk);
           } else {
-            T* vv = reinterpret_cast<T*>(&rows[q]);
+            T* vv = reinterpret_cast<T*>(&v[p]);
 #pragma unroll
             for (int e = 0; e < VE; ++e)
-              if (gr + e < rext) vv[e] = load_elem<T, GATED>(op, base, ybase, rowoff + gr + e);
+              if (gk + e < kext) vv[e] = load_elem<T, GATED>(op, base, ybase, rowoff + gather(op.cidx, gk + e));
           }
         }
-      }
+      } else if constexpr (MODE == MC_VEC) {
+        // k runs fastest across threads so that the transposed 32-bit LDS
+        // writes of one wave land in distinct banks
+        constexpr int KU = BK / KP;
+        const int kp = (u % KU) * KP, rc = (u / KU) * VE;
+        const int gk = k0 + kp, gr = r0 + rc;
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        uint32_t word;
-        if constexpr (KP == 1) {
-          word = rows[0][e];
-        } else {
-          const uint16_t* r0p = reinterpret_cast<const uint16_t*>(&rows[0]);
-          const uint16_t* r1p = reinterpret_cast<const uint16_t*>(&rows[1]);
-          word = static_cast<uint32_t>(r0p[e]) | (static_cast<uint32_t>(r1p[e]) << 16);
+        for (int q = 0; q < KP; ++q) {
+          if (gk + q < kext) {
+            const int64_t rowoff = gather(op.ridx, gk + q) * op.ld;
+            if (gr + VE <= rext) {
+              v[p * KP + q] = load_vec<T, GATED>(op, base, ybase, rowoff + gr);
+            } else {
+              T* vv = reinterpret_cast<T*>(&v[p * KP + q]);
+#pragma unroll
+              for (int e = 0; e < VE; ++e)
+                if (gr + e < rext) vv[e] = load_elem<T, GATED>(op, base, ybase, rowoff + gr + e);
+            }
+          }
         }
-        *reinterpret_cast<uint32_t*>(lds + (rc + e) * LDK + kp) = word;
-      }
-    }
-  } else {  // MC_ELEM: each thread gathers VE consecutive k of one tile row
-    constexpr int CPR = BK / VE;
-    constexpr int CHUNKS = R * CPR;
+      } else {  // MC_ELEM: VE consecutive k of one tile row
+        const int r = u % R, kc = (u / R) * VE;
+        const int gr = r0 + r, gk = k0 + kc;
+        if (gr < rext) {
+          const int64_t coloff = gather(op.cidx, gr);
+          T* vv = reinterpret_cast<T*>(&v[p]);
 #pragma unroll
-    for (int c = tid; c < CHUNKS; c += NT) {
-      const int r = c % R;
-      const int kc = (c / R) * VE;
-      const int gr = r0 + r, gk = k0 + kc;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (gr < rext) {
-        const int64_t coloff = gather(op.cidx, gr);
-        T* vv = reinterpret_cast<T*>(&v);
-#pragma unroll
-        for (int e = 0; e < VE; ++e)
-          if (gk + e < kext)
-            vv[e] = load_elem<T, GATED>(op, base, ybase, gather(op.ridx, gk + e) * op.ld + coloff);
+          for (int e = 0; e < VE; ++e)
+            if (gk + e < kext) vv[e] = load_elem<T, GATED>(op, base, ybase, gather(op.ridx, gk + e) * op.ld + coloff);
+        }
       }
-      *reinterpret_cast<u32x4*>(lds + r * LDK + kc) = v;
     }
   }
+
+  __device__ __forceinline__ void store(T* lds) const {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int u = tid + p * NT;
+      if (UNITS % NT != 0 && u >= UNITS) continue;
+      if constexpr (MODE == KC_VEC || MODE == KC_ELEM) {
+        constexpr int CPR = BK / VE;
+        *reinterpret_cast<u32x4*>(lds + (u / CPR) * LDK + (u % CPR) * VE) = v[p];
+      } else if constexpr (MODE == MC_VEC) {
+        constexpr int KU = BK / KP;
+        const int kp = (u % KU) * KP, rc = (u / KU) * VE;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          uint32_t word;
+          if constexpr (KP == 1) {
+            word = v[p][e];
+          } else {
+            const uint16_t* a = reinterpret_cast<const uint16_t*>(&v[p * KP]);
+            const uint16_t* b = reinterpret_cast<const uint16_t*>(&v[p * KP + 1]);
+            word = static_cast<uint32_t>(a[e]) | (static_cast<uint32_t>(b[e]) << 16);
+          }
+          *reinterpret_cast<uint32_t*>(lds + (rc + e) * LDK + kp) = word;
+        }
+      } else {
+        *reinterpret_cast<u32x4*>(lds + (u % R) * LDK + (u / R) * VE) = v[p];
+      }
+    }
+  }
+};
+
+// One-shot load of a tile into LDS (load then store).
+template <typename T, int MODE, bool GATED, int R, int BK, int LDK, int NT>
+__device__ __forceinline__ void load_tile(const GemmOperand& op, const T* base, const T* ybase, T* lds,
+                                          int r0, int k0, int rext, int kext) {
+  TileLoader<T, MODE, GATED, R, BK, LDK, NT> t;
+  t.load(op, base, ybase, r0, k0, rext, kext);
+  t.store(lds);
 }
 
 template <int BM_, int BN_, int BK_, int WGM_, int WGN_>
@@ -284,13 +307,41 @@ __device__ __forceinline__ void mma_slab(const T* As, const T* Bs, f32x16 (&acc)
   }
 }
 
-// Writes the accumulators through the epilogue. Output element (m, n) goes to
+// Applies the epilogue to one accumulator value of compact element (m, n).
+template <int EPI>
+__device__ __forceinline__ float epilogue(const GemmOutput& c, float v, float bias) {
+  if constexpr (EPI == EPI_FWD) {
+    v += bias;
+    if (c.relu) v = v > 0.0f ? v : 0.0f;
+    v *= c.scale;
+  }
+  return v;
+}
+
+// Writes the accumulators through the epilogue (splits == 1) or as raw fp32
+// partial sums (splits > 1). Output element (m, n) goes to
 // c.p[ridx(m) * ld + cidx(n)] of the batch entry.
 template <typename OutT, class Cfg, int EPI>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, f32x16 (&acc)[Cfg::FM][Cfg::FN],
-                                           int m0, int n0, int wm, int wn, int64_t bz) {
+                                           int m0, int n0, int wm, int wn, int64_t bz, int split) {
   const int lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
+  if (g.splits > 1) {
+    float* part = g.partial + (bz * g.splits + split) * static_cast<int64_t>(g.M) * g.N;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * Cfg::TM + 32 * i + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (m >= g.M) continue;
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j) {
+          const int n = n0 + wn * Cfg::TN + 32 * j + lr;
+          if (n < g.N) part[static_cast<int64_t>(m) * g.N + n] = acc[i][j][r];
+        }
+      }
+    return;
+  }
   OutT* out = static_cast<OutT*>(g.c.p) + bz * g.c.bstride;
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i) {
@@ -299,21 +350,12 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, f32x16 (&acc)[Cfg:
       const int m = m0 + wm * Cfg::TM + 32 * i + 8 * (r >> 2) + 4 * lh + (r & 3);
       if (m >= g.M) continue;
       const int64_t orow = gather(g.c.ridx, m);
-      float bias = 0.0f;
-      if constexpr (EPI == EPI_FWD) {
-        if (g.c.bias) bias = g.c.bias[orow];
-      }
+      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int n = n0 + wn * Cfg::TN + 32 * j + lr;
         if (n >= g.N) continue;
-        float v = acc[i][j][r];
-        if constexpr (EPI == EPI_FWD) {
-          v += bias;
-          if (g.c.relu) v = v > 0.0f ? v : 0.0f;
-          v *= g.c.scale;
-        }
-        out[orow * g.c.ld + gather(g.c.cidx, n)] = from_f32<OutT>(v);
+        out[orow * g.c.ld + gather(g.c.cidx, n)] = from_f32<OutT>(epilogue<EPI>(g.c, acc[i][j][r], bias));
       }
     }
   }
@@ -322,12 +364,14 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, f32x16 (&acc)[Cfg:
 template <typename T, typename OutT, class Cfg, int AMODE, int BMODE, bool AGATE, bool BGATE, int EPI>
 __global__ void __launch_bounds__(Cfg::NT) gemm_kernel(GemmArgs g) {
   constexpr int LDK = Cfg::BK + 16 / sizeof(T);
-  __shared__ __attribute__((aligned(16))) T As[Cfg::BM * LDK];
-  __shared__ __attribute__((aligned(16))) T Bs[Cfg::BN * LDK];
+  __shared__ __attribute__((aligned(16))) T As[2][Cfg::BM * LDK];
+  __shared__ __attribute__((aligned(16))) T Bs[2][Cfg::BN * LDK];
 
   const int n0 = blockIdx.x * Cfg::BN;
   const int m0 = blockIdx.y * Cfg::BM;
-  const int64_t bz = blockIdx.z;
+  const int splits = g.splits > 1 ? g.splits : 1;
+  const int64_t bz = blockIdx.z / splits;
+  const int split = blockIdx.z % splits;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
 
@@ -344,29 +388,72 @@ __global__ void __launch_bounds__(Cfg::NT) gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // slabs q = kb * nks + ks over the kbatch x ceil(K / BK) contraction
+  const int nks = (g.K + Cfg::BK - 1) / Cfg::BK;
   const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
-  for (int kb = 0; kb < kbatch; ++kb) {
-    const T* ab = abase + kb * g.a.kbstride;
-    const T* aby = AGATE ? aybase + kb * g.a.kbstride : nullptr;
-    const T* bb = bbase + kb * g.b.kbstride;
-    const T* bby = BGATE ? bybase + kb * g.b.kbstride : nullptr;
-    for (int k0 = 0; k0 < g.K; k0 += Cfg::BK) {
-      load_tile<T, AMODE, AGATE, Cfg::BM, Cfg::BK, LDK, Cfg::NT>(g.a, ab, aby, As, m0, k0, g.M, g.K);
-      load_tile<T, BMODE, BGATE, Cfg::BN, Cfg::BK, LDK, Cfg::NT>(g.b, bb, bby, Bs, n0, k0, g.N, g.K);
-      __syncthreads();
-      mma_slab<T, Cfg, LDK>(As, Bs, acc, wm, wn);
-      __syncthreads();
-    }
+  const int nslab = kbatch * nks;
+  const int q0 = static_cast<int>((static_cast<int64_t>(nslab) * split) / splits);
+  const int q1 = static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits);
+
+  TileLoader<T, AMODE, AGATE, Cfg::BM, Cfg::BK, LDK, Cfg::NT> la;
+  TileLoader<T, BMODE, BGATE, Cfg::BN, Cfg::BK, LDK, Cfg::NT> lb;
+  auto load = [&](int q) {
+    const int kb = q / nks, k0 = (q % nks) * Cfg::BK;
+    la.load(g.a, abase + kb * g.a.kbstride, AGATE ? aybase + kb * g.a.kbstride : nullptr, m0, k0, g.M, g.K);
+    lb.load(g.b, bbase + kb * g.b.kbstride, BGATE ? bybase + kb * g.b.kbstride : nullptr, n0, k0, g.N, g.K);
+  };
+
+  if (q0 < q1) {
+    load(q0);
+    la.store(As[0]);
+    lb.store(Bs[0]);
   }
-  store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz);
+  __syncthreads();
+  for (int q = q0; q < q1; ++q) {
+    const int cur = (q - q0) & 1;
+    const bool more = q + 1 < q1;
+    if (more) load(q + 1);
+    mma_slab<T, Cfg, LDK>(As[cur], Bs[cur], acc, wm, wn);
+    if (more) {
+      la.store(As[cur ^ 1]);
+      lb.store(Bs[cur ^ 1]);
+    }
+    __syncthreads();
+  }
+  store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
 }
 
-// Host-side launch of one instantiation over an (N/BN, M/BM, batch) grid.
+// Sums the split partials of every compact element in fixed split order and
+// applies the epilogue.
+template <typename OutT, int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs g) {
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= mn) return;
+  const int64_t bz = blockIdx.y;
+  const float* part = g.partial + bz * g.splits * mn + e;
+  float v = 0.0f;
+  for (int s = 0; s < g.splits; ++s) v += part[s * mn];
+  const int64_t m = e / g.N, n = e % g.N;
+  const int64_t orow = gather(g.c.ridx, m);
+  const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
+  OutT* out = static_cast<OutT*>(g.c.p) + bz * g.c.bstride;
+  out[orow * g.c.ld + gather(g.c.cidx, n)] = from_f32<OutT>(epilogue<EPI>(g.c, v, bias));
+}
+
+// Host-side launch of one instantiation over an (N/BN, M/BM, batch x splits)
+// grid, followed by the reduction when the contraction is split.
 template <typename T, typename OutT, class Cfg, int AMODE, int BMODE, bool AGATE, bool BGATE, int EPI>
 inline hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t stream) {
-  dim3 grid((g.N + Cfg::BN - 1) / Cfg::BN, (g.M + Cfg::BM - 1) / Cfg::BM, batch);
-  hipLaunchKernelGGL((gemm_kernel<T, OutT, Cfg, AMODE, BMODE, AGATE, BGATE, EPI>), grid,
-                     dim3(Cfg::NT), 0, stream, g);
+  const int splits = g.splits > 1 ? g.splits : 1;
+  dim3 grid((g.N + Cfg::BN - 1) / Cfg::BN, (g.M + Cfg::BM - 1) / Cfg::BM, batch * splits);
+  hipLaunchKernelGGL((gemm_kernel<T, OutT, Cfg, AMODE, BMODE, AGATE, BGATE, EPI>), grid, dim3(Cfg::NT), 0,
+                     stream, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+  hipLaunchKernelGGL((splitk_reduce_kernel<OutT, EPI>), dim3(static_cast<unsigned>((mn + 255) / 256), batch),
+                     dim3(256), 0, stream, g);
   return hipGetLastError();
 }
 
@@ -384,31 +471,65 @@ inline hipError_t dispatch_gemm(const GemmArgs& g, int batch, bool a_vec, bool b
   return launch_gemm<T, OutT, Cfg, A1, B1, AGATE, BGATE, EPI>(g, batch, stream);
 }
 
-// Tile shapes: 128x128 output tiles for large problems, 64x64 when the large
-// tiles would leave most of the 256 compute units idle.
+// Tile shapes: 128x128 output tiles for large problems, 64x64 otherwise.
 template <typename T>
 struct GemmCfgs;
 template <>
 struct GemmCfgs<bf16> {
-  using Big = TileCfg<128, 128, 32, 2, 2>;
-  using Small = TileCfg<64, 64, 32, 2, 2>;
+  using Big = TileCfg<128, 128, 64, 2, 2>;
+  using Small = TileCfg<64, 64, 64, 2, 2>;
 };
 template <>
 struct GemmCfgs<float> {
-  using Big = TileCfg<128, 128, 16, 2, 2>;
-  using Small = TileCfg<64, 64, 16, 2, 2>;
+  using Big = TileCfg<128, 128, 32, 2, 2>;
+  using Small = TileCfg<64, 64, 32, 2, 2>;
 };
 
-inline bool use_big_tiles(int M, int N, int batch) {
-  const int64_t big = static_cast<int64_t>((M + 127) / 128) * ((N + 127) / 128) * batch;
-  return big >= 160;
+constexpr int kTargetBlocks = 256;   // one workgroup per compute unit
+constexpr int kMaxSplits = 16;
+constexpr int kMinSlabsPerSplit = 4;
+
+struct GemmPlan {
+  bool big;
+  int splits;
+};
+
+// Picks the tile shape and the split of the contraction for a problem.
+template <typename T>
+inline GemmPlan plan_gemm(int M, int N, int K, int kbatch, int batch) {
+  using C = GemmCfgs<T>;
+  const int64_t big_tiles = static_cast<int64_t>((M + C::Big::BM - 1) / C::Big::BM) *
+                            ((N + C::Big::BN - 1) / C::Big::BN) * batch;
+  GemmPlan p;
+  p.big = big_tiles >= kTargetBlocks / 2;
+  const int bm = p.big ? C::Big::BM : C::Small::BM, bn = p.big ? C::Big::BN : C::Small::BN;
+  const int bk = p.big ? C::Big::BK : C::Small::BK;
+  const int64_t tiles = static_cast<int64_t>((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch;
+  const int64_t slabs = static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk);
+  int s = 1;
+  while (tiles * s * 2 <= kTargetBlocks && slabs / (s * 2) >= kMinSlabsPerSplit && s * 2 <= kMaxSplits) s *= 2;
+  p.splits = s;
+  return p;
 }
 
+// fp32 elements of split-K partials a problem needs (0 when it is not split).
+template <typename T>
+inline size_t gemm_partial_floats(int M, int N, int K, int kbatch, int batch) {
+  const GemmPlan p = plan_gemm<T>(M, N, K, kbatch, batch);
+  return p.splits > 1 ? static_cast<size_t>(p.splits) * batch * M * N : 0;
+}
+
+// Runs a gathered GEMM. `partial` must hold gemm_partial_floats() floats when
+// that is nonzero; with partial == NULL the contraction is never split.
 template <typename T, typename OutT, int A0, int A1, int B0, int B1, bool AGATE, bool BGATE, int EPI>
-inline hipError_t run_gemm(const GemmArgs& g, int batch, bool a_vec, bool b_vec,
-                           hipStream_t stream) {
+inline hipError_t run_gemm(GemmArgs g, int batch, bool a_vec, bool b_vec, hipStream_t stream,
+                           float* partial = nullptr) {
   if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
-  if (use_big_tiles(g.M, g.N, batch))
+  GemmPlan p = plan_gemm<T>(g.M, g.N, g.K, g.kbatch, batch);
+  if (!partial) p.splits = 1;
+  g.splits = p.splits;
+  g.partial = partial;
+  if (p.big)
     return dispatch_gemm<T, OutT, typename GemmCfgs<T>::Big, A0, A1, B0, B1, AGATE, BGATE, EPI>(
         g, batch, a_vec, b_vec, stream);
   return dispatch_gemm<T, OutT, typename GemmCfgs<T>::Small, A0, A1, B0, B1, AGATE, BGATE, EPI>(

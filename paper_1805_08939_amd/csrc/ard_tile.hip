@@ -184,7 +184,7 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_kernel(TdpArgs a) {
     st.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(tn) * T_ * a.K + static_cast<int64_t>(tk) * T_;
     st.c.ld = a.K;
   }
-  store_tile<OutT, Cfg, EPI_FWD>(st, acc, 0, n0, wm, wn, 0);
+  store_tile<OutT, Cfg, EPI_FWD>(st, acc, 0, n0, wm, wn, 0, 0);
 }
 
 // ZERO mode: clears every dropped tile of dW.

@@ -61,3 +61,10 @@ def compare(got, want, norm, rel_tol, what):
     assert comp <= rel_tol, f"{what}: componentwise error {comp:.3e} > {rel_tol}"
     assert normwise <= rel_tol, f"{what}: normwise error {normwise:.3e} > {rel_tol}"
     return comp, normwise
+
+
+def workspace(nbytes):
+    """A device workspace of at least nbytes (None when nothing is needed)."""
+    if nbytes == 0:
+        return None
+    return torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=device())

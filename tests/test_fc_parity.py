@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import compare, device, f64, row_plan, to_dev, tol, ard_dtype
+from gpu_util import ard_dtype, compare, device, f64, row_plan, to_dev, tol, workspace
 from oracle import fc as ofc
 from oracle import patterns as opat
 from oracle import prng as oprng
@@ -58,10 +58,23 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
     dW = torch.full((N, K), fill, dtype=torch.float32, device=device())
     db = torch.full((N,), fill, dtype=torch.float32, device=device())
 
-    api.ard_fc_fwd(desc, Xt, Wd, bd, Yt)
-    api.ard_fc_bwd_data(desc, dYt, Yst, Wd, dXt)
-    api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dW, db)
+    ws = workspace(api.ard_fc_workspace_bytes(desc))
+    api.ard_fc_fwd(desc, Xt, Wd, bd, Yt, ws)
+    api.ard_fc_bwd_data(desc, dYt, Yst, Wd, dXt, ws)
+    api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dW, db, ws)
     torch.cuda.synchronize()
+    if pin != (1, 0) and not poison:
+        # the same layer with the caller compacting W once: bitwise identical
+        cdesc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped,
+                            api.ARD_WEIGHTS_COMPACT)
+        Wc = torch.empty(max(api.ard_fc_compact_bytes(cdesc), 16) // 2, dtype=torch.int16, device=device())
+        api.ard_fc_compact_weights(cdesc, Wd, Wc)
+        cws = workspace(api.ard_fc_workspace_bytes(cdesc))
+        Yt2, dXt2 = Yt.clone(), dXt.clone()
+        api.ard_fc_fwd(cdesc, Xt, Wc, bd, Yt2, cws)
+        api.ard_fc_bwd_data(cdesc, dYt, Yst, Wc, dXt2, cws)
+        torch.cuda.synchronize()
+        assert torch.equal(Yt2, Yt) and torch.equal(dXt2, dXt)
 
     Xa, Wa = np.abs(f64(X) * m_in[None, :]), np.abs(f64(W))
     G = ofc.fc_output_grad(f64(Ys), f64(dY), m_out, scale, act)
@@ -157,6 +170,15 @@ def test_invalid_arguments_are_rejected_before_launch():
     good = api.fc_desc(api.ARD_F32, 8, 16, 8)
     with pytest.raises(api.ArdError):
         api.ard_fc_fwd(good, None, W, None, Y)
+    # a layer whose small output grid splits the contraction needs its workspace
+    big_k = api.fc_desc(api.ARD_F32, 8, 4096, 8)
+    assert api.ard_fc_workspace_bytes(big_k) > 0
+    Xk, Wk = torch.zeros(4096, 8, device=d), torch.zeros(8, 4096, device=d)
+    with pytest.raises(api.ArdError) as e:
+        api.ard_fc_fwd(big_k, Xk, Wk, None, Y)
+    assert e.value.status == 5
+    with pytest.raises(api.ArdError):
+        api.ard_fc_fwd(api.fc_desc(api.ARD_F32, 8, 16, 8, weight_layout=3), X, W, None, Y)
     with pytest.raises(api.ArdError):
         api.ard_fc_fwd(good, X[:, 1:].contiguous().view(-1)[1:], W, None, Y)  # misaligned
     with pytest.raises(api.ArdError):
