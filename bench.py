@@ -126,12 +126,15 @@ class Mlp:
 
         for l in range(self.L):
             call("fwd", l, lambda l=l: api.ard_fc_fwd(self.cdescs[l], acts[l], Wf[l], self.bias[l], self.Y[l], ws))
+        # backward: each bwd_data also applies the ReLU derivative of the layer
+        # below (Xgate = that layer's output), so every dY[l] below the top is
+        # already gated and is passed with Yt = None
         for l in reversed(range(self.L)):
-            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.descs[l], acts[l], self.dY[l],
-                                                                     self.Y[l], self.dW[l], self.db[l], ws))
+            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.cdescs[l], acts[l], self.dY[l],
+                                                                     None, self.dW[l], self.db[l], ws))
             if l > 0:
-                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], self.dY[l], self.Y[l],
-                                                                     Wf[l], self.dY[l - 1], ws))
+                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], self.dY[l], None,
+                                                                     Wf[l], self.dY[l - 1], ws, Xgate=acts[l]))
         return pats
 
     # ------------------------------------------------------------------ oracle

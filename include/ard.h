@@ -251,9 +251,16 @@ size_t ard_fc_workspace_bytes(const ard_fc_desc* desc);
 
 int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias,
                void* Yt, void* ws, size_t ws_bytes, void* stream);
-/* Yt: the forward output (for the ReLU gate), may be NULL when act == NONE. */
+/*
+ * Backward gating. With act == ARD_ACT_RELU the output derivative is gated by
+ * [Yt > 0], Yt being the stored forward output. Yt == NULL means dYt is
+ * already gated (for instance written by the layer above through Xgate) and is
+ * used as is. Xgate (optional, [K][B], dtype) is this layer's input as
+ * produced by a ReLU: when given, dXt is multiplied by [Xgate > 0], so that it
+ * is directly the gated gradient of the layer below. Both gates are 0/1.
+ */
 int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
-                    void* dXt, void* ws, size_t ws_bytes, void* stream);
+                    void* dXt, const void* Xgate, void* ws, size_t ws_bytes, void* stream);
 /* dbias may be NULL. */
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
                       float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);

@@ -85,8 +85,8 @@ SIGNATURES = {
     "ard_fc_compact_weights": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp]),
     "ard_fc_workspace_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
-    "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size,
-                                       c_vp]),
+    "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                       c_size, c_vp]),
     "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                          c_size, c_vp]),
     "ard_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),

@@ -188,10 +188,10 @@ def ard_fc_fwd(desc, Xt, W, bias, Yt, ws=None, stream=None):
                                  _stream(stream)))
 
 
-def ard_fc_bwd_data(desc, dYt, Yt, W, dXt, ws=None, stream=None):
+def ard_fc_bwd_data(desc, dYt, Yt, W, dXt, ws=None, stream=None, Xgate=None):
     p, n = _ws(ws)
-    _check(_ffi.lib().ard_fc_bwd_data(ctypes.byref(desc), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt), p, n,
-                                      _stream(stream)))
+    _check(_ffi.lib().ard_fc_bwd_data(ctypes.byref(desc), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt),
+                                      _ptr(Xgate), p, n, _stream(stream)))
 
 
 def ard_fc_bwd_weight(desc, Xt, dYt, Yt, dW, dbias, ws=None, stream=None):

@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include "ard_gemm.hpp"
+#include "ard_gemm_fast.hpp"
 #include "ard_internal.hpp"
 
 namespace ard {
@@ -137,11 +138,24 @@ size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 size_t compact_bytes(const FcShape& s) { return static_cast<size_t>(s.kout) * s.ldc * s.esize; }
 
+// Split-K partial floats of one problem under whichever kernel may run it.
+template <typename T>
+size_t problem_partials(int M, int N, int K) {
+  size_t f = gemm_partial_floats<T>(M, N, K, 1, 1);
+  if (sizeof(T) == 2) {
+    const size_t h = fast_partial_floats(M, N, K, 1, 1);
+    f = f > h ? f : h;
+  }
+  return f;
+}
+
 template <typename T>
 size_t partial_bytes(const FcShape& s) {
-  size_t f = gemm_partial_floats<T>(s.kout, s.B, s.kin, 1, 1);                  // fwd
-  f = f > gemm_partial_floats<T>(s.kin, s.B, s.kout, 1, 1) ? f : gemm_partial_floats<T>(s.kin, s.B, s.kout, 1, 1);
-  f = f > gemm_partial_floats<T>(s.kout, s.kin, s.B, 1, 1) ? f : gemm_partial_floats<T>(s.kout, s.kin, s.B, 1, 1);
+  size_t f = problem_partials<T>(s.kout, s.B, s.kin);                 // fwd
+  const size_t d = problem_partials<T>(s.kin, s.B, s.kout);           // bwd_data
+  const size_t w = problem_partials<T>(s.kout, s.kin, s.B);           // bwd_weight
+  f = f > d ? f : d;
+  f = f > w ? f : w;
   return 4 * f;
 }
 
@@ -216,8 +230,12 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
   const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-      g, 1, a_vec, b_vec, stream, wv.partial)));
+  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
+    ARD_HIP_CHECK((run_fast_gemm<false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+        g, 1, a_vec, b_vec, stream, wv.partial)));
+  }
   if (d->dropped == ARD_DROPPED_ZERO && s.out_period > 1) {
     hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.N), dim3(256), 0, stream,
                        static_cast<T*>(Yt), static_cast<int64_t>(s.B), s.B, s.out_period,
@@ -229,7 +247,7 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
 
 template <typename T>
 int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
-                     const void* W, void* dXt, void* ws, hipStream_t stream) {
+                     const void* W, void* dXt, const void* Xgate, void* ws, hipStream_t stream) {
   WeightView wv;
   int st = weight_view<T>(s, W, ws, stream, &wv);
   if (st != ARD_OK) return st;
@@ -239,14 +257,24 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
   g.a = {wv.p, nullptr, wv.ld, wv.ridx, nullptr, 0, 0, 1.0f, 0};
-  // B(t, n) = dY[out(t)][n] * [Y > 0]: the 0/1 gate keeps bf16 operands exact;
-  // scale is applied to the fp32 accumulators in the epilogue.
-  g.b = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f, 0};
-  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale};
+  // B(t, n) = dY[out(t)][n] * [Y > 0] (no gate when Yt is NULL: dY is already
+  // the gated gradient); the 0/1 gate keeps bf16 operands exact, and scale is
+  // applied to the fp32 accumulators in the epilogue, as is the optional gate
+  // [Xgate > 0] of the layer below.
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
+  g.b = {dYt, gated ? Yt : nullptr, s.B, s.out_idx, nullptr, 0, gated, 1.0f, 0};
+  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale, Xgate};
   const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
-      g, 1, a_vec, b_vec, stream, wv.partial)));
+  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
+    ARD_HIP_CHECK((run_fast_gemm<true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
+  } else if (gated) {
+    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
+        g, 1, a_vec, b_vec, stream, wv.partial)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+        g, 1, a_vec, b_vec, stream, wv.partial)));
+  }
   if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
     hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
                        static_cast<T*>(dXt), static_cast<int64_t>(s.B), s.B, s.in_period,
@@ -263,19 +291,27 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.M = s.kout;
   g.N = s.kin;
   g.K = s.B;
-  g.a = {dYt, Yt, s.B, s.out_idx, nullptr, 0, d->act == ARD_ACT_RELU, 1.0f, 0};
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
+  g.a = {dYt, gated ? Yt : nullptr, s.B, s.out_idx, nullptr, 0, gated, 1.0f, 0};
   g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
   g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
   const bool v = vec_rows(s.B, sizeof(T));
   float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
-  ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
-      g, 1, v, v, stream, partial)));
+  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
+    ARD_HIP_CHECK((run_fast_gemm<false, false, float, EPI_FWD>(g, 1, stream, partial)));
+  } else if (gated) {
+    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
+        g, 1, v, v, stream, partial)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
+        g, 1, v, v, stream, partial)));
+  }
   if (dbias && s.kout > 0) {
     hipLaunchKernelGGL(dbias_kernel<T>, dim3(s.kout), dim3(256), 0, stream,
                        static_cast<const T*>(dYt), static_cast<const T*>(Yt), s.B, s.out_idx,
-                       d->scale, d->act == ARD_ACT_RELU ? 1 : 0, dbias);
+                       d->scale, gated ? 1 : 0, dbias);
     ARD_LAUNCH_CHECK();
   }
   if (d->dropped == ARD_DROPPED_ZERO && (s.out_period > 1 || s.in_period > 1)) {
@@ -369,18 +405,19 @@ int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const flo
 }
 
 int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
-                    void* dXt, void* ws, size_t ws_bytes, void* stream) {
+                    void* dXt, const void* Xgate, void* ws, size_t ws_bytes, void* stream) {
   clear_error();
   FcShape s;
   int st = check_desc(desc, &s);
   if (st != ARD_OK) return st;
   if ((st = check_ptr(dYt, "dYt")) || (st = check_ptr(W, "W")) || (st = check_ptr(dXt, "dXt")))
     return st;
-  if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
+  if (Yt && !aligned16(Yt)) return fail(ARD_ERR_INVALID_ARG, "Yt is not 16-byte aligned");
+  if (Xgate && !aligned16(Xgate)) return fail(ARD_ERR_INVALID_ARG, "Xgate is not 16-byte aligned");
   if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);
-  if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, ws, sm);
-  return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, ws, sm);
+  if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, Xgate, ws, sm);
+  return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, Xgate, ws, sm);
 }
 
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
@@ -391,7 +428,7 @@ int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, 
   if (st != ARD_OK) return st;
   if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(dYt, "dYt")) || (st = check_ptr(dW, "dW")))
     return st;
-  if (desc->act == ARD_ACT_RELU && (st = check_ptr(Yt, "Yt"))) return st;
+  if (Yt && !aligned16(Yt)) return fail(ARD_ERR_INVALID_ARG, "Yt is not 16-byte aligned");
   if (dbias && !aligned16(dbias)) return fail(ARD_ERR_INVALID_ARG, "dbias is not 16-byte aligned");
   if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);

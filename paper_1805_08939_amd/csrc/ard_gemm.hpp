@@ -70,6 +70,8 @@ struct GemmOutput {
   int32_t relu;          // EPI_FWD: apply ReLU
   float scale;           // EPI_FWD: multiply after the activation (also the
                          // dropout scale of the backward passes)
+  const void* gate;      // EPI_FWD: if set, multiply by [gate > 0] at the output
+                         // position (the ReLU derivative of the layer below)
 };
 
 // The contraction runs over kbatch x K: K batch kb reads both operands at
@@ -355,7 +357,11 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, f32x16 (&acc)[Cfg:
       for (int j = 0; j < Cfg::FN; ++j) {
         const int n = n0 + wn * Cfg::TN + 32 * j + lr;
         if (n >= g.N) continue;
-        out[orow * g.c.ld + gather(g.c.cidx, n)] = from_f32<OutT>(epilogue<EPI>(g.c, acc[i][j][r], bias));
+        const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+        float v = epilogue<EPI>(g.c, acc[i][j][r], bias);
+        if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
+          v = 0.0f;
+        out[o] = from_f32<OutT>(v);
       }
     }
   }
@@ -438,7 +444,11 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs g) {
   const int64_t orow = gather(g.c.ridx, m);
   const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
   OutT* out = static_cast<OutT*>(g.c.p) + bz * g.c.bstride;
-  out[orow * g.c.ld + gather(g.c.cidx, n)] = from_f32<OutT>(epilogue<EPI>(g.c, v, bias));
+  const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+  v = epilogue<EPI>(g.c, v, bias);
+  if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
+    v = 0.0f;
+  out[o] = from_f32<OutT>(v);
 }
 
 // Host-side launch of one instantiation over an (N/BN, M/BM, batch x splits)

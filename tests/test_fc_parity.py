@@ -183,3 +183,93 @@ def test_invalid_arguments_are_rejected_before_launch():
         api.ard_fc_fwd(good, X[:, 1:].contiguous().view(-1)[1:], W, None, Y)  # misaligned
     with pytest.raises(api.ArdError):
         api.ard_fc_bwd_data(api.fc_desc(api.ARD_F32, 8, 16, 8, act=api.ARD_ACT_RELU), Y, None, W, X)
+
+
+@pytest.mark.parametrize("shape,pin,pout", [
+    ((256, 1000, 520), (3, 1), (2, 0)),     # gathers both sides, K tail, ragged tiles
+    ((512, 2048, 1536), (1, 0), (5, 4)),    # one-sided, several 256-wide tiles
+    ((128, 4096, 64), (2, 1), (1, 0)),      # tiny output grid: split contraction
+    ((1024, 512, 640), (7, 3), (3, 2)),     # batch-heavy
+])
+def test_bf16_large_tiles(shape, pin, pout):
+    B, K, N = shape
+    X, W, b, dY = make_inputs("bf16", B, K, N, seed=B + K)
+    run_layer("bf16", X, W, b, dY, pin, pout, "relu", 1.0, api.ARD_DROPPED_SKIP, use_null_plans=False,
+              sentinel=-3.0)
+    run_layer("bf16", X, W, b, dY, pin, pout, "none", 2.0, api.ARD_DROPPED_ZERO)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pregated_gradient_and_input_gate(dtype):
+    """Yt = NULL takes dYt as already gated; Xgate gates dXt with [Xgate > 0]."""
+    B, K, N = 128, 264, 192
+    X, W, b, dY = make_inputs(dtype, B, K, N, seed=99)
+    Xr = synth.to_storage(torch.relu(X.float()), dtype)           # a ReLU output as this layer's input
+    m_in, m_out = opat.row_mask(K, 3, 1), opat.row_mask(N, 2, 0)
+    Y64 = ofc.fc_forward(f64(Xr), f64(W), f64(b), m_in, m_out, 1.0, "relu")
+    Ys = synth.to_storage(torch.from_numpy(Y64).float(), dtype)
+    G = synth.to_storage(torch.from_numpy(ofc.fc_output_grad(f64(Ys), f64(dY), m_out, 1.0, "relu")).float(),
+                         dtype)  # exact: dY times a 0/1 gate
+    dX64, dW64, db64 = ofc.fc_backward(f64(Xr), f64(W), f64(Ys), f64(dY), m_in, m_out, 1.0, "relu")
+    in_plan, out_plan = row_plan(K, 3, 1), row_plan(N, 2, 0)
+    desc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, 1.0, api.ARD_ACT_RELU, api.ARD_DROPPED_ZERO)
+    ws = workspace(api.ard_fc_workspace_bytes(desc))
+    Xt, Wd, Gt, Xrt = to_dev(X.T), to_dev(W), to_dev(G.T), to_dev(Xr.T)
+    sdt = synth.storage_dtype(dtype)
+    dXt = torch.empty(K, B, dtype=sdt, device=device())
+    dW = torch.empty(N, K, device=device())
+    db = torch.empty(N, device=device())
+    api.ard_fc_bwd_data(desc, Gt, None, Wd, dXt, ws, Xgate=Xrt)
+    api.ard_fc_bwd_weight(desc, Xrt, Gt, None, dW, db, ws)
+    torch.cuda.synchronize()
+    Ga = np.abs(f64(G))
+    ndX = (Ga @ np.abs(f64(W))) * m_in[None, :]
+    want_dX = dX64 * (f64(Xr) > 0)
+    compare(f64(dXt).T, want_dX, ndX * (f64(Xr) > 0), tol(dtype), "dX gated")
+    compare(f64(dW), dW64, (Ga.T @ np.abs(f64(Xr))) * np.outer(m_out, m_in), tol(dtype), "dW")
+    compare(f64(db), db64, Ga.sum(0), tol(dtype), "db")
+
+
+def test_wide_layer_bf16_full_size_sampled():
+    """One hidden layer of the wide bf16 MLP (8192 -> 8192, batch 2048) under
+    patterns on both sides, in the launch configuration of the benchmark
+    (compact weights, SKIP, workspace), against the oracle on sampled rows and
+    columns. The oracle's forward output, rounded to bf16, is the ReLU gate of
+    both backward implementations."""
+    B, K, N = 2048, 8192, 8192
+    g = synth.generator(1805 + 4)
+    X = synth.to_storage(torch.relu(synth.normal(g, (B, K))), "bf16")
+    W = synth.to_storage(synth.he(g, N, K), "bf16")
+    dY = synth.to_storage(synth.normal(g, (B, N)), "bf16")
+    (pi, oi), (po, oo) = (3, 2), (2, 1)
+    m_in, m_out = opat.row_mask(K, pi, oi), opat.row_mask(N, po, oo)
+    Xf, Wf, dYf = f64(X), f64(W), f64(dY)
+    Y64 = ofc.fc_forward(Xf, Wf, None, m_in, m_out, 1.0, "relu")
+    Ys = synth.to_storage(torch.from_numpy(Y64).float(), "bf16")
+    in_plan, out_plan = row_plan(K, pi, oi), row_plan(N, po, oo)
+    desc = api.fc_desc(api.ARD_BF16, B, K, N, in_plan, out_plan, 1.0, api.ARD_ACT_RELU, api.ARD_DROPPED_SKIP,
+                       api.ARD_WEIGHTS_COMPACT)
+    Xt, Wd, dYt, Yst = to_dev(X.T), to_dev(W), to_dev(dY.T), to_dev(Ys.T)
+    Wc = torch.empty(api.ard_fc_compact_bytes(desc) // 2, dtype=torch.bfloat16, device=device())
+    api.ard_fc_compact_weights(desc, Wd, Wc)
+    ws = workspace(api.ard_fc_workspace_bytes(desc))
+    Yt = torch.zeros(N, B, dtype=torch.bfloat16, device=device())
+    dXt = torch.zeros(K, B, dtype=torch.bfloat16, device=device())
+    dW = torch.zeros(N, K, device=device())
+    api.ard_fc_fwd(desc, Xt, Wc, None, Yt, ws)
+    api.ard_fc_bwd_data(desc, dYt, Yst, Wc, dXt, ws)
+    api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dW, None, ws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    Sin, Sout = np.array(opat.row_kept_list(K, pi, oi)), np.array(opat.row_kept_list(N, po, oo))
+    rows = np.sort(rng.choice(Sout, 40, replace=False))
+    cols = np.sort(rng.choice(Sin, 40, replace=False))
+    Xm = Xf * m_in[None, :]
+    compare(f64(Yt)[rows].T, Y64[:, rows], np.abs(Xm) @ np.abs(Wf[rows]).T, 2e-2, "Y rows")
+    G = ofc.fc_output_grad(f64(Ys), dYf, m_out, 1.0, "relu")        # [B][N]
+    Wk = Wf[:, cols] * m_out[:, None]
+    compare(f64(dXt)[cols].T, G @ Wk, np.abs(G) @ np.abs(Wk), 2e-2, "dX cols")
+    compare(f64(dW)[np.ix_(rows, cols)], G[:, rows].T @ Xf[:, cols],
+            np.abs(G[:, rows]).T @ np.abs(Xf[:, cols]), 2e-2, "dW")
+    dropped_rows = np.setdiff1d(np.arange(N), Sout)[:64]
+    assert not f64(Yt)[dropped_rows].any() and not f64(dW)[dropped_rows].any()
