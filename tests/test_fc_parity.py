@@ -181,8 +181,9 @@ def test_invalid_arguments_are_rejected_before_launch():
         api.ard_fc_fwd(api.fc_desc(api.ARD_F32, 8, 16, 8, weight_layout=3), X, W, None, Y)
     with pytest.raises(api.ArdError):
         api.ard_fc_fwd(good, X[:, 1:].contiguous().view(-1)[1:], W, None, Y)  # misaligned
-    with pytest.raises(api.ArdError):
-        api.ard_fc_bwd_data(api.fc_desc(api.ARD_F32, 8, 16, 8, act=api.ARD_ACT_RELU), Y, None, W, X)
+    relu = api.fc_desc(api.ARD_F32, 8, 16, 8, act=api.ARD_ACT_RELU)
+    with pytest.raises(api.ArdError):  # misaligned input gate
+        api.ard_fc_bwd_data(relu, Y, None, W, X, Xgate=X.view(-1)[1:])
 
 
 @pytest.mark.parametrize("shape,pin,pout", [
