@@ -250,6 +250,8 @@ def main():
     ap.add_argument("--p", type=float, default=0.5, help="dropout rate of the headline value")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of 1 GiB (3 times), the reference for HBM counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
@@ -257,9 +259,17 @@ def main():
         sys.exit(2)
 
     import torch
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": src.numel() * 4, "copies": 3}), flush=True)
+        return
     from paper_1805_08939_amd import _ffi
     _ffi.lib()
-    torch.cuda.set_device(0)
     spec = WORKLOADS[args.workload]
     wl = Mlp(**spec)
     dtype = spec["dtype"]
@@ -301,6 +311,7 @@ def main():
         "speedup_vs_p0": speedup,
         "kept_flop_fraction": kept_frac,
         "per_p": {f"{p}": {"ms_per_step": results[p]["ms"] / args.steps,
+                           "host_ms_per_step": results[p]["wall_s"] * 1e3 / args.steps,
                            "tflops_kept": results[p]["flops"] / (results[p]["ms"] * 1e-3) / 1e12}
                   for p in rates},
         "roofline": roofline,
