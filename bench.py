@@ -66,6 +66,15 @@ class Mlp:
                             for l in range(1, L)]
         self.ws = torch.empty(256 * 128 * 128, dtype=torch.float32, device=dev)
         self.K = None
+        # raw device addresses and the stream handle, resolved once: the step
+        # then costs one C call per launch with no per-call tensor lookups
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.ptr = {
+            "X0": self.X0.data_ptr(), "W": [w.data_ptr() for w in self.W],
+            "Wc": [None] + [w.data_ptr() for w in self.Wc[1:]], "bias": [b.data_ptr() for b in self.bias],
+            "Y": [y.data_ptr() for y in self.Y], "dY": [d.data_ptr() for d in self.dY],
+            "dW": [w.data_ptr() for w in self.dW], "db": [b.data_ptr() for b in self.db],
+            "idx": [i.data_ptr() for i in self.idx]}
 
     def set_rate(self, p):
         api = self.api
@@ -106,15 +115,15 @@ class Mlp:
         return sum(per.values()), per
 
     def step(self, it, timed_call=None, events=None):
-        api = self.api
+        api, P, st = self.api, self.ptr, self.stream
         pats = self.patterns(it)
         for l, (per, off) in enumerate(pats):
-            api.ard_plan_rows(self.dims[l + 1], per, off, self.idx[l], plan=self.plans[l])
+            api.ard_plan_rows(self.dims[l + 1], per, off, P["idx"][l], st, plan=self.plans[l])
         for l in range(1, self.L):
-            api.ard_fc_compact_weights(self.cdescs[l], self.W[l], self.Wc[l])
-        Wf = [self.W[0]] + self.Wc[1:]
-        acts = [self.X0] + self.Y
-        ws = self.ws
+            api.ard_fc_compact_weights(self.cdescs[l], P["W"][l], P["Wc"][l], st)
+        Wf = [P["W"][0]] + P["Wc"][1:]
+        acts = [P["X0"]] + P["Y"]
+        ws = (self.ws.data_ptr(), self.ws.numel() * 4)
 
         def call(kind, l, fn):
             if timed_call == (kind, l):
@@ -125,16 +134,17 @@ class Mlp:
                 fn()
 
         for l in range(self.L):
-            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.cdescs[l], acts[l], Wf[l], self.bias[l], self.Y[l], ws))
+            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.cdescs[l], acts[l], Wf[l], P["bias"][l], P["Y"][l], ws, st))
         # backward: each bwd_data also applies the ReLU derivative of the layer
         # below (Xgate = that layer's output), so every dY[l] below the top is
         # already gated and is passed with Yt = None
         for l in reversed(range(self.L)):
-            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.cdescs[l], acts[l], self.dY[l],
-                                                                     None, self.dW[l], self.db[l], ws))
+            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.cdescs[l], acts[l], P["dY"][l],
+                                                                     None, P["dW"][l], P["db"][l], ws, st))
             if l > 0:
-                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], self.dY[l], None,
-                                                                     Wf[l], self.dY[l - 1], ws, Xgate=acts[l]))
+                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], P["dY"][l], None,
+                                                                     Wf[l], P["dY"][l - 1], ws, st,
+                                                                     Xgate=acts[l]))
         return pats
 
     # ------------------------------------------------------------------ oracle

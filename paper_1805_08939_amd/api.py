@@ -163,7 +163,12 @@ def fc_desc(dtype, batch, in_features, out_features, in_plan=None, out_plan=None
 
 
 def _ws(ws):
-    return (_ptr(ws), ws.numel() * ws.element_size()) if ws is not None else (None, 0)
+    """(pointer, bytes) of a workspace tensor, or of a (pointer, bytes) pair."""
+    if ws is None:
+        return None, 0
+    if isinstance(ws, tuple):
+        return ws
+    return ws.data_ptr(), ws.numel() * ws.element_size()
 
 
 def ard_fc_compact_ld(desc):

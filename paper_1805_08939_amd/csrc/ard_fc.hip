@@ -142,11 +142,8 @@ size_t compact_bytes(const FcShape& s) { return static_cast<size_t>(s.kout) * s.
 template <typename T>
 size_t problem_partials(int M, int N, int K) {
   size_t f = gemm_partial_floats<T>(M, N, K, 1, 1);
-  if (sizeof(T) == 2) {
-    const size_t h = fast_partial_floats(M, N, K, 1, 1);
-    f = f > h ? f : h;
-  }
-  return f;
+  const size_t h = fast_partial_floats<T>(M, N, K, 1, 1);
+  return f > h ? f : h;
 }
 
 template <typename T>
@@ -230,8 +227,8 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
   const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
-    ARD_HIP_CHECK((run_fast_gemm<false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
+  if (fast_ok(g.a, g.b, sizeof(T))) {
+    ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
         g, 1, a_vec, b_vec, stream, wv.partial)));
@@ -266,8 +263,8 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale, Xgate};
   const bool a_vec = vec_rows(wv.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
-    ARD_HIP_CHECK((run_fast_gemm<true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
+  if (fast_ok(g.a, g.b, sizeof(T))) {
+    ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
         g, 1, a_vec, b_vec, stream, wv.partial)));
@@ -299,8 +296,8 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
-  if (sizeof(T) == 2 && fast_ok(g.a, g.b)) {
-    ARD_HIP_CHECK((run_fast_gemm<false, false, float, EPI_FWD>(g, 1, stream, partial)));
+  if (fast_ok(g.a, g.b, sizeof(T))) {
+    ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD>(g, 1, stream, partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
         g, 1, v, v, stream, partial)));

@@ -451,6 +451,112 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs g) {
   out[o] = from_f32<OutT>(v);
 }
 
+// Small output grids: one 32 x 32 output block per workgroup; the four waves
+// take disjoint quarters of every K slab and reduce through LDS, which fills
+// the chip without a second (reduction) launch when M x N is small.
+template <typename T>
+struct SmallCfg {
+  static constexpr int BK = sizeof(T) == 2 ? 128 : 64;
+  static constexpr int LDK = BK + 16 / sizeof(T);
+  static constexpr int QK = BK / 4;  // k per wave per slab
+};
+
+template <typename T, typename OutT, int AMODE, int BMODE, bool AGATE, bool BGATE, int EPI>
+__global__ void __launch_bounds__(256) gemm_small_kernel(GemmArgs g) {
+  using C = SmallCfg<T>;
+  __shared__ __attribute__((aligned(16))) T As[2][32 * C::LDK];
+  __shared__ __attribute__((aligned(16))) T Bs[2][32 * C::LDK];
+  __shared__ float red[4 * 16 * 64];
+  const int n0 = blockIdx.x * 32, m0 = blockIdx.y * 32;
+  const int splits = g.splits > 1 ? g.splits : 1;
+  const int64_t bz = blockIdx.z / splits;
+  const int split = blockIdx.z % splits;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lr = lane & 31, lh = lane >> 5;
+
+  const T* abase = static_cast<const T*>(g.a.p) + bz * g.a.bstride;
+  const T* aybase = AGATE ? static_cast<const T*>(g.a.y) + bz * g.a.bstride : nullptr;
+  const T* bbase = static_cast<const T*>(g.b.p) + bz * g.b.bstride;
+  const T* bybase = BGATE ? static_cast<const T*>(g.b.y) + bz * g.b.bstride : nullptr;
+
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+
+  const int nks = (g.K + C::BK - 1) / C::BK;
+  const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
+  const int nslab = kbatch * nks;
+  const int q0 = static_cast<int>((static_cast<int64_t>(nslab) * split) / splits);
+  const int q1 = static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits);
+
+  TileLoader<T, AMODE, AGATE, 32, C::BK, C::LDK, 256> la;
+  TileLoader<T, BMODE, BGATE, 32, C::BK, C::LDK, 256> lb;
+  auto load = [&](int q) {
+    const int kb = q / nks, k0 = (q % nks) * C::BK;
+    la.load(g.a, abase + kb * g.a.kbstride, AGATE ? aybase + kb * g.a.kbstride : nullptr, m0, k0, g.M, g.K);
+    lb.load(g.b, bbase + kb * g.b.kbstride, BGATE ? bybase + kb * g.b.kbstride : nullptr, n0, k0, g.N, g.K);
+  };
+  if (q0 < q1) {
+    load(q0);
+    la.store(As[0]);
+    lb.store(Bs[0]);
+  }
+  __syncthreads();
+  for (int q = q0; q < q1; ++q) {
+    const int cur = (q - q0) & 1;
+    const bool more = q + 1 < q1;
+    if (more) load(q + 1);
+    const T* as = As[cur] + lr * C::LDK + w * C::QK;
+    const T* bs = Bs[cur] + lr * C::LDK + w * C::QK;
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int kk = 0; kk < C::QK; kk += 16) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(as + kk + 8 * lh);
+        const bf16x8 b = *reinterpret_cast<const bf16x8*>(bs + kk + 8 * lh);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < C::QK; kk += 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(as + kk + 4 * lh);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(bs + kk + 4 * lh);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
+      }
+    }
+    if (more) {
+      la.store(As[cur ^ 1]);
+      lb.store(Bs[cur ^ 1]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) red[(w * 16 + r) * 64 + lane] = acc[r];
+  __syncthreads();
+  // wave w finishes accumulator registers 4w..4w+3: rows 8w + 4*lh + q, column lr
+  const int n = n0 + lr;
+  if (n >= g.N) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int m = m0 + 8 * w + 4 * lh + q;
+    if (m >= g.M) continue;
+    float v = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v += red[(u * 16 + 4 * w + q) * 64 + lane];
+    if (splits > 1) {
+      g.partial[(bz * splits + split) * static_cast<int64_t>(g.M) * g.N + static_cast<int64_t>(m) * g.N + n] = v;
+      continue;
+    }
+    const int64_t orow = gather(g.c.ridx, m);
+    const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
+    const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+    v = epilogue<EPI>(g.c, v, bias);
+    if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
+      v = 0.0f;
+    (static_cast<OutT*>(g.c.p) + bz * g.c.bstride)[o] = from_f32<OutT>(v);
+  }
+}
+
 // Host-side launch of one instantiation over an (N/BN, M/BM, batch x splits)
 // grid, followed by the reduction when the contraction is split.
 template <typename T, typename OutT, class Cfg, int AMODE, int BMODE, bool AGATE, bool BGATE, int EPI>
@@ -467,6 +573,29 @@ inline hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t stream) 
   return hipGetLastError();
 }
 
+template <typename T, typename OutT, int AMODE, int BMODE, bool AGATE, bool BGATE, int EPI>
+inline hipError_t launch_small(const GemmArgs& g, int batch, hipStream_t stream) {
+  const int splits = g.splits > 1 ? g.splits : 1;
+  dim3 grid((g.N + 31) / 32, (g.M + 31) / 32, batch * splits);
+  hipLaunchKernelGGL((gemm_small_kernel<T, OutT, AMODE, BMODE, AGATE, BGATE, EPI>), grid, dim3(256), 0, stream, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+  hipLaunchKernelGGL((splitk_reduce_kernel<OutT, EPI>), dim3(static_cast<unsigned>((mn + 255) / 256), batch),
+                     dim3(256), 0, stream, g);
+  return hipGetLastError();
+}
+
+template <typename T, typename OutT, int A0, int A1, int B0, int B1, bool AGATE, bool BGATE, int EPI>
+inline hipError_t dispatch_small(const GemmArgs& g, int batch, bool a_vec, bool b_vec, hipStream_t stream) {
+  if (a_vec) {
+    if (b_vec) return launch_small<T, OutT, A0, B0, AGATE, BGATE, EPI>(g, batch, stream);
+    return launch_small<T, OutT, A0, B1, AGATE, BGATE, EPI>(g, batch, stream);
+  }
+  if (b_vec) return launch_small<T, OutT, A1, B0, AGATE, BGATE, EPI>(g, batch, stream);
+  return launch_small<T, OutT, A1, B1, AGATE, BGATE, EPI>(g, batch, stream);
+}
+
 // Launches the instantiation matching whether each operand can use 16-byte
 // vector loads (A0/B0) or needs element loads (A1/B1).
 template <typename T, typename OutT, class Cfg, int A0, int A1, int B0, int B1, bool AGATE,
@@ -481,7 +610,7 @@ inline hipError_t dispatch_gemm(const GemmArgs& g, int batch, bool a_vec, bool b
   return launch_gemm<T, OutT, Cfg, A1, B1, AGATE, BGATE, EPI>(g, batch, stream);
 }
 
-// Tile shapes: 128x128 output tiles for large problems, 64x64 otherwise.
+// Tile shapes of the general kernel: 128x128 and 64x64 output tiles.
 template <typename T>
 struct GemmCfgs;
 template <>
@@ -499,22 +628,39 @@ constexpr int kTargetBlocks = 256;   // one workgroup per compute unit
 constexpr int kMaxSplits = 16;
 constexpr int kMinSlabsPerSplit = 4;
 
+enum TileKind { TILE_BIG = 0, TILE_MEDIUM = 1, TILE_SMALL = 2 };
+
 struct GemmPlan {
-  bool big;
+  int kind;
   int splits;
 };
 
-// Picks the tile shape and the split of the contraction for a problem.
+// Picks the tile shape and the split of the contraction for a problem:
+// 128x128 tiles when they fill half the chip, 64x64 when those fill it,
+// otherwise 32x32 blocks with the contraction split inside the workgroup
+// (and over workgroups while the grid stays below one workgroup per CU).
 template <typename T>
 inline GemmPlan plan_gemm(int M, int N, int K, int kbatch, int batch) {
   using C = GemmCfgs<T>;
-  const int64_t big_tiles = static_cast<int64_t>((M + C::Big::BM - 1) / C::Big::BM) *
-                            ((N + C::Big::BN - 1) / C::Big::BN) * batch;
+  auto tiles_of = [&](int bm, int bn) {
+    return static_cast<int64_t>((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch;
+  };
   GemmPlan p;
-  p.big = big_tiles >= kTargetBlocks / 2;
-  const int bm = p.big ? C::Big::BM : C::Small::BM, bn = p.big ? C::Big::BN : C::Small::BN;
-  const int bk = p.big ? C::Big::BK : C::Small::BK;
-  const int64_t tiles = static_cast<int64_t>((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch;
+  int bk;
+  int64_t tiles;
+  if (tiles_of(C::Big::BM, C::Big::BN) >= kTargetBlocks / 2) {
+    p.kind = TILE_BIG;
+    bk = C::Big::BK;
+    tiles = tiles_of(C::Big::BM, C::Big::BN);
+  } else if (tiles_of(C::Small::BM, C::Small::BN) >= kTargetBlocks) {
+    p.kind = TILE_MEDIUM;
+    bk = C::Small::BK;
+    tiles = tiles_of(C::Small::BM, C::Small::BN);
+  } else {
+    p.kind = TILE_SMALL;
+    bk = SmallCfg<T>::BK;
+    tiles = tiles_of(32, 32);
+  }
   const int64_t slabs = static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk);
   int s = 1;
   while (tiles * s * 2 <= kTargetBlocks && slabs / (s * 2) >= kMinSlabsPerSplit && s * 2 <= kMaxSplits) s *= 2;
@@ -539,11 +685,13 @@ inline hipError_t run_gemm(GemmArgs g, int batch, bool a_vec, bool b_vec, hipStr
   if (!partial) p.splits = 1;
   g.splits = p.splits;
   g.partial = partial;
-  if (p.big)
+  if (p.kind == TILE_BIG)
     return dispatch_gemm<T, OutT, typename GemmCfgs<T>::Big, A0, A1, B0, B1, AGATE, BGATE, EPI>(
         g, batch, a_vec, b_vec, stream);
-  return dispatch_gemm<T, OutT, typename GemmCfgs<T>::Small, A0, A1, B0, B1, AGATE, BGATE, EPI>(
-      g, batch, a_vec, b_vec, stream);
+  if (p.kind == TILE_MEDIUM)
+    return dispatch_gemm<T, OutT, typename GemmCfgs<T>::Small, A0, A1, B0, B1, AGATE, BGATE, EPI>(
+        g, batch, a_vec, b_vec, stream);
+  return dispatch_small<T, OutT, A0, A1, B0, B1, AGATE, BGATE, EPI>(g, batch, a_vec, b_vec, stream);
 }
 
 }  // namespace ard

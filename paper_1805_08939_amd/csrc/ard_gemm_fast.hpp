@@ -1,21 +1,26 @@
-// bf16 gathered GEMM for large compact problems on gfx950.
+// Gathered GEMM with direct global -> LDS loads and a deep K pipeline (gfx950).
 //
-// The same contraction as gemm_kernel (ard_gemm.hpp) with operands that allow
-// 16-byte chunks (rows of a multiple of 8 elements, no column gathers, no
-// load-time gates), shaped for MFMA throughput:
+// The same contraction as gemm_kernel (ard_gemm.hpp) for operand views that
+// can be read in whole 16-byte chunks (row stride a multiple of 16 bytes,
+// aligned base, no column gather, no load-time gate):
 //
 //  * global -> LDS without register staging: each lane issues
 //    global_load_lds_dwordx4 for one 16-byte chunk of a (row-gathered) tile;
 //    a wave writes 64 consecutive LDS chunks, and the lane picks the global
-//    chunk that belongs at its LDS position under an XOR swizzle, which keeps
-//    the MFMA fragment reads free of bank conflicts;
-//  * k-contiguous operands live in LDS as [rows][64 k] and are read with
-//    ds_read_b128; m/n-contiguous operands (feature-major activations,
-//    transposed weights) live as [64 k][rows] exactly as in HBM and are read
-//    with ds_read_b64_tr_b16, whose 16-lane transpose delivers 4 consecutive
-//    k of one column per lane — no transpose pass anywhere;
-//  * two LDS stages of a 64-deep K slab: the loads of slab q+1 are in flight
-//    while the waves run v_mfma_f32_32x32x16_bf16 on slab q;
+//    chunk that belongs at its LDS position under an XOR swizzle that keeps the
+//    MFMA fragment reads free of bank conflicts;
+//  * k-contiguous operands live in LDS as [rows][BK] and are read as whole
+//    fragments (ds_read_b128); m/n-contiguous operands (feature-major
+//    activations, transposed weights) stay [BK][rows] exactly as in HBM: bf16
+//    fragments come from ds_read_b64_tr_b16, whose 16-lane transpose delivers
+//    4 consecutive k of one column per lane, fp32 fragments from one
+//    ds_read_b32 per k (consecutive lanes read consecutive columns);
+//  * STAGES LDS stages: the loads of the next STAGES - 1 slabs are in flight
+//    while the waves run MFMA on the current one; a wave waits only for the
+//    slab it is about to use (vmcnt counts the later slabs it has issued);
+//  * optionally the waves of a workgroup split each slab's k between them and
+//    reduce through LDS at the end (small output tiles that still fill the
+//    chip);
 //  * the last, partial K slab is cleaned in LDS (entries past the contraction
 //    length set to 0) before use; rows past the output extents load a clamped
 //    valid row and their results are discarded.
@@ -28,106 +33,144 @@ namespace ard {
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-template <int BM_, int BN_, int WGM_, int WGN_>
+template <typename T_, int BM_, int BN_, int BK_, int STAGES_, int WGM_, int WGN_, int KSPLIT_>
 struct FastCfg {
-  static constexpr int BM = BM_, BN = BN_, BK = 64, WGM = WGM_, WGN = WGN_;
-  static constexpr int NT = 64 * WGM * WGN, NW = WGM * WGN;
-  static constexpr int TM = BM / WGM, TN = BN / WGN;
-  static constexpr int FM = TM / 32, FN = TN / 32;
+  using T = T_;
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
+  static constexpr int WGM = WGM_, WGN = WGN_, KSPLIT = KSPLIT_;
+  static constexpr int NW = WGM * WGN * KSPLIT, NT = 64 * NW;
+  static constexpr int TM = BM / WGM, TN = BN / WGN;  // wave tile
+  static constexpr int FM = TM / 32, FN = TN / 32;    // 32x32 MFMA blocks per wave
+  static constexpr int KW = BK / KSPLIT;              // k per wave per slab
+  static constexpr int ES = sizeof(T);
+  static constexpr int ABYTES = BM * BK * ES, BBYTES = BN * BK * ES;
+  static constexpr int STAGE = ABYTES + BBYTES;
+  static constexpr int LDS = STAGES * STAGE;
+  // 16-byte load instructions per wave per slab
+  static constexpr int LPW = (ABYTES + BBYTES) / 16 / 64 / NW;
+  static_assert(ABYTES % (1024 * NW) == 0 && BBYTES % (1024 * NW) == 0, "tile must split into wave loads");
+  static_assert(KW % (ES == 2 ? 16 : 8) == 0, "per-wave k must hold whole MFMA steps");
 };
 
-// Byte offsets of 16-byte chunk c of row r. k-contiguous tiles have 8 chunks
-// (64 k) per row, swizzled by row / 2; m/n-contiguous tiles have CPR chunks per
-// k-row, the low three chunk bits swizzled by k. Loads and fragment reads use
-// the same maps.
-__device__ __forceinline__ int kc_chunk(int r, int c) { return (r * 8 + (c ^ ((r >> 1) & 7))) * 16; }
+// Byte offset of 16-byte chunk c of row r. k-contiguous tiles hold CPR = BK*ES/16
+// chunks per row, the chunk index swizzled by row / 2; m/n-contiguous tiles
+// hold CPR = R*ES/16 chunks per k-row, the low three chunk bits (fewer when a
+// row has fewer chunks) swizzled by k.
 template <int CPR>
-__device__ __forceinline__ int mc_chunk(int k, int c) { return (k * CPR + (c ^ (k & 7))) * 16; }
+__device__ __forceinline__ int kc_off(int r, int c) {
+  return (r * CPR + (c ^ ((r >> 1) & (CPR - 1)))) * 16;
+}
+template <int CPR>
+__device__ __forceinline__ int mc_off(int k, int c) {
+  constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
+  return (k * CPR + (c ^ (k & MASK))) * 16;
+}
 
-// Issues this wave's direct loads of one operand tile for the slab at k0.
-//   KC: tile rows r0.. (R of them, gathered by ridx), 64 k per row, LDS [R][64]
-//   MC: tile k-rows k0.. (64, gathered by ridx), R columns, LDS [64][R]
-template <class Cfg, int R, bool MC>
-__device__ __forceinline__ void fast_issue(const bf16* base, int64_t ld, const int32_t* ridx, int r0,
-                                           int rext, int k0, int kext, char* region) {
-  constexpr int CHUNKS = R * 8;                      // R * 64 bf16 / 8 per chunk
-  constexpr int PER_WAVE = CHUNKS / 64 / Cfg::NW;     // load instructions per wave
+// Issues this wave's direct loads of one k-contiguous operand tile for the
+// slab at k0: tile rows r0.. (R of them, gathered by ridx), BK k per row,
+// LDS [R][BK].
+template <class Cfg, int R>
+__device__ __forceinline__ void issue_kc(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
+                                         int k0, int kext, char* region) {
+  using T = typename Cfg::T;
+  const T* base = static_cast<const T*>(vbase);
+  constexpr int ES = Cfg::ES, EPC = 16 / ES;  // elements per chunk
+  constexpr int CPR = Cfg::BK * ES / 16;
+  constexpr int PER_WAVE = R * Cfg::BK * ES / 1024 / Cfg::NW;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
   for (int i = 0; i < PER_WAVE; ++i) {
     const int blk = wave * PER_WAVE + i;
     const int pos = blk * 64 + lane;  // chunk position in the LDS region
-    int64_t off;
-    if constexpr (!MC) {
-      const int r = pos >> 3;
-      const int c = (pos & 7) ^ ((r >> 1) & 7);
-      int row = r0 + r;
-      row = row < rext ? row : rext - 1;
-      int k = k0 + c * 8;
-      k = k < kext ? k : 0;
-      off = gather(ridx, row) * ld + k;
-    } else {
-      constexpr int CPR = R / 8;
-      const int kk = pos / CPR;
-      const int c = (pos % CPR) ^ (kk & 7);
-      int krow = k0 + kk;
-      krow = krow < kext ? krow : kext - 1;
-      int col = r0 + c * 8;
-      col = col < rext ? col : 0;
-      off = gather(ridx, krow) * ld + col;
-    }
-    __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(region + blk * 1024), 16, 0, 0);
+    const int r = pos / CPR;
+    const int c = (pos % CPR) ^ ((r >> 1) & (CPR - 1));
+    int row = r0 + r;
+    row = row < rext ? row : rext - 1;
+    int k = k0 + c * EPC;
+    k = k < kext ? k : 0;
+    __builtin_amdgcn_global_load_lds(base + gather(ridx, row) * ld + k, (lds_void*)(region + blk * 1024), 16, 0, 0);
   }
 }
 
-// Zeroes the entries of a loaded slab whose k is >= kvalid (k counted from the
-// slab start).
+// The same for an m/n-contiguous operand: tile k-rows k0.. (BK of them,
+// gathered by ridx), R columns from r0, LDS [BK][R].
+template <class Cfg, int R>
+__device__ __forceinline__ void issue_mc(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
+                                         int k0, int kext, char* region) {
+  using T = typename Cfg::T;
+  const T* base = static_cast<const T*>(vbase);
+  constexpr int ES = Cfg::ES, EPC = 16 / ES;
+  constexpr int CPR = R * ES / 16;
+  constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
+  constexpr int PER_WAVE = R * Cfg::BK * ES / 1024 / Cfg::NW;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int blk = wave * PER_WAVE + i;
+    const int pos = blk * 64 + lane;
+    const int kk = pos / CPR;
+    const int c = (pos % CPR) ^ (kk & MASK);
+    int krow = k0 + kk;
+    krow = krow < kext ? krow : kext - 1;
+    int col = r0 + c * EPC;
+    col = col < rext ? col : 0;
+    __builtin_amdgcn_global_load_lds(base + gather(ridx, krow) * ld + col, (lds_void*)(region + blk * 1024), 16, 0, 0);
+  }
+}
+
+template <class Cfg, int R, bool MC>
+__device__ __forceinline__ void fast_issue(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
+                                           int k0, int kext, char* region) {
+  if constexpr (MC)
+    issue_mc<Cfg, R>(vbase, ld, ridx, r0, rext, k0, kext, region);
+  else
+    issue_kc<Cfg, R>(vbase, ld, ridx, r0, rext, k0, kext, region);
+}
+
+// Zeroes the entries of a loaded slab whose k is >= kvalid (k from the slab start).
 template <class Cfg, int R, bool MC>
 __device__ __forceinline__ void fast_zero_tail(char* region, int kvalid) {
+  constexpr int ES = Cfg::ES, EPC = 16 / ES;
   if constexpr (!MC) {
-    // rows of 64 k: element (r, k) lives in chunk k / 8 of row r
-    for (int e = threadIdx.x; e < R * 64; e += Cfg::NT) {
-      const int r = e >> 6, k = e & 63;
-      if (k >= kvalid)
-        *reinterpret_cast<uint16_t*>(region + kc_chunk(r, k >> 3) + (k & 7) * 2) = 0;
+    constexpr int CPR = Cfg::BK * ES / 16;
+    for (int e = threadIdx.x; e < R * Cfg::BK; e += Cfg::NT) {
+      const int r = e / Cfg::BK, k = e % Cfg::BK;
+      if (k >= kvalid) {
+        char* p = region + kc_off<CPR>(r, k / EPC) + (k % EPC) * ES;
+        if constexpr (ES == 2)
+          *reinterpret_cast<uint16_t*>(p) = 0;
+        else
+          *reinterpret_cast<uint32_t*>(p) = 0;
+      }
     }
   } else {
-    // k-rows of R columns: clear whole rows kk >= kvalid
-    constexpr int CPR = R / 8;
-    for (int e = threadIdx.x; e < 64 * CPR; e += Cfg::NT) {
+    constexpr int CPR = R * ES / 16;
+    for (int e = threadIdx.x; e < Cfg::BK * CPR; e += Cfg::NT) {
       const int kk = e / CPR;
-      if (kk >= kvalid) *reinterpret_cast<u32x4*>(region + kk * CPR * 16 + (e % CPR) * 16) = u32x4{0u, 0u, 0u, 0u};
+      if (kk >= kvalid) *reinterpret_cast<u32x4*>(region + e * 16) = u32x4{0u, 0u, 0u, 0u};
     }
   }
 }
 
-// MFMA operand fragment (8 k of one row/column for this lane) at k offset kk
-// of the slab, for the 32-row block starting at tile row rb.
-template <int R, bool MC>
-__device__ __forceinline__ bf16x8 fast_frag(const char* region, int rb, int kk) {
+// bf16 MFMA operand fragment: 8 k (kk .. kk+15 split over the two lane halves)
+// of the row/column rb + lane % 32.
+template <class Cfg, int R, bool MC>
+__device__ __forceinline__ bf16x8 frag_bf16(const char* region, int rb, int kk) {
   const int lane = threadIdx.x & 63;
   if constexpr (!MC) {
-    const int row = rb + (lane & 31);
-    const int c = (kk >> 3) + (lane >> 5);
-    return *reinterpret_cast<const bf16x8*>(region + kc_chunk(row, c));
+    constexpr int CPR = Cfg::BK * 2 / 16;
+    return *reinterpret_cast<const bf16x8*>(region + kc_off<CPR>(rb + (lane & 31), (kk >> 3) + (lane >> 5)));
   } else {
-    // 16-lane groups: group g covers columns rb + 16 (g % 2) .. +15 and k
-    // kk + 8 (g / 2) .. +7, read as two 4-k transposed halves
-    constexpr int CPR = R / 8;
+    // 16-lane group g covers columns rb + 16 (g % 2) .. +15 and k kk + 8 (g / 2) .. +7,
+    // read as two transposed 4-k halves
+    constexpr int CPR = R * 2 / 16;
     const int g = lane >> 4, s = lane & 15;
     const int col = rb + 16 * (g & 1) + 4 * (s & 3);
-    const int kbase = kk + 8 * (g >> 1) + (s >> 2);
-    i16x4 lo, hi;
-    {
-      const int kr = kbase;
-      const char* p = region + mc_chunk<CPR>(kr, col >> 3) + (col & 7) * 2;
-      lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
-    }
-    {
-      const int kr = kbase + 4;
-      const char* p = region + mc_chunk<CPR>(kr, col >> 3) + (col & 7) * 2;
-      hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
-    }
+    const int kr = kk + 8 * (g >> 1) + (s >> 2);
+    const char* p0 = region + mc_off<CPR>(kr, col >> 3) + (col & 7) * 2;
+    const char* p1 = region + mc_off<CPR>(kr + 4, col >> 3) + (col & 7) * 2;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
     bf16x8 out;
     const bf16* l4 = reinterpret_cast<const bf16*>(&lo);
     const bf16* h4 = reinterpret_cast<const bf16*>(&hi);
@@ -140,10 +183,67 @@ __device__ __forceinline__ bf16x8 fast_frag(const char* region, int rb, int kk) 
   }
 }
 
+// fp32 MFMA operands: 4 k (kk + 4 * (lane / 32) + 0..3) of row/column rb + lane % 32.
+template <class Cfg, int R, bool MC>
+__device__ __forceinline__ f32x4 frag_f32(const char* region, int rb, int kk) {
+  const int lane = threadIdx.x & 63;
+  const int rc = rb + (lane & 31), k = kk + 4 * (lane >> 5);
+  if constexpr (!MC) {
+    constexpr int CPR = Cfg::BK * 4 / 16;
+    return *reinterpret_cast<const f32x4*>(region + kc_off<CPR>(rc, k >> 2));
+  } else {
+    constexpr int CPR = R * 4 / 16;
+    f32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = *reinterpret_cast<const float*>(region + mc_off<CPR>(k + e, rc >> 2) + (rc & 3) * 4);
+    return v;
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  if constexpr (N == 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Waits until at most `later` slabs of this wave's loads are outstanding.
+template <class Cfg>
+__device__ __forceinline__ void wait_slabs(int later) {
+  constexpr int L = Cfg::LPW;
+  if constexpr (Cfg::STAGES >= 4) {
+    if (later >= 2) {
+      wait_vm<2 * L>();
+      return;
+    }
+  }
+  if constexpr (Cfg::STAGES >= 3) {
+    if (later >= 1) {
+      wait_vm<L>();
+      return;
+    }
+  }
+  wait_vm<0>();
+}
+
+// Issues both operands' loads of slab q into its LDS stage.
+template <class Cfg, bool AMC, bool BMC>
+__device__ __forceinline__ void fast_issue_slab(const GemmArgs& g, const void* va, const void* vb, int m0, int n0,
+                                                int q, int q0, int nks, char* smem) {
+  using T = typename Cfg::T;
+  const T* abase = static_cast<const T*>(va);
+  const T* bbase = static_cast<const T*>(vb);
+  const int kb = q / nks, k0 = (q % nks) * Cfg::BK;
+  char* st = smem + ((q - q0) % Cfg::STAGES) * Cfg::STAGE;
+  fast_issue<Cfg, Cfg::BM, AMC>(abase + kb * g.a.kbstride, g.a.ld, g.a.ridx, m0, g.M, k0, g.K, st);
+  fast_issue<Cfg, Cfg::BN, BMC>(bbase + kb * g.b.kbstride, g.b.ld, g.b.ridx, n0, g.N, k0, g.K, st + Cfg::ABYTES);
+}
+
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
-  constexpr int ABYTES = Cfg::BM * 64 * 2, BBYTES = Cfg::BN * 64 * 2;
-  constexpr int STAGE = ABYTES + BBYTES;
+  using T = typename Cfg::T;
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
   // XCD-aware order: consecutive workgroups land on different XCDs, so give
@@ -158,10 +258,12 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int64_t bz = blockIdx.z / splits;
   const int split = blockIdx.z % splits;
   const int wave = threadIdx.x >> 6;
-  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  const int ks = wave / (Cfg::WGM * Cfg::WGN);
+  const int wmn = wave % (Cfg::WGM * Cfg::WGN);
+  const int wm = wmn / Cfg::WGN, wn = wmn % Cfg::WGN;
 
-  const bf16* abase = static_cast<const bf16*>(g.a.p) + bz * g.a.bstride;
-  const bf16* bbase = static_cast<const bf16*>(g.b.p) + bz * g.b.bstride;
+  const T* abase = static_cast<const T*>(g.a.p) + bz * g.a.bstride;
+  const T* bbase = static_cast<const T*>(g.b.p) + bz * g.b.bstride;
 
   f32x16 acc[Cfg::FM][Cfg::FN];
 #pragma unroll
@@ -171,86 +273,171 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nks = (g.K + 63) / 64;
+  const int nks = (g.K + Cfg::BK - 1) / Cfg::BK;
   const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
   const int nslab = kbatch * nks;
   const int q0 = static_cast<int>((static_cast<int64_t>(nslab) * split) / splits);
   const int q1 = static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits);
 
-  auto issue = [&](int q, int stage) {
-    const int kb = q / nks, k0 = (q % nks) * 64;
-    char* st = smem + stage * STAGE;
-    fast_issue<Cfg, Cfg::BM, AMC>(abase + kb * g.a.kbstride, g.a.ld, g.a.ridx, m0, g.M, k0, g.K, st);
-    fast_issue<Cfg, Cfg::BN, BMC>(bbase + kb * g.b.kbstride, g.b.ld, g.b.ridx, n0, g.N, k0, g.K, st + ABYTES);
-  };
-
-  if (q0 < q1) issue(q0, 0);
+#pragma unroll
+  for (int s = 0; s < Cfg::STAGES - 1; ++s)
+    if (q0 + s < q1) fast_issue_slab<Cfg, AMC, BMC>(g, abase, bbase, m0, n0, q0 + s, q0, nks, smem);
   for (int q = q0; q < q1; ++q) {
-    const int cur = (q - q0) & 1;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (q + 1 < q1) issue(q + 1, cur ^ 1);
-    char* st = smem + cur * STAGE;
-    const int kvalid = g.K - (q % nks) * 64;
-    if (kvalid < 64) {
+    // slabs issued after q: min(STAGES - 2, q1 - 1 - q)
+    const int later = q1 - 1 - q < Cfg::STAGES - 2 ? q1 - 1 - q : Cfg::STAGES - 2;
+    wait_slabs<Cfg>(later);
+    __syncthreads();  // slab q visible to all waves; slab q - 1 no longer read
+    if (q + Cfg::STAGES - 1 < q1) fast_issue_slab<Cfg, AMC, BMC>(g, abase, bbase, m0, n0, q + Cfg::STAGES - 1, q0, nks, smem);
+    char* st = smem + ((q - q0) % Cfg::STAGES) * Cfg::STAGE;
+    const int kvalid = g.K - (q % nks) * Cfg::BK;
+    if (kvalid < Cfg::BK) {
       fast_zero_tail<Cfg, Cfg::BM, AMC>(st, kvalid);
-      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + ABYTES, kvalid);
+      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, kvalid);
       __syncthreads();
     }
+    const int kw0 = ks * Cfg::KW;
+    if constexpr (Cfg::ES == 2) {
 #pragma unroll
-    for (int kk = 0; kk < 64; kk += 16) {
-      bf16x8 a[Cfg::FM], b[Cfg::FN];
+      for (int kk = 0; kk < Cfg::KW; kk += 16) {
+        bf16x8 a[Cfg::FM], b[Cfg::FN];
 #pragma unroll
-      for (int i = 0; i < Cfg::FM; ++i) a[i] = fast_frag<Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kk);
-#pragma unroll
-      for (int j = 0; j < Cfg::FN; ++j) b[j] = fast_frag<Cfg::BN, BMC>(st + ABYTES, wn * Cfg::TN + 32 * j, kk);
-#pragma unroll
-      for (int i = 0; i < Cfg::FM; ++i)
+        for (int i = 0; i < Cfg::FM; ++i) a[i] = frag_bf16<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kw0 + kk);
 #pragma unroll
         for (int j = 0; j < Cfg::FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          b[j] = frag_bf16<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kw0 + kk);
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < Cfg::KW; kk += 8) {
+        f32x4 a[Cfg::FM], b[Cfg::FN];
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i) a[i] = frag_f32<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kw0 + kk);
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+          b[j] = frag_f32<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kw0 + kk);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < Cfg::FN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
+      }
     }
   }
-  store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
+  if constexpr (Cfg::KSPLIT == 1) {
+    store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
+  } else {
+    // the KSPLIT waves of one output tile reduce through LDS; wave ks finishes
+    // the accumulator registers t (flattened over i, j, r) with t % KSPLIT == ks
+    constexpr int NREG = Cfg::FM * Cfg::FN * 16;
+    static_assert(Cfg::KSPLIT * Cfg::WGM * Cfg::WGN * NREG * 64 * 4 <= Cfg::LDS, "reduction buffer exceeds LDS");
+    float* red = reinterpret_cast<float*>(smem);
+    const int lane = threadIdx.x & 63;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          red[((ks * Cfg::WGM * Cfg::WGN + wmn) * NREG + (i * Cfg::FN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    __syncthreads();
+    const int lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+    for (int t = ks; t < NREG; t += Cfg::KSPLIT) {
+      const int i = t / (Cfg::FN * 16), j = (t / 16) % Cfg::FN, r = t % 16;
+      float v = 0.0f;
+#pragma unroll
+      for (int u = 0; u < Cfg::KSPLIT; ++u) v += red[((u * Cfg::WGM * Cfg::WGN + wmn) * NREG + t) * 64 + lane];
+      const int m = m0 + wm * Cfg::TM + 32 * i + 8 * (r >> 2) + 4 * lh + (r & 3);
+      const int n = n0 + wn * Cfg::TN + 32 * j + lr;
+      if (m >= g.M || n >= g.N) continue;
+      if (splits > 1) {
+        g.partial[(bz * splits + split) * static_cast<int64_t>(g.M) * g.N + static_cast<int64_t>(m) * g.N + n] = v;
+        continue;
+      }
+      const int64_t orow = gather(g.c.ridx, m);
+      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
+      const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+      v = epilogue<EPI>(g.c, v, bias);
+      if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
+        v = 0.0f;
+      (static_cast<OutT*>(g.c.p) + bz * g.c.bstride)[o] = from_f32<OutT>(v);
+    }
+  }
 }
 
-using FastHuge = FastCfg<256, 256, 2, 2>;
-using FastBig = FastCfg<128, 128, 2, 2>;
-
-template <class Cfg>
-constexpr int fast_lds_bytes() { return 2 * (Cfg::BM + Cfg::BN) * 64 * 2; }
-
-// Whether a bf16 problem can run on fast_gemm_kernel: every operand view is
-// read in whole 16-byte chunks (row stride a multiple of 8 elements, aligned
-// base, no column gather, no load-time gate).
-inline bool fast_ok(const GemmOperand& a, const GemmOperand& b) {
-  auto ok = [](const GemmOperand& o) {
-    return o.cidx == nullptr && o.y == nullptr && o.ld % 8 == 0 && o.bstride % 8 == 0 && o.kbstride % 8 == 0 &&
+// Whether a problem can run on fast_gemm_kernel: every operand view is read
+// in whole 16-byte chunks.
+inline bool fast_ok(const GemmOperand& a, const GemmOperand& b, size_t esize) {
+  const int64_t epc = static_cast<int64_t>(16 / esize);
+  auto ok = [epc](const GemmOperand& o) {
+    return o.cidx == nullptr && o.y == nullptr && o.ld % epc == 0 && o.bstride % epc == 0 && o.kbstride % epc == 0 &&
            (reinterpret_cast<uintptr_t>(o.p) & 15u) == 0;
   };
   return ok(a) && ok(b);
 }
 
+// Configurations: large tiles for large grids, 32x32 tiles with the k of each
+// slab split over the 4 waves for small grids.
+template <typename T>
+struct FastCfgs;
+template <>
+struct FastCfgs<bf16> {
+  using Huge = FastCfg<bf16, 256, 256, 32, 4, 2, 2, 1>;   // 128 KB LDS
+  using Big = FastCfg<bf16, 128, 128, 64, 3, 2, 2, 1>;    // 96 KB
+  using Small = FastCfg<bf16, 32, 32, 128, 4, 1, 1, 4>;   // 64 KB
+};
+template <>
+struct FastCfgs<float> {
+  using Huge = FastCfg<float, 128, 128, 32, 4, 2, 2, 1>;  // 128 KB
+  using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 1>;     // 96 KB
+  using Small = FastCfg<float, 32, 32, 64, 4, 1, 1, 4>;   // 64 KB
+};
+
 struct FastPlan {
-  int cfg;     // 0: 256x256, 1: 128x128
+  int kind;    // TILE_BIG (Huge), TILE_MEDIUM (Big), TILE_SMALL (Small)
   int splits;
 };
 
+template <typename T>
 inline FastPlan plan_fast(int M, int N, int K, int kbatch, int batch) {
+  using C = FastCfgs<T>;
+  auto tiles_of = [&](int bm, int bn) {
+    return static_cast<int64_t>((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch;
+  };
   FastPlan p;
-  const int64_t huge = static_cast<int64_t>((M + 255) / 256) * ((N + 255) / 256) * batch;
-  p.cfg = huge >= 160 ? 0 : 1;
-  const int bm = p.cfg == 0 ? 256 : 128;
-  const int64_t tiles = static_cast<int64_t>((M + bm - 1) / bm) * ((N + bm - 1) / bm) * batch;
-  const int64_t slabs = static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + 63) / 64);
+  int bk;
+  int64_t tiles;
+  if (tiles_of(C::Huge::BM, C::Huge::BN) >= kTargetBlocks * 5 / 8) {
+    p.kind = TILE_BIG;
+    bk = C::Huge::BK;
+    tiles = tiles_of(C::Huge::BM, C::Huge::BN);
+  } else if (tiles_of(C::Big::BM, C::Big::BN) >= kTargetBlocks * 5 / 8) {
+    p.kind = TILE_MEDIUM;
+    bk = C::Big::BK;
+    tiles = tiles_of(C::Big::BM, C::Big::BN);
+  } else {
+    p.kind = TILE_SMALL;
+    bk = C::Small::BK;
+    tiles = tiles_of(C::Small::BM, C::Small::BN);
+  }
+  const int64_t slabs = static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk);
   int s = 1;
   while (tiles * s * 2 <= kTargetBlocks && slabs / (s * 2) >= kMinSlabsPerSplit && s * 2 <= kMaxSplits) s *= 2;
   p.splits = s;
   return p;
 }
 
+template <typename T>
 inline size_t fast_partial_floats(int M, int N, int K, int kbatch, int batch) {
-  const FastPlan p = plan_fast(M, N, K, kbatch, batch);
+  const FastPlan p = plan_fast<T>(M, N, K, kbatch, batch);
   return p.splits > 1 ? static_cast<size_t>(p.splits) * batch * M * N : 0;
 }
 
@@ -258,15 +445,15 @@ template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) {
   const int splits = g.splits > 1 ? g.splits : 1;
   auto kern = fast_gemm_kernel<Cfg, AMC, BMC, OutT, EPI>;
-  static bool attr_set = false;  // per instantiation: allow > 64 KB of dynamic LDS
+  static bool attr_set = false;  // per instantiation: allow more than 64 KB of dynamic LDS
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, fast_lds_bytes<Cfg>());
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   dim3 grid((g.N + Cfg::BN - 1) / Cfg::BN, (g.M + Cfg::BM - 1) / Cfg::BM, batch * splits);
-  hipLaunchKernelGGL(kern, grid, dim3(Cfg::NT), fast_lds_bytes<Cfg>(), stream, g);
+  hipLaunchKernelGGL(kern, grid, dim3(Cfg::NT), Cfg::LDS, stream, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const int64_t mn = static_cast<int64_t>(g.M) * g.N;
@@ -275,16 +462,18 @@ inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) 
   return hipGetLastError();
 }
 
-// Runs a bf16 GEMM on the fast kernel; the caller has checked fast_ok().
-template <bool AMC, bool BMC, typename OutT, int EPI>
+// Runs a GEMM on the fast kernel; the caller has checked fast_ok().
+template <typename T, bool AMC, bool BMC, typename OutT, int EPI>
 inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float* partial) {
   if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
-  FastPlan p = plan_fast(g.M, g.N, g.K, g.kbatch, batch);
+  FastPlan p = plan_fast<T>(g.M, g.N, g.K, g.kbatch, batch);
   if (!partial) p.splits = 1;
   g.splits = p.splits;
   g.partial = partial;
-  if (p.cfg == 0) return launch_fast<FastHuge, AMC, BMC, OutT, EPI>(g, batch, stream);
-  return launch_fast<FastBig, AMC, BMC, OutT, EPI>(g, batch, stream);
+  using C = FastCfgs<T>;
+  if (p.kind == TILE_BIG) return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI>(g, batch, stream);
+  if (p.kind == TILE_MEDIUM) return launch_fast<typename C::Big, AMC, BMC, OutT, EPI>(g, batch, stream);
+  return launch_fast<typename C::Small, AMC, BMC, OutT, EPI>(g, batch, stream);
 }
 
 }  // namespace ard
