@@ -187,12 +187,26 @@ hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t
   return hipGetLastError();
 }
 
-// The view of W used by fwd / bwd_data: either the full matrix gathered by
+// The kept rows offset + period * i of a row-major matrix (row stride ld): a
+// row-based pattern keeps an arithmetic progression of neurons (Sec. 3.2,
+// Eq. 1), so the gather folds into the view's base and row stride and the
+// GEMM reads no index list. y, when set, is the gate source of the same shape.
+GemmOperand kept_rows(const void* p, const void* y, int64_t ld, int32_t period, int32_t offset, size_t esize,
+                      int32_t relu) {
+  const int64_t skip = static_cast<int64_t>(offset) * ld * static_cast<int64_t>(esize);
+  GemmOperand o = {};
+  o.p = static_cast<const char*>(p) + skip;
+  o.y = y ? static_cast<const char*>(y) + skip : nullptr;
+  o.ld = ld * period;
+  o.relu = relu;
+  o.scale = 1.0f;
+  return o;
+}
+
+// The view of W used by fwd / bwd_data: either the full matrix's kept output
 // rows (no input gather), or a compact copy (given, or built into ws).
 struct WeightView {
-  const void* p;
-  int64_t ld;
-  const int32_t* ridx;
+  GemmOperand op;
   float* partial;  // split-K partial sums in ws, or NULL
 };
 
@@ -200,13 +214,13 @@ template <typename T>
 int weight_view(const FcShape& s, const void* W, void* ws, hipStream_t stream, WeightView* v) {
   char* w = static_cast<char*>(ws);
   if (s.compact_given) {
-    *v = {W, s.ldc, nullptr, nullptr};
+    v->op = kept_rows(W, nullptr, s.ldc, 1, 0, sizeof(T), 0);
   } else if (s.needs_compact) {
     ARD_HIP_CHECK(launch_compact<T>(s, W, w, stream));
-    *v = {w, s.ldc, nullptr, nullptr};
+    v->op = kept_rows(w, nullptr, s.ldc, 1, 0, sizeof(T), 0);
     w += al256(compact_bytes(s));
   } else {
-    *v = {W, s.K, s.out_idx, nullptr};
+    v->op = kept_rows(W, nullptr, s.K, s.out_period, s.out_offset, sizeof(T), 0);
   }
   v->partial = ws ? reinterpret_cast<float*>(w) : nullptr;
   return ARD_OK;
@@ -222,12 +236,12 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   g.M = s.kout;
   g.N = s.B;
   g.K = s.kin;
-  g.a = {wv.p, nullptr, wv.ld, wv.ridx, nullptr, 0, 0, 1.0f, 0};
-  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
+  g.a = wv.op;
+  g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
   g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
-  const bool a_vec = vec_rows(wv.ld, sizeof(T));
+  const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok(g.a, g.b, sizeof(T))) {
+  if (fast_ok(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -253,17 +267,17 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   g.N = s.B;
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
-  g.a = {wv.p, nullptr, wv.ld, wv.ridx, nullptr, 0, 0, 1.0f, 0};
+  g.a = wv.op;
   // B(t, n) = dY[out(t)][n] * [Y > 0] (no gate when Yt is NULL: dY is already
   // the gated gradient); the 0/1 gate keeps bf16 operands exact, and scale is
   // applied to the fp32 accumulators in the epilogue, as is the optional gate
   // [Xgate > 0] of the layer below.
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
-  g.b = {dYt, gated ? Yt : nullptr, s.B, s.out_idx, nullptr, 0, gated, 1.0f, 0};
+  g.b = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
   g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale, Xgate};
-  const bool a_vec = vec_rows(wv.ld, sizeof(T));
+  const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok(g.a, g.b, sizeof(T))) {
+  if (fast_ok(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
@@ -289,14 +303,14 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.N = s.kin;
   g.K = s.B;
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
-  g.a = {dYt, gated ? Yt : nullptr, s.B, s.out_idx, nullptr, 0, gated, 1.0f, 0};
-  g.b = {Xt, nullptr, s.B, s.in_idx, nullptr, 0, 0, 1.0f, 0};
+  g.a = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
+  g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
   g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
   const bool v = vec_rows(s.B, sizeof(T));
   float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
-  if (fast_ok(g.a, g.b, sizeof(T))) {
+  if (fast_ok(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD>(g, 1, stream, partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(

@@ -1,11 +1,11 @@
-// Gathered GEMM with direct global -> LDS loads and a deep K pipeline (gfx950).
+// GEMM with direct global -> LDS loads and a deep K pipeline (gfx950).
 //
 // The same contraction as gemm_kernel (ard_gemm.hpp) for operand views that
 // can be read in whole 16-byte chunks (row stride a multiple of 16 bytes,
-// aligned base, no column gather, no load-time gate):
+// aligned base, no row or column gather, no load-time gate):
 //
 //  * global -> LDS without register staging: each lane issues
-//    global_load_lds_dwordx4 for one 16-byte chunk of a (row-gathered) tile;
+//    global_load_lds_dwordx4 for one 16-byte chunk of a tile;
 //    a wave writes 64 consecutive LDS chunks, and the lane picks the global
 //    chunk that belongs at its LDS position under an XOR swizzle that keeps the
 //    MFMA fragment reads free of bank conflicts;
@@ -23,7 +23,16 @@
 //    chip);
 //  * the last, partial K slab is cleaned in LDS (entries past the contraction
 //    length set to 0) before use; rows past the output extents load a clamped
-//    valid row and their results are discarded.
+//    valid row and their results are discarded;
+//  * operands are plain strided views (a row-based pattern's gather is folded
+//    into base and row stride by the caller), so the main loop reads no index
+//    lists: an index load would make the wave wait for every earlier direct load.
+//
+// The direct loads are issued as inline assembly and ordered only by the
+// explicit vmcnt waits and LDS barriers of the main loop: the compiler, which
+// cannot tell that an LDS read targets another stage than the loads in
+// flight, would otherwise wait for all of them before such reads, and
+// __syncthreads() waits for all outstanding vector memory operations.
 #pragma once
 
 #include "ard_gemm.hpp"
@@ -31,7 +40,6 @@
 namespace ard {
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
 
 template <typename T_, int BM_, int BN_, int BK_, int STAGES_, int WGM_, int WGN_, int KSPLIT_>
 struct FastCfg {
@@ -66,66 +74,93 @@ __device__ __forceinline__ int mc_off(int k, int c) {
   return (k * CPR + (c ^ (k & MASK))) * 16;
 }
 
-// Issues this wave's direct loads of one k-contiguous operand tile for the
-// slab at k0: tile rows r0.. (R of them, gathered by ridx), BK k per row,
-// LDS [R][BK].
-template <class Cfg, int R>
-__device__ __forceinline__ void issue_kc(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
-                                         int k0, int kext, char* region) {
-  using T = typename Cfg::T;
-  const T* base = static_cast<const T*>(vbase);
-  constexpr int ES = Cfg::ES, EPC = 16 / ES;  // elements per chunk
-  constexpr int CPR = Cfg::BK * ES / 16;
-  constexpr int PER_WAVE = R * Cfg::BK * ES / 1024 / Cfg::NW;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-#pragma unroll
-  for (int i = 0; i < PER_WAVE; ++i) {
-    const int blk = wave * PER_WAVE + i;
-    const int pos = blk * 64 + lane;  // chunk position in the LDS region
-    const int r = pos / CPR;
-    const int c = (pos % CPR) ^ ((r >> 1) & (CPR - 1));
-    int row = r0 + r;
-    row = row < rext ? row : rext - 1;
-    int k = k0 + c * EPC;
-    k = k < kext ? k : 0;
-    __builtin_amdgcn_global_load_lds(base + gather(ridx, row) * ld + k, (lds_void*)(region + blk * 1024), 16, 0, 0);
-  }
+// One direct load of 16 bytes per lane from sbase + voff into LDS at
+// lds_base + 16 * lane. sbase (an SGPR pair) and lds_base are wave-uniform;
+// lds_base travels in M0, which the compiler writes before the statement.
+// The compiler's hazard tracking does not look into the statement, so it
+// starts with the 5 wait states a vector memory instruction needs after a VALU
+// write of an SGPR it reads (sbase often comes from v_readfirstlane), which
+// also cover the one needed after an M0 write. No memory clobber: the load
+// writes a stage that no LDS access between two loop barriers touches, and
+// volatile statements keep their order relative to the barriers and waits.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile(
+      "s_nop 4\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "{m0}"(lds_base));
 }
 
-// The same for an m/n-contiguous operand: tile k-rows k0.. (BK of them,
-// gathered by ridx), R columns from r0, LDS [BK][R].
-template <class Cfg, int R>
-__device__ __forceinline__ void issue_mc(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
-                                         int k0, int kext, char* region) {
-  using T = typename Cfg::T;
-  const T* base = static_cast<const T*>(vbase);
-  constexpr int ES = Cfg::ES, EPC = 16 / ES;
-  constexpr int CPR = R * ES / 16;
-  constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
-  constexpr int PER_WAVE = R * Cfg::BK * ES / 1024 / Cfg::NW;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-#pragma unroll
-  for (int i = 0; i < PER_WAVE; ++i) {
-    const int blk = wave * PER_WAVE + i;
-    const int pos = blk * 64 + lane;
-    const int kk = pos / CPR;
-    const int c = (pos % CPR) ^ (kk & MASK);
-    int krow = k0 + kk;
-    krow = krow < kext ? krow : kext - 1;
-    int col = r0 + c * EPC;
-    col = col < rext ? col : 0;
-    __builtin_amdgcn_global_load_lds(base + gather(ridx, krow) * ld + col, (lds_void*)(region + blk * 1024), 16, 0, 0);
-  }
+// A wave-uniform pointer as such (SGPR pair): integer division and other VALU
+// lowerings leave uniform values in VGPRs.
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const char*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
+// LDS address (byte offset in the workgroup's LDS) of a pointer into shared memory.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)p));
+}
+
+// Workgroup barrier for the LDS hand-off: waits for this wave's own LDS
+// operations only, not for its direct loads in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Per-lane sources of one operand's direct loads. Per slab a wave loads
+// PER_WAVE blocks of 64 16-byte chunks; LDS chunk pos = blk * 64 + lane of the
+// operand's region holds, for a k-contiguous tile [R][BK], row pos / CPR and
+// the swizzled k chunk; for an m/n-contiguous tile [BK][R], k-row pos / CPR
+// and the swizzled column chunk. A chunk is addressed as a 32-bit byte offset
+// from the slab's first element (uniform, in SGPRs). Rows and columns past the
+// extents are clamped once to a valid one (their results are discarded); a
+// chunk past the contraction length of a partial slab loads the same row's
+// (or column's) chunk at k 0 of the slab instead, and the slab's tail is
+// zeroed in LDS before use.
 template <class Cfg, int R, bool MC>
-__device__ __forceinline__ void fast_issue(const void* vbase, int64_t ld, const int32_t* ridx, int r0, int rext,
-                                           int k0, int kext, char* region) {
-  if constexpr (MC)
-    issue_mc<Cfg, R>(vbase, ld, ridx, r0, rext, k0, kext, region);
-  else
-    issue_kc<Cfg, R>(vbase, ld, ridx, r0, rext, k0, kext, region);
-}
+struct DmaSrc {
+  static constexpr int ES = Cfg::ES, EPC = 16 / ES;  // EPC: elements per chunk
+  static constexpr int CPR = MC ? R * ES / 16 : Cfg::BK * ES / 16;
+  static constexpr int PER_WAVE = R * Cfg::BK * ES / 1024 / Cfg::NW;
+  uint32_t off[PER_WAVE];   // byte offset of the lane's chunk from the slab base
+  uint32_t off0[PER_WAVE];  // the same chunk at k (KC) or k-row (MC) 0 of the slab
+  int k[PER_WAVE];          // the chunk's k (KC) or k-row (MC) within the slab
+
+  __device__ __forceinline__ void init(int64_t ld, int r0, int rext, int wave) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int pos = (wave * PER_WAVE + i) * 64 + lane;
+      if constexpr (!MC) {
+        const int r = pos / CPR;
+        const int c = (pos % CPR) ^ ((r >> 1) & (CPR - 1));
+        const int row = r0 + r < rext ? r0 + r : rext - 1;
+        off0[i] = static_cast<uint32_t>(row * ld * ES);
+        off[i] = off0[i] + static_cast<uint32_t>(c * 16);
+        k[i] = c * EPC;
+      } else {
+        constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
+        const int kk = pos / CPR;
+        const int c = (pos % CPR) ^ (kk & MASK);
+        const int col = r0 + c * EPC < rext ? r0 + c * EPC : 0;
+        off0[i] = static_cast<uint32_t>(col * ES);
+        off[i] = off0[i] + static_cast<uint32_t>(kk * ld * ES);
+        k[i] = kk;
+      }
+    }
+  }
+
+  // Loads the slab whose first element is at sbase (uniform), of which the
+  // first kv k (k-rows) are valid, into the LDS region at byte address region.
+  __device__ __forceinline__ void issue(const char* sbase, int kv, uint32_t region, int wave) const {
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i)
+      dma16(uniform_ptr(sbase), k[i] < kv ? off[i] : off0[i],
+            region + static_cast<uint32_t>((wave * PER_WAVE + i) * 1024));
+  }
+};
 
 // Zeroes the entries of a loaded slab whose k is >= kvalid (k from the slab start).
 template <class Cfg, int R, bool MC>
@@ -209,38 +244,6 @@ __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Waits until at most `later` slabs of this wave's loads are outstanding.
-template <class Cfg>
-__device__ __forceinline__ void wait_slabs(int later) {
-  constexpr int L = Cfg::LPW;
-  if constexpr (Cfg::STAGES >= 4) {
-    if (later >= 2) {
-      wait_vm<2 * L>();
-      return;
-    }
-  }
-  if constexpr (Cfg::STAGES >= 3) {
-    if (later >= 1) {
-      wait_vm<L>();
-      return;
-    }
-  }
-  wait_vm<0>();
-}
-
-// Issues both operands' loads of slab q into its LDS stage.
-template <class Cfg, bool AMC, bool BMC>
-__device__ __forceinline__ void fast_issue_slab(const GemmArgs& g, const void* va, const void* vb, int m0, int n0,
-                                                int q, int q0, int nks, char* smem) {
-  using T = typename Cfg::T;
-  const T* abase = static_cast<const T*>(va);
-  const T* bbase = static_cast<const T*>(vb);
-  const int kb = q / nks, k0 = (q % nks) * Cfg::BK;
-  char* st = smem + ((q - q0) % Cfg::STAGES) * Cfg::STAGE;
-  fast_issue<Cfg, Cfg::BM, AMC>(abase + kb * g.a.kbstride, g.a.ld, g.a.ridx, m0, g.M, k0, g.K, st);
-  fast_issue<Cfg, Cfg::BN, BMC>(bbase + kb * g.b.kbstride, g.b.ld, g.b.ridx, n0, g.N, k0, g.K, st + Cfg::ABYTES);
-}
-
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   using T = typename Cfg::T;
@@ -279,21 +282,64 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int q0 = static_cast<int>((static_cast<int64_t>(nslab) * split) / splits);
   const int q1 = static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits);
 
+  // Slabs q0 .. q1 - 1 of this split. Every iteration issues one slab; past
+  // the last slab the last one is loaded again into a stage that is no longer
+  // read, so each wave has exactly (STAGES - 2) * LPW loads younger than the
+  // slab it waits for.
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  DmaSrc<Cfg, Cfg::BM, AMC> da;
+  DmaSrc<Cfg, Cfg::BN, BMC> db;
+  static_assert(DmaSrc<Cfg, Cfg::BM, AMC>::PER_WAVE + DmaSrc<Cfg, Cfg::BN, BMC>::PER_WAVE == Cfg::LPW, "load count");
+  if (q0 < q1) {
+    da.init(g.a.ld, m0, g.M, wv);
+    db.init(g.b.ld, n0, g.N, wv);
+  }
+  // first element of slab (batch ib, k ik) of each operand
+  const char* const ab = reinterpret_cast<const char*>(abase);
+  const char* const bb = reinterpret_cast<const char*>(bbase);
+  const int64_t a_kstep = AMC ? g.a.ld : 1, b_kstep = BMC ? g.b.ld : 1;
+  int iq = q0, ib = __builtin_amdgcn_readfirstlane(q0 / (nks > 0 ? nks : 1));  // next slab to load: batch ib,
+  int ik = __builtin_amdgcn_readfirstlane((q0 - ib * nks) * Cfg::BK), is = 0;     // first k ik, stage is
+  int ck = ik, cs = 0;                                                               // slab to compute
 #pragma unroll
-  for (int s = 0; s < Cfg::STAGES - 1; ++s)
-    if (q0 + s < q1) fast_issue_slab<Cfg, AMC, BMC>(g, abase, bbase, m0, n0, q0 + s, q0, nks, smem);
+  for (int s = 0; s < Cfg::STAGES - 1; ++s) {
+    if (q0 < q1) {
+      const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
+      da.issue(ab + (ib * g.a.kbstride + ik * a_kstep) * Cfg::ES, g.K - ik, st, wv);
+      db.issue(bb + (ib * g.b.kbstride + ik * b_kstep) * Cfg::ES, g.K - ik, st + Cfg::ABYTES, wv);
+      is = is + 1 == Cfg::STAGES ? 0 : is + 1;
+      if (iq + 1 < q1) {
+        ++iq;
+        ik += Cfg::BK;
+        if (ik >= g.K) ik = 0, ++ib;
+      }
+    }
+  }
   for (int q = q0; q < q1; ++q) {
-    // slabs issued after q: min(STAGES - 2, q1 - 1 - q)
-    const int later = q1 - 1 - q < Cfg::STAGES - 2 ? q1 - 1 - q : Cfg::STAGES - 2;
-    wait_slabs<Cfg>(later);
-    __syncthreads();  // slab q visible to all waves; slab q - 1 no longer read
-    if (q + Cfg::STAGES - 1 < q1) fast_issue_slab<Cfg, AMC, BMC>(g, abase, bbase, m0, n0, q + Cfg::STAGES - 1, q0, nks, smem);
-    char* st = smem + ((q - q0) % Cfg::STAGES) * Cfg::STAGE;
-    const int kvalid = g.K - (q % nks) * Cfg::BK;
+    wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+    lds_barrier();  // slab q visible to all waves; the stage of slab q - 1 no longer read
+    char* st = smem + cs * Cfg::STAGE;
+    const int kvalid = g.K - ck;
+    cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
+    ck += Cfg::BK;
+    if (ck >= g.K) ck = 0;
     if (kvalid < Cfg::BK) {
       fast_zero_tail<Cfg, Cfg::BM, AMC>(st, kvalid);
       fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, kvalid);
-      __syncthreads();
+      lds_barrier();
+    }
+    // the next slab goes to the stage of slab q - 1, read by no wave any more
+    {
+      const uint32_t nst = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
+      da.issue(ab + (ib * g.a.kbstride + ik * a_kstep) * Cfg::ES, g.K - ik, nst, wv);
+      db.issue(bb + (ib * g.b.kbstride + ik * b_kstep) * Cfg::ES, g.K - ik, nst + Cfg::ABYTES, wv);
+      is = is + 1 == Cfg::STAGES ? 0 : is + 1;
+      if (iq + 1 < q1) {
+        ++iq;
+        ik += Cfg::BK;
+        if (ik >= g.K) ik = 0, ++ib;
+      }
     }
     const int kw0 = ks * Cfg::KW;
     if constexpr (Cfg::ES == 2) {
@@ -330,6 +376,7 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
       }
     }
   }
+  wait_vm<0>();  // no direct load may still write LDS past this point
   if constexpr (Cfg::KSPLIT == 1) {
     store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
   } else {
@@ -373,15 +420,19 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   }
 }
 
-// Whether a problem can run on fast_gemm_kernel: every operand view is read
-// in whole 16-byte chunks.
-inline bool fast_ok(const GemmOperand& a, const GemmOperand& b, size_t esize) {
+// Whether a problem can run on fast_gemm_kernel: every operand is a plain
+// strided view read in whole 16-byte chunks, and every chunk of a slab lies
+// less than 2^31 bytes past the slab's first element.
+inline bool fast_ok(const GemmArgs& g, size_t esize) {
   const int64_t epc = static_cast<int64_t>(16 / esize);
-  auto ok = [epc](const GemmOperand& o) {
-    return o.cidx == nullptr && o.y == nullptr && o.ld % epc == 0 && o.bstride % epc == 0 && o.kbstride % epc == 0 &&
-           (reinterpret_cast<uintptr_t>(o.p) & 15u) == 0;
+  auto ok = [epc, esize, &g](const GemmOperand& o, int ext) {
+    int64_t rows = ext > g.K ? ext : g.K;
+    rows = (rows > 256 ? rows : 256) + 1;  // a slab spans at most 256 k-rows
+    return o.ridx == nullptr && o.cidx == nullptr && o.y == nullptr && o.ld % epc == 0 && o.bstride % epc == 0 &&
+           o.kbstride % epc == 0 && (reinterpret_cast<uintptr_t>(o.p) & 15u) == 0 &&
+           rows * o.ld * static_cast<int64_t>(esize) < (int64_t{1} << 31);
   };
-  return ok(a) && ok(b);
+  return ok(g.a, g.M) && ok(g.b, g.N);
 }
 
 // Configurations: large tiles for large grids, 32x32 tiles with the k of each

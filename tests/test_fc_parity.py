@@ -231,31 +231,39 @@ def test_pregated_gradient_and_input_gate(dtype):
     compare(f64(db), db64, Ga.sum(0), tol(dtype), "db")
 
 
-def test_wide_layer_bf16_full_size_sampled():
-    """One hidden layer of the wide bf16 MLP (8192 -> 8192, batch 2048) under
-    patterns on both sides, in the launch configuration of the benchmark
-    (compact weights, SKIP, workspace), against the oracle on sampled rows and
-    columns. The oracle's forward output, rounded to bf16, is the ReLU gate of
-    both backward implementations."""
-    B, K, N = 2048, 8192, 8192
+@pytest.mark.parametrize("dtype,B,K,N,pats", [
+    ("bf16", 2048, 8192, 8192, ((3, 2), (2, 1))),
+    # dense, 256 x 256 output tiles in all three passes, a partial last K slab
+    # (8152 = 254 * 32 + 24) and a ragged last tile row
+    ("bf16", 2048, 8152, 8192, ((1, 0), (1, 0))),
+    # fp32 128 x 128 tiles (fwd, bwd_weight) with a partial last K slab
+    ("f32", 1024, 2040, 4096, ((1, 0), (1, 0))),
+    ("f32", 1024, 2040, 4096, ((2, 1), (3, 0))),
+], ids=["bf16-patterned", "bf16-dense-ragged", "f32-dense-ragged", "f32-patterned"])
+def test_wide_layer_full_size_sampled(dtype, B, K, N, pats):
+    """One hidden layer of the wide MLP in the launch configuration of the
+    benchmark (compact weights, SKIP, workspace), against the oracle on sampled
+    rows and columns. The oracle's forward output, rounded to the storage type,
+    is the ReLU gate of both backward implementations."""
     g = synth.generator(1805 + 4)
-    X = synth.to_storage(torch.relu(synth.normal(g, (B, K))), "bf16")
-    W = synth.to_storage(synth.he(g, N, K), "bf16")
-    dY = synth.to_storage(synth.normal(g, (B, N)), "bf16")
-    (pi, oi), (po, oo) = (3, 2), (2, 1)
+    X = synth.to_storage(torch.relu(synth.normal(g, (B, K))), dtype)
+    W = synth.to_storage(synth.he(g, N, K), dtype)
+    dY = synth.to_storage(synth.normal(g, (B, N)), dtype)
+    (pi, oi), (po, oo) = pats
     m_in, m_out = opat.row_mask(K, pi, oi), opat.row_mask(N, po, oo)
     Xf, Wf, dYf = f64(X), f64(W), f64(dY)
     Y64 = ofc.fc_forward(Xf, Wf, None, m_in, m_out, 1.0, "relu")
-    Ys = synth.to_storage(torch.from_numpy(Y64).float(), "bf16")
+    Ys = synth.to_storage(torch.from_numpy(Y64).float(), dtype)
     in_plan, out_plan = row_plan(K, pi, oi), row_plan(N, po, oo)
-    desc = api.fc_desc(api.ARD_BF16, B, K, N, in_plan, out_plan, 1.0, api.ARD_ACT_RELU, api.ARD_DROPPED_SKIP,
+    desc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, 1.0, api.ARD_ACT_RELU, api.ARD_DROPPED_SKIP,
                        api.ARD_WEIGHTS_COMPACT)
     Xt, Wd, dYt, Yst = to_dev(X.T), to_dev(W), to_dev(dY.T), to_dev(Ys.T)
-    Wc = torch.empty(api.ard_fc_compact_bytes(desc) // 2, dtype=torch.bfloat16, device=device())
+    sdt = synth.storage_dtype(dtype)
+    Wc = torch.empty(api.ard_fc_compact_bytes(desc) // Wd.element_size(), dtype=sdt, device=device())
     api.ard_fc_compact_weights(desc, Wd, Wc)
     ws = workspace(api.ard_fc_workspace_bytes(desc))
-    Yt = torch.zeros(N, B, dtype=torch.bfloat16, device=device())
-    dXt = torch.zeros(K, B, dtype=torch.bfloat16, device=device())
+    Yt = torch.zeros(N, B, dtype=sdt, device=device())
+    dXt = torch.zeros(K, B, dtype=sdt, device=device())
     dW = torch.zeros(N, K, device=device())
     api.ard_fc_fwd(desc, Xt, Wc, None, Yt, ws)
     api.ard_fc_bwd_data(desc, dYt, Yst, Wc, dXt, ws)
@@ -266,11 +274,22 @@ def test_wide_layer_bf16_full_size_sampled():
     rows = np.sort(rng.choice(Sout, 40, replace=False))
     cols = np.sort(rng.choice(Sin, 40, replace=False))
     Xm = Xf * m_in[None, :]
-    compare(f64(Yt)[rows].T, Y64[:, rows], np.abs(Xm) @ np.abs(Wf[rows]).T, 2e-2, "Y rows")
+    compare(f64(Yt)[rows].T, Y64[:, rows], np.abs(Xm) @ np.abs(Wf[rows]).T, tol(dtype), "Y rows")
     G = ofc.fc_output_grad(f64(Ys), dYf, m_out, 1.0, "relu")        # [B][N]
     Wk = Wf[:, cols] * m_out[:, None]
-    compare(f64(dXt)[cols].T, G @ Wk, np.abs(G) @ np.abs(Wk), 2e-2, "dX cols")
+    compare(f64(dXt)[cols].T, G @ Wk, np.abs(G) @ np.abs(Wk), tol(dtype), "dX cols")
     compare(f64(dW)[np.ix_(rows, cols)], G[:, rows].T @ Xf[:, cols],
-            np.abs(G[:, rows]).T @ np.abs(Xf[:, cols]), 2e-2, "dW")
+            np.abs(G[:, rows]).T @ np.abs(Xf[:, cols]), tol(dtype), "dW")
+    # every output tile: Y in full (normwise), dX and dW through random projections
+    Yg = f64(Yt)
+    err = np.abs(Yg[Sout] - Y64.T[Sout]).max() / np.abs(Y64).max()
+    assert err <= tol(dtype), f"Y normwise error {err:.3e}"
+    v, u = rng.standard_normal(B), rng.standard_normal(K)
+    Wm = Wf * m_out[:, None]
+    compare(f64(dXt)[Sin] @ v, (Wm[:, Sin].T @ (G.T @ v)), np.abs(Wm[:, Sin]).T @ (np.abs(G).T @ np.abs(v)),
+            tol(dtype), "dX projection")
+    dWg = f64(dW)
+    compare(dWg[np.ix_(Sout, Sin)] @ u[Sin], G[:, Sout].T @ (Xf[:, Sin] @ u[Sin]),
+            np.abs(G[:, Sout]).T @ (np.abs(Xf[:, Sin]) @ np.abs(u[Sin])), tol(dtype), "dW projection")
     dropped_rows = np.setdiff1d(np.arange(N), Sout)[:64]
-    assert not f64(Yt)[dropped_rows].any() and not f64(dW)[dropped_rows].any()
+    assert not Yg[dropped_rows].any() and not dWg[dropped_rows].any()
