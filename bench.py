@@ -90,6 +90,30 @@ class Mlp:
                     api.ARD_DROPPED_SKIP)
             self.descs.append(api.fc_desc(*args))
             self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT) if l > 0 else self.descs[-1])
+        # the calls of one step, in order, with their arguments resolved once
+        P, st = self.ptr, self.stream
+        Wf = [P["W"][0]] + P["Wc"][1:]
+        acts = [P["X0"]] + P["Y"]
+        ws = (self.ws.data_ptr(), self.ws.numel() * 4)
+        self.calls, self.seq = {}, []
+        for l in range(self.L):
+            self.calls[("fwd", l)] = (api.ard_fc_fwd, (self.cdescs[l], acts[l], Wf[l], P["bias"][l], P["Y"][l],
+                                                      ws, st), {})
+        # backward: each bwd_data also applies the ReLU derivative of the layer
+        # below (Xgate = that layer's output), so every dY[l] below the top is
+        # already gated and is passed with Yt = None
+        for l in reversed(range(self.L)):
+            self.calls[("bwd_weight", l)] = (api.ard_fc_bwd_weight, (self.cdescs[l], acts[l], P["dY"][l], None,
+                                                                     P["dW"][l], P["db"][l], ws, st), {})
+            if l > 0:
+                self.calls[("bwd_data", l)] = (api.ard_fc_bwd_data, (self.cdescs[l], P["dY"][l], None, Wf[l],
+                                                                     P["dY"][l - 1], ws, st), {"Xgate": acts[l]})
+        order = [("fwd", l) for l in range(self.L)]
+        for l in reversed(range(self.L)):
+            order.append(("bwd_weight", l))
+            if l > 0:
+                order.append(("bwd_data", l))
+        self.seq = [(key,) + self.calls[key] for key in order]
 
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
@@ -114,38 +138,44 @@ class Mlp:
                 per[("bwd_data", l)] = f
         return sum(per.values()), per
 
-    def step(self, it, timed_call=None, events=None):
+    def gemm_shape(self, pats, kind, l):
+        """(M, N, K) of the GEMM a call runs: fwd kept_out x B x kept_in, bwd_data
+        kept_in x B x kept_out, bwd_weight kept_out x kept_in x B."""
+        n = self.kept(pats)
+        if kind == "fwd":
+            return (n[l + 1], self.B, n[l])
+        if kind == "bwd_data":
+            return (n[l], self.B, n[l + 1])
+        return (n[l + 1], n[l], self.B)
+
+    def prepare(self, it):
+        """Samples this step's patterns, compacts them on the device and gathers
+        the compact weights of the layers whose inputs are dropped."""
         api, P, st = self.api, self.ptr, self.stream
         pats = self.patterns(it)
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, P["idx"][l], st, plan=self.plans[l])
         for l in range(1, self.L):
             api.ard_fc_compact_weights(self.cdescs[l], P["W"][l], P["Wc"][l], st)
-        Wf = [P["W"][0]] + P["Wc"][1:]
-        acts = [P["X0"]] + P["Y"]
-        ws = (self.ws.data_ptr(), self.ws.numel() * 4)
+        return pats
 
-        def call(kind, l, fn):
-            if timed_call == (kind, l):
+    def step(self, it, timed_call=None, events=None):
+        pats = self.prepare(it)
+        for key, fn, args, kw in self.seq:
+            if key == timed_call:
                 events[0].record()
-                fn()
+                fn(*args, **kw)
                 events[1].record()
             else:
-                fn()
-
-        for l in range(self.L):
-            call("fwd", l, lambda l=l: api.ard_fc_fwd(self.cdescs[l], acts[l], Wf[l], P["bias"][l], P["Y"][l], ws, st))
-        # backward: each bwd_data also applies the ReLU derivative of the layer
-        # below (Xgate = that layer's output), so every dY[l] below the top is
-        # already gated and is passed with Yt = None
-        for l in reversed(range(self.L)):
-            call("bwd_weight", l, lambda l=l: api.ard_fc_bwd_weight(self.cdescs[l], acts[l], P["dY"][l],
-                                                                     None, P["dW"][l], P["db"][l], ws, st))
-            if l > 0:
-                call("bwd_data", l, lambda l=l: api.ard_fc_bwd_data(self.cdescs[l], P["dY"][l], None,
-                                                                     Wf[l], P["dY"][l - 1], ws, st,
-                                                                     Xgate=acts[l]))
+                fn(*args, **kw)
         return pats
+
+    def replay(self, it, key, reps):
+        """Runs one call of step it reps times (for counter collection)."""
+        self.prepare(it)
+        fn, args, kw = self.calls[key]
+        for _ in range(reps):
+            fn(*args, **kw)
 
     # ------------------------------------------------------------------ oracle
     def oracle_step(self, pats):
@@ -200,34 +230,35 @@ def time_steps(wl, steps, warmup, it0, timed_call=None):
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     start.record()
+    shapes = []
     for i in range(steps):
         pats = wl.step(it0 + warmup + i, timed_call, ev[i] if ev else None)
         f, per = wl.kept_flops(pats)
         total_flops += f
         if timed_call is not None:
             call_flops += per[timed_call]
+            shapes.append((wl.gemm_shape(pats, *timed_call), per[timed_call], it0 + warmup + i))
     end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = start.elapsed_time(end)
     if ev:
         durs = [a.elapsed_time(b) for a, b in ev]
-    return {"ms": gpu_ms, "wall_s": wall, "flops": total_flops, "call_ms": durs, "call_flops": call_flops}
+    return {"ms": gpu_ms, "wall_s": wall, "flops": total_flops, "call_ms": durs, "call_flops": call_flops,
+            "call_shapes": shapes}
 
 
-def dominant_call(wl, it0):
-    """The (pass, layer) call with the largest summed event time over a few steps."""
-    import torch
+def roofline_call(wl, first_it, steps):
+    """The call with the most kept work over the timed steps (summed kept
+    FLOPs; ties go to the first call of a step). The patterns are seeded, so
+    the choice is the same in every run of the same command."""
     totals = {}
-    for i in range(3):
-        pats = wl.patterns(it0 + i)
-        _, per = wl.kept_flops(pats)
-        for key in per:
-            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            wl.step(it0 + i, key, ev)
-            torch.cuda.synchronize()
-            totals[key] = totals.get(key, 0.0) + ev[0].elapsed_time(ev[1])
-    return max(totals, key=totals.get)
+    for i in range(steps):
+        _, per = wl.kept_flops(wl.patterns(first_it + i))
+        for key in (k for k, *_ in wl.seq):
+            totals[key] = totals.get(key, 0.0) + per.get(key, 0.0)
+    best = max(totals.values())
+    return next(k for k, *_ in wl.seq if totals.get(k, 0.0) == best)
 
 
 def cpu_baseline(wl, p, budget_s):
@@ -251,6 +282,119 @@ def cpu_baseline(wl, p, budget_s):
             "sample": f"{n} steps of the same workload at p={p} (fp64 masked dense layers, numpy), {t:.1f} s"}
 
 
+def source_digest():
+    """sha256 over the kernel sources and the header: a stored counter reading
+    holds only for the code it was taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1805_08939_amd", "csrc")
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc))
+    files.append(os.path.join(ROOT, "include", "ard.h"))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_record(workload, kind, layer, shape):
+    """HBM bytes per launch of the roofline call, from the committed rocprofv3
+    counter summaries (FETCH_SIZE and WRITE_SIZE passes, each scaled by what the
+    counter reads for a plain copy of known size). None when no summary covers
+    this call and shape, or when the kernel sources changed since."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    digest = source_digest()
+    for f in sorted(os.listdir(pdir)):
+        if not f.endswith((".txt", ".md")):
+            continue
+        with open(os.path.join(pdir, f)) as fh:
+            for line in fh:
+                if not line.startswith("traffic-record: "):
+                    continue
+                rec = json.loads(line[len("traffic-record: "):])
+                if (rec.get("workload") == workload and rec.get("call") == [kind, layer]
+                        and rec.get("shape") == list(shape) and rec.get("source_digest") == digest):
+                    return rec["bytes_per_launch"]
+    return None
+
+
+def _demangle(name):
+    if not name.startswith("_Z"):
+        return name
+    import shutil
+    import subprocess
+    if shutil.which("c++filt"):
+        return subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip() or name
+    return name
+
+
+def _short_kernel(name):
+    name = _demangle(name).replace("void ", "").replace("ard::", "").replace("(anonymous namespace)::", "")
+    depth, out = 0, []
+    for ch in name:  # drop the argument list, keep template arguments
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out).strip()[:150]
+
+
+def _col(row, *names):
+    low = {k.lower(): v for k, v in row.items()}
+    for n in names:
+        if n.lower() in low and low[n.lower()] not in (None, ""):
+            return low[n.lower()]
+    raise KeyError(names[0])
+
+
+def summarize_trace(path, top):
+    """Per (kernel, grid) table of a rocprofv3 kernel trace (CSV)."""
+    import csv
+    agg = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            name = _short_kernel(_col(r, "Kernel_Name"))
+            wg = [max(int(_col(r, f"Workgroup_Size_{d}")), 1) for d in "XYZ"]
+            grid = tuple(int(_col(r, f"Grid_Size_{d}")) // w for d, w in zip("XYZ", wg))
+            us = (int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1000.0
+            a = agg.setdefault((name, grid), [0, 0.0])
+            a[0] += 1
+            a[1] += us
+    tot = sum(a[1] for a in agg.values()) or 1.0
+    print("| calls | total us | avg us | % | workgroups | kernel |")
+    print("|---:|---:|---:|---:|---|---|")
+    for (name, grid), (n, us) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:top]:
+        print(f"| {n} | {us:.1f} | {us / n:.2f} | {100 * us / tot:.2f} | {grid[0]}x{grid[1]}x{grid[2]} | `{name}` |")
+
+
+def summarize_counters(path, top, last=0):
+    """Per (kernel, grid size, counter) mean value per dispatch of a rocprofv3
+    counter collection (CSV); with last > 0 only each kernel's last dispatches."""
+    import csv
+    agg = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            key = (_short_kernel(_col(r, "Kernel_Name")), _col(r, "Grid_Size"), _col(r, "Counter_Name"),
+                   int(_col(r, "Dispatch_Id")))
+            agg[key] = agg.get(key, 0.0) + float(_col(r, "Counter_Value"))
+    by = {}
+    for (name, grid, counter, disp), v in agg.items():
+        by.setdefault((name, grid, counter), []).append((disp, v))
+    per = {}
+    for key, vals in by.items():
+        vals.sort()
+        if last > 0:
+            vals = vals[-last:]
+        per[key] = (len(vals), sum(v for _, v in vals))
+    print("| dispatches | mean per dispatch | counter | grid size (work-items) | kernel |")
+    print("|---:|---:|---|---:|---|")
+    for (name, grid, counter), (n, v) in sorted(per.items(), key=lambda kv: -kv[1][1])[:top]:
+        print(f"| {n} | {v / n:.1f} | {counter} | {grid} | `{name}` |")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -260,9 +404,22 @@ def main():
     ap.add_argument("--p", type=float, default=0.5, help="dropout rate of the headline value")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize-trace", metavar="CSV", help="print a per-kernel table of a rocprofv3 kernel trace")
+    ap.add_argument("--summarize-counters", metavar="CSV", help="print per-kernel means of a rocprofv3 counter run")
+    ap.add_argument("--top", type=int, default=25)
+    ap.add_argument("--last", type=int, default=0, help="--summarize-counters: only the last N dispatches per kernel")
+    ap.add_argument("--replay", type=int, default=0,
+                    help="after timing, run the roofline call N more times at its shape (for counter passes)")
+    ap.add_argument("--digest", action="store_true", help="print the kernel source digest")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 1 GiB (3 times), the reference for HBM counters")
     args = ap.parse_args()
+    if args.summarize_trace:
+        return summarize_trace(args.summarize_trace, args.top)
+    if args.summarize_counters:
+        return summarize_counters(args.summarize_counters, args.top, args.last)
+    if args.digest:
+        return print(source_digest())
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)",
               file=sys.stderr)
@@ -291,7 +448,7 @@ def main():
         it0 = 1_000_000 * (i + 1)
         timed = None
         if p == args.p:
-            timed = dominant_call(wl, it0)
+            timed = roofline_call(wl, it0 + args.warmup, args.steps)
         r = time_steps(wl, args.steps, args.warmup, it0, timed)
         r["timed_call"] = timed
         results[p] = r
@@ -303,14 +460,25 @@ def main():
     t0 = results[0.0]["ms"]
     speedup = {f"{p}": t0 / results[p]["ms"] for p in rates if p > 0}
     kept_frac = {f"{p}": (results[p]["flops"] / results[0.0]["flops"]) for p in rates if p > 0}
+    # the roofline call's launches in the timed region, grouped by GEMM shape
+    # (patterns change per step); the shape with the most kept work is the
+    # roofline kernel: one tile configuration and launch grid
     kind, layer = head["timed_call"]
-    call_ms = sum(head["call_ms"]) / len(head["call_ms"])
-    call_flops = head["call_flops"] / args.steps
+    groups = {}
+    for (shape, fl, it), ms in zip(head["call_shapes"], head["call_ms"]):
+        g = groups.setdefault(shape, [0, 0.0, 0.0, it])
+        g[0] += 1
+        g[1] += ms
+        g[2] += fl
+    shape, (count, ms_sum, fl_sum, shape_it) = max(groups.items(), key=lambda kv: (kv[1][2], kv[0]))
+    call_ms, call_flops = ms_sum / count, fl_sum / count
     achieved = call_flops / (call_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
-                "frac": achieved / PEAK_TFLOPS[dtype], "traffic": None,
-                "kernel": f"gemm ({kind}, layer {layer})", "avg_launch_us": call_ms * 1e3,
-                "flops_per_launch": call_flops}
+                "frac": achieved / PEAK_TFLOPS[dtype],
+                "traffic": traffic_record(spec["name"], kind, layer, shape),
+                "kernel": f"gemm ({kind}, layer {layer}), M x N x K = {shape[0]} x {shape[1]} x {shape[2]}",
+                "launches": count, "avg_launch_us": call_ms * 1e3, "flops_per_launch": call_flops,
+                "call_share_of_step": sum(head["call_ms"]) / head["ms"]}
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms"] / args.steps, "higher_is_better": True,
@@ -326,6 +494,12 @@ def main():
                   for p in rates},
         "roofline": roofline,
     }
+    if args.replay > 0:
+        wl.set_rate(args.p)
+        wl.replay(shape_it, (kind, layer), args.replay)
+        torch.cuda.synchronize()
+        print(f"# replayed {kind} layer {layer} of step {shape_it} ({shape}) {args.replay} times",
+              file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.p, args.cpu_budget)
     print(json.dumps(out), flush=True)

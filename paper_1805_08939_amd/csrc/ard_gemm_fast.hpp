@@ -35,6 +35,8 @@
 // __syncthreads() waits for all outstanding vector memory operations.
 #pragma once
 
+#include <type_traits>
+
 #include "ard_gemm.hpp"
 
 namespace ard {
@@ -60,35 +62,74 @@ struct FastCfg {
   static_assert(KW % (ES == 2 ? 16 : 8) == 0, "per-wave k must hold whole MFMA steps");
 };
 
-// Byte offset of 16-byte chunk c of row r. k-contiguous tiles hold CPR = BK*ES/16
-// chunks per row, the chunk index swizzled by row / 2; m/n-contiguous tiles
-// hold CPR = R*ES/16 chunks per k-row, the low three chunk bits (fewer when a
-// row has fewer chunks) swizzled by k.
+// LDS layout. gfx950 LDS has 64 banks of 4 bytes: a wave's 16-byte reads are
+// served 16 lanes per pass, its 8-byte reads 32 lanes per pass, and a pass is
+// free of bank conflicts when its lanes touch 16 different 16-byte bank groups
+// (byte address / 16 mod 16). Chunk c of row r goes to position
+// r * CPR + (c ^ swizzle(r)); the swizzles make the fragment reads below
+// conflict-free.
+//
+// k-contiguous tiles [R][BK] (CPR = BK*ES/16 chunks per row), read as 16 bytes
+// per lane from 16 consecutive rows at one chunk: rows r and r + 16/CPR share
+// bank groups unless the swizzle tells them apart.
+template <int CPR>
+__device__ __forceinline__ int kc_swz(int r) {
+  constexpr int SH = CPR >= 16 ? 0 : CPR == 8 ? 1 : CPR == 4 ? 2 : 3;
+  return (r >> SH) & (CPR - 1);
+}
+// m/n-contiguous tiles [BK][R] (CPR = R*ES/16 chunks per k-row). 16-bit data
+// is read transposed: per 32 lanes, 4 consecutive k-rows x 4 consecutive
+// chunks; 32-bit data per lane from k-rows k and k + 4, 8 chunks each.
+template <int CPR, int ES>
+__device__ __forceinline__ int mc_swz(int k) {
+  if constexpr (ES == 2) {
+    if constexpr (CPR >= 16)
+      return (k & 3) << 2;
+    else if constexpr (CPR == 8)
+      return ((k >> 1) & 1) << 2;
+    else
+      return 0;
+  } else {
+    if constexpr (CPR >= 16)
+      return ((k >> 2) & 1) << 3;
+    else
+      return 0;
+  }
+}
+
 template <int CPR>
 __device__ __forceinline__ int kc_off(int r, int c) {
-  return (r * CPR + (c ^ ((r >> 1) & (CPR - 1)))) * 16;
+  return (r * CPR + (c ^ kc_swz<CPR>(r))) * 16;
 }
-template <int CPR>
+template <int CPR, int ES>
 __device__ __forceinline__ int mc_off(int k, int c) {
-  constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
-  return (k * CPR + (c ^ (k & MASK))) * 16;
+  return (k * CPR + (c ^ mc_swz<CPR, ES>(k))) * 16;
 }
 
 // One direct load of 16 bytes per lane from sbase + voff into LDS at
 // lds_base + 16 * lane. sbase (an SGPR pair) and lds_base are wave-uniform;
-// lds_base travels in M0, which the compiler writes before the statement.
-// The compiler's hazard tracking does not look into the statement, so it
-// starts with the 5 wait states a vector memory instruction needs after a VALU
-// write of an SGPR it reads (sbase often comes from v_readfirstlane), which
-// also cover the one needed after an M0 write. No memory clobber: the load
-// writes a stage that no LDS access between two loop barriers touches, and
-// volatile statements keep their order relative to the barriers and waits.
+// lds_base travels in M0, which the compiler writes before the statement and
+// which the load reads one wait state later at the earliest. The compiler's
+// hazard tracking does not look into the statement: the first load of a group
+// (FIRST) also waits the 5 states a vector memory instruction needs after a
+// VALU write (v_readfirstlane) of an SGPR it reads; later loads of the group
+// use the same base. No memory clobber: the load writes a stage that no LDS
+// access between two loop barriers touches, and volatile statements keep
+// their order relative to the barriers and waits.
+template <bool FIRST>
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
-  asm volatile(
-      "s_nop 4\n\t"
-      "global_load_lds_dwordx4 %0, %1"
-      :
-      : "v"(voff), "s"(sbase), "{m0}"(lds_base));
+  if constexpr (FIRST)
+    asm volatile(
+        "s_nop 4\n\t"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(voff), "s"(sbase), "{m0}"(lds_base));
+  else
+    asm volatile(
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(voff), "s"(sbase), "{m0}"(lds_base));
 }
 
 // A wave-uniform pointer as such (SGPR pair): integer division and other VALU
@@ -135,15 +176,14 @@ struct DmaSrc {
       const int pos = (wave * PER_WAVE + i) * 64 + lane;
       if constexpr (!MC) {
         const int r = pos / CPR;
-        const int c = (pos % CPR) ^ ((r >> 1) & (CPR - 1));
+        const int c = (pos % CPR) ^ kc_swz<CPR>(r);
         const int row = r0 + r < rext ? r0 + r : rext - 1;
         off0[i] = static_cast<uint32_t>(row * ld * ES);
         off[i] = off0[i] + static_cast<uint32_t>(c * 16);
         k[i] = c * EPC;
       } else {
-        constexpr int MASK = CPR >= 8 ? 7 : CPR - 1;
         const int kk = pos / CPR;
-        const int c = (pos % CPR) ^ (kk & MASK);
+        const int c = (pos % CPR) ^ mc_swz<CPR, ES>(kk);
         const int col = r0 + c * EPC < rext ? r0 + c * EPC : 0;
         off0[i] = static_cast<uint32_t>(col * ES);
         off[i] = off0[i] + static_cast<uint32_t>(kk * ld * ES);
@@ -155,10 +195,11 @@ struct DmaSrc {
   // Loads the slab whose first element is at sbase (uniform), of which the
   // first kv k (k-rows) are valid, into the LDS region at byte address region.
   __device__ __forceinline__ void issue(const char* sbase, int kv, uint32_t region, int wave) const {
+    const char* b = uniform_ptr(sbase);
+    const uint32_t r0 = region + static_cast<uint32_t>(wave * PER_WAVE * 1024);
+    dma16<true>(b, k[0] < kv ? off[0] : off0[0], r0);
 #pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i)
-      dma16(uniform_ptr(sbase), k[i] < kv ? off[i] : off0[i],
-            region + static_cast<uint32_t>((wave * PER_WAVE + i) * 1024));
+    for (int i = 1; i < PER_WAVE; ++i) dma16<false>(b, k[i] < kv ? off[i] : off0[i], r0 + static_cast<uint32_t>(i * 1024));
   }
 };
 
@@ -202,8 +243,8 @@ __device__ __forceinline__ bf16x8 frag_bf16(const char* region, int rb, int kk) 
     const int g = lane >> 4, s = lane & 15;
     const int col = rb + 16 * (g & 1) + 4 * (s & 3);
     const int kr = kk + 8 * (g >> 1) + (s >> 2);
-    const char* p0 = region + mc_off<CPR>(kr, col >> 3) + (col & 7) * 2;
-    const char* p1 = region + mc_off<CPR>(kr + 4, col >> 3) + (col & 7) * 2;
+    const char* p0 = region + mc_off<CPR, 2>(kr, col >> 3) + (col & 7) * 2;
+    const char* p1 = region + mc_off<CPR, 2>(kr + 4, col >> 3) + (col & 7) * 2;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
     bf16x8 out;
@@ -231,7 +272,7 @@ __device__ __forceinline__ f32x4 frag_f32(const char* region, int rb, int kk) {
     f32x4 v;
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      v[e] = *reinterpret_cast<const float*>(region + mc_off<CPR>(k + e, rc >> 2) + (rc & 3) * 4);
+      v[e] = *reinterpret_cast<const float*>(region + mc_off<CPR, 4>(k + e, rc >> 2) + (rc & 3) * 4);
     return v;
   }
 }
@@ -244,19 +285,101 @@ __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Fragments of one k step (16 bf16 or 8 fp32 k) of a wave's output tile, and
+// the MFMAs that consume them.
+template <class Cfg, bool AMC, bool BMC>
+struct StepFrags {
+  static constexpr int KSTEP = Cfg::ES == 2 ? 16 : 8;
+  using FT = typename std::conditional<Cfg::ES == 2, bf16x8, f32x4>::type;
+  FT a[Cfg::FM], b[Cfg::FN];
+
+  __device__ __forceinline__ void load(const char* st, int wm, int wn, int kk) {
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i) {
+      if constexpr (Cfg::ES == 2)
+        a[i] = frag_bf16<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kk);
+      else
+        a[i] = frag_f32<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kk);
+    }
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j) {
+      if constexpr (Cfg::ES == 2)
+        b[j] = frag_bf16<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kk);
+      else
+        b[j] = frag_f32<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kk);
+    }
+  }
+
+  __device__ __forceinline__ void mma(f32x16 (&acc)[Cfg::FM][Cfg::FN]) const {
+    if constexpr (Cfg::ES == 2) {
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
+    }
+  }
+};
+
+// The direct loads of one operand pair, slab after slab: wave-uniform
+// pointers to the next slab's first element, its first k, its stage, and how
+// many slabs of the split are still to come after it. Past the last slab the
+// last one is loaded again (into a stage no longer read), so every wave issues
+// the same number of loads per slab.
+template <class Cfg, bool AMC, bool BMC>
+struct SlabLoader {
+  DmaSrc<Cfg, Cfg::BM, AMC> da;
+  DmaSrc<Cfg, Cfg::BN, BMC> db;
+  const char* na;
+  const char* nb;
+  int64_t a_step, b_step, a_wrap, b_wrap;
+  int K, ik, is, left, wv;
+  uint32_t lds0;
+
+  __device__ __forceinline__ void issue() {
+    const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
+    da.issue(na, K - ik, st, wv);
+    db.issue(nb, K - ik, st + Cfg::ABYTES, wv);
+    is = is + 1 == Cfg::STAGES ? 0 : is + 1;
+    if (left > 0) {
+      --left;
+      na += a_step;
+      nb += b_step;
+      ik += Cfg::BK;
+      if (ik >= K) ik = 0, na += a_wrap, nb += b_wrap;
+    }
+  }
+};
+
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   using T = typename Cfg::T;
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
-  // XCD-aware order: consecutive workgroups land on different XCDs, so give
-  // each XCD a contiguous run of output tiles (shared operand rows in its L2).
+  // Tile order. Workgroup i runs on XCD i % 8, each XCD with its own L2, so
+  // XCD x takes a contiguous run of positions t in a grouped order: kGroupRows
+  // tile rows at a time, column by column within the group. The workgroups
+  // running together on one XCD then share a few A row panels and a few B
+  // column panels instead of each bringing its own.
   const int nx = gridDim.x, ny = gridDim.y;
   const int nxy = nx * ny;
-  int bid = blockIdx.y * nx + blockIdx.x;
-  if (nxy % 8 == 0) bid = (bid % 8) * (nxy / 8) + bid / 8;
-  const int n0 = (bid % nx) * Cfg::BN;
-  const int m0 = (bid / nx) * Cfg::BM;
+  const int bid = blockIdx.y * nx + blockIdx.x;
+  const int xcd = bid % 8, per = nxy / 8, extra = nxy % 8;
+  const int t = xcd * per + (xcd < extra ? xcd : extra) + bid / 8;
+  constexpr int kGroupRows = 8;
+  const int first_row = (t / (kGroupRows * nx)) * kGroupRows;
+  const int rows = ny - first_row < kGroupRows ? ny - first_row : kGroupRows;
+  const int local = t % (kGroupRows * nx);
+  const int n0 = (local / rows) * Cfg::BN;
+  const int m0 = (first_row + local % rows) * Cfg::BM;
   const int splits = g.splits > 1 ? g.splits : 1;
   const int64_t bz = blockIdx.z / splits;
   const int split = blockIdx.z % splits;
@@ -279,101 +402,88 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int nks = (g.K + Cfg::BK - 1) / Cfg::BK;
   const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
   const int nslab = kbatch * nks;
-  const int q0 = static_cast<int>((static_cast<int64_t>(nslab) * split) / splits);
-  const int q1 = static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits);
+  const int q0 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * split) / splits));
+  const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits));
 
-  // Slabs q0 .. q1 - 1 of this split. Every iteration issues one slab; past
-  // the last slab the last one is loaded again into a stage that is no longer
-  // read, so each wave has exactly (STAGES - 2) * LPW loads younger than the
-  // slab it waits for.
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
-  DmaSrc<Cfg, Cfg::BM, AMC> da;
-  DmaSrc<Cfg, Cfg::BN, BMC> db;
+  // Slabs q0 .. q1 - 1 of this split, in STAGES LDS stages. Each wave waits
+  // only for its own loads of the slab it is about to read (vmcnt: exactly
+  // (STAGES - 2) * LPW younger loads are allowed), then a barrier makes every
+  // wave's loads of that slab visible and certifies that all waves have
+  // finished reading the previous slab, whose stage takes the next load.
+  // Fragments are double-buffered in registers: the reads of the next k step
+  // (the first step of the next slab, behind the barrier) are issued before
+  // the MFMAs of the current one, so LDS latency and the barrier overlap MFMA
+  // execution.
+  SlabLoader<Cfg, AMC, BMC> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
   static_assert(DmaSrc<Cfg, Cfg::BM, AMC>::PER_WAVE + DmaSrc<Cfg, Cfg::BN, BMC>::PER_WAVE == Cfg::LPW, "load count");
   if (q0 < q1) {
-    da.init(g.a.ld, m0, g.M, wv);
-    db.init(g.b.ld, n0, g.N, wv);
+    ld.da.init(g.a.ld, m0, g.M, ld.wv);
+    ld.db.init(g.b.ld, n0, g.N, ld.wv);
   }
-  // first element of slab (batch ib, k ik) of each operand
-  const char* const ab = reinterpret_cast<const char*>(abase);
-  const char* const bb = reinterpret_cast<const char*>(bbase);
-  const int64_t a_kstep = AMC ? g.a.ld : 1, b_kstep = BMC ? g.b.ld : 1;
-  int iq = q0, ib = __builtin_amdgcn_readfirstlane(q0 / (nks > 0 ? nks : 1));  // next slab to load: batch ib,
-  int ik = __builtin_amdgcn_readfirstlane((q0 - ib * nks) * Cfg::BK), is = 0;     // first k ik, stage is
-  int ck = ik, cs = 0;                                                               // slab to compute
+  constexpr int ES = Cfg::ES;
+  ld.K = g.K;
+  ld.a_step = (AMC ? g.a.ld : 1) * Cfg::BK * ES;
+  ld.b_step = (BMC ? g.b.ld : 1) * Cfg::BK * ES;
+  ld.a_wrap = g.a.kbstride * ES - nks * ld.a_step;
+  ld.b_wrap = g.b.kbstride * ES - nks * ld.b_step;
+  const int ib = q0 / (nks > 0 ? nks : 1);
+  ld.ik = (q0 - ib * nks) * Cfg::BK;
+  ld.is = 0;
+  ld.left = q1 - q0 - 1;
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(abase) + (ib * g.a.kbstride) * ES + ld.ik / Cfg::BK * ld.a_step);
+  ld.nb = uniform_ptr(reinterpret_cast<const char*>(bbase) + (ib * g.b.kbstride) * ES + ld.ik / Cfg::BK * ld.b_step);
+  int ck = ld.ik, cs = 0;  // first k and stage of the slab being computed
+
+  using Frags = StepFrags<Cfg, AMC, BMC>;
+  constexpr int STEPS = Cfg::KW / Frags::KSTEP;
+  static_assert(STEPS % 2 == 0, "a slab holds an even number of k steps");
+  const int kw0 = ks * Cfg::KW;
+  Frags fr[2];
+  char* st = smem;
+  if (q0 < q1) {
 #pragma unroll
-  for (int s = 0; s < Cfg::STAGES - 1; ++s) {
-    if (q0 < q1) {
-      const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
-      da.issue(ab + (ib * g.a.kbstride + ik * a_kstep) * Cfg::ES, g.K - ik, st, wv);
-      db.issue(bb + (ib * g.b.kbstride + ik * b_kstep) * Cfg::ES, g.K - ik, st + Cfg::ABYTES, wv);
-      is = is + 1 == Cfg::STAGES ? 0 : is + 1;
-      if (iq + 1 < q1) {
-        ++iq;
-        ik += Cfg::BK;
-        if (ik >= g.K) ik = 0, ++ib;
-      }
-    }
-  }
-  for (int q = q0; q < q1; ++q) {
+    for (int s = 0; s < Cfg::STAGES - 1; ++s) ld.issue();
     wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
-    lds_barrier();  // slab q visible to all waves; the stage of slab q - 1 no longer read
-    char* st = smem + cs * Cfg::STAGE;
-    const int kvalid = g.K - ck;
-    cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
-    ck += Cfg::BK;
-    if (ck >= g.K) ck = 0;
-    if (kvalid < Cfg::BK) {
-      fast_zero_tail<Cfg, Cfg::BM, AMC>(st, kvalid);
-      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, kvalid);
+    lds_barrier();
+    if (g.K - ck < Cfg::BK) {
+      fast_zero_tail<Cfg, Cfg::BM, AMC>(st, g.K - ck);
+      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, g.K - ck);
       lds_barrier();
     }
-    // the next slab goes to the stage of slab q - 1, read by no wave any more
-    {
-      const uint32_t nst = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
-      da.issue(ab + (ib * g.a.kbstride + ik * a_kstep) * Cfg::ES, g.K - ik, nst, wv);
-      db.issue(bb + (ib * g.b.kbstride + ik * b_kstep) * Cfg::ES, g.K - ik, nst + Cfg::ABYTES, wv);
-      is = is + 1 == Cfg::STAGES ? 0 : is + 1;
-      if (iq + 1 < q1) {
-        ++iq;
-        ik += Cfg::BK;
-        if (ik >= g.K) ik = 0, ++ib;
+    ld.issue();
+    fr[0].load(st, wm, wn, kw0);
+  }
+  // all slabs but the last one: the last k step crosses into the next slab
+  for (int q = q0; q < q1 - 1; ++q) {
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (s + 1 < STEPS) {
+        fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
+      } else {
+        cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
+        ck += Cfg::BK;
+        if (ck >= g.K) ck = 0;
+        st = smem + cs * Cfg::STAGE;
+        wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+        lds_barrier();  // slab q + 1 visible; slab q read by no wave any more
+        if (g.K - ck < Cfg::BK) {
+          fast_zero_tail<Cfg, Cfg::BM, AMC>(st, g.K - ck);
+          fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, g.K - ck);
+          lds_barrier();
+        }
+        ld.issue();  // into the stage of slab q
+        fr[(s + 1) & 1].load(st, wm, wn, kw0);
       }
+      fr[s & 1].mma(acc);
     }
-    const int kw0 = ks * Cfg::KW;
-    if constexpr (Cfg::ES == 2) {
+  }
+  if (q0 < q1) {  // the last slab (a separate copy keeps the loop body's LDS waits exact)
 #pragma unroll
-      for (int kk = 0; kk < Cfg::KW; kk += 16) {
-        bf16x8 a[Cfg::FM], b[Cfg::FN];
-#pragma unroll
-        for (int i = 0; i < Cfg::FM; ++i) a[i] = frag_bf16<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kw0 + kk);
-#pragma unroll
-        for (int j = 0; j < Cfg::FN; ++j)
-          b[j] = frag_bf16<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kw0 + kk);
-#pragma unroll
-        for (int i = 0; i < Cfg::FM; ++i)
-#pragma unroll
-          for (int j = 0; j < Cfg::FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < Cfg::KW; kk += 8) {
-        f32x4 a[Cfg::FM], b[Cfg::FN];
-#pragma unroll
-        for (int i = 0; i < Cfg::FM; ++i) a[i] = frag_f32<Cfg, Cfg::BM, AMC>(st, wm * Cfg::TM + 32 * i, kw0 + kk);
-#pragma unroll
-        for (int j = 0; j < Cfg::FN; ++j)
-          b[j] = frag_f32<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, wn * Cfg::TN + 32 * j, kw0 + kk);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-#pragma unroll
-          for (int i = 0; i < Cfg::FM; ++i)
-#pragma unroll
-            for (int j = 0; j < Cfg::FN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
-      }
+    for (int s = 0; s < STEPS; ++s) {
+      if (s + 1 < STEPS) fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
+      fr[s & 1].mma(acc);
     }
   }
   wait_vm<0>();  // no direct load may still write LDS past this point
@@ -441,7 +551,7 @@ template <typename T>
 struct FastCfgs;
 template <>
 struct FastCfgs<bf16> {
-  using Huge = FastCfg<bf16, 256, 256, 32, 4, 2, 2, 1>;   // 128 KB LDS
+  using Huge = FastCfg<bf16, 256, 256, 32, 4, 2, 4, 1>;   // 128 KB LDS, 8 waves (2 per SIMD)
   using Big = FastCfg<bf16, 128, 128, 64, 3, 2, 2, 1>;    // 96 KB
   using Small = FastCfg<bf16, 32, 32, 128, 4, 1, 1, 4>;   // 64 KB
 };
