@@ -171,11 +171,20 @@ class Mlp:
         return pats
 
     def replay(self, it, key, reps):
-        """Runs one call of step it reps times (for counter collection)."""
+        """Runs one call of step it reps times back to back and returns the
+        mean GPU time per launch (ms, HIP events on the call's stream around
+        the whole replay)."""
+        torch = self.torch
         self.prepare(it)
         fn, args, kw = self.calls[key]
+        fn(*args, **kw)  # the same call once untimed: operands in cache as in the step
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
         for _ in range(reps):
             fn(*args, **kw)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
 
     # ------------------------------------------------------------------ oracle
     def oracle_step(self, pats):
@@ -269,7 +278,6 @@ def cpu_baseline(wl, p, budget_s):
     except Exception:  # pragma: no cover
         threads = 1
     wl.set_rate(p)
-    wl.host_copies()
     n, flops, t = 0, 0.0, 0.0
     while t < budget_s and n < 1000:
         pats = wl.patterns(10_000 + n)
@@ -325,8 +333,10 @@ def _demangle(name):
         return name
     import shutil
     import subprocess
-    if shutil.which("c++filt"):
-        return subprocess.run(["c++filt", name], capture_output=True, text=True).stdout.strip() or name
+    tool = shutil.which("c++filt")
+    if tool:  # GNU c++filt does not know the bf16 mangling DF16b: spell it as a vendor type
+        out = subprocess.run([tool, name.replace("DF16b", "u6__bf16")], capture_output=True, text=True).stdout
+        return out.strip() or name
     return name
 
 
@@ -350,36 +360,52 @@ def _col(row, *names):
     raise KeyError(names[0])
 
 
-def summarize_trace(path, top):
-    """Per (kernel, grid) table of a rocprofv3 kernel trace (CSV)."""
+def summarize_trace(path, top, last=0, tail=0):
+    """Per (kernel, grid) table of a rocprofv3 kernel trace (CSV); with
+    last > 0 only each kernel's last dispatches, with tail > 0 only the run's
+    last tail dispatches (a replayed call)."""
     import csv
-    agg = {}
     with open(path) as fh:
-        for r in csv.DictReader(fh):
-            name = _short_kernel(_col(r, "Kernel_Name"))
-            wg = [max(int(_col(r, f"Workgroup_Size_{d}")), 1) for d in "XYZ"]
-            grid = tuple(int(_col(r, f"Grid_Size_{d}")) // w for d, w in zip("XYZ", wg))
-            us = (int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1000.0
-            a = agg.setdefault((name, grid), [0, 0.0])
-            a[0] += 1
-            a[1] += us
-    tot = sum(a[1] for a in agg.values()) or 1.0
+        recs = sorted((int(_col(r, "Start_Timestamp")), r) for r in csv.DictReader(fh))
+    if tail > 0:
+        recs = recs[-tail:]
+    agg = {}
+    for start, r in recs:
+        name = _short_kernel(_col(r, "Kernel_Name"))
+        wg = [max(int(_col(r, f"Workgroup_Size_{d}")), 1) for d in "XYZ"]
+        grid = tuple(int(_col(r, f"Grid_Size_{d}")) // w for d, w in zip("XYZ", wg))
+        end = int(_col(r, "End_Timestamp"))
+        agg.setdefault((name, grid), []).append((start, (end - start) / 1000.0))
+    rows = {}
+    for key, v in agg.items():
+        v.sort()
+        if last > 0:
+            v = v[-last:]
+        rows[key] = (len(v), sum(us for _, us in v))
+    tot = sum(us for _, us in rows.values()) or 1.0
     print("| calls | total us | avg us | % | workgroups | kernel |")
     print("|---:|---:|---:|---:|---|---|")
-    for (name, grid), (n, us) in sorted(agg.items(), key=lambda kv: -kv[1][1])[:top]:
+    for (name, grid), (n, us) in sorted(rows.items(), key=lambda kv: -kv[1][1])[:top]:
         print(f"| {n} | {us:.1f} | {us / n:.2f} | {100 * us / tot:.2f} | {grid[0]}x{grid[1]}x{grid[2]} | `{name}` |")
 
 
-def summarize_counters(path, top, last=0):
+def summarize_counters(path, top, last=0, tail=0):
     """Per (kernel, grid size, counter) mean value per dispatch of a rocprofv3
-    counter collection (CSV); with last > 0 only each kernel's last dispatches."""
+    counter collection (CSV); with last > 0 only each kernel's last
+    dispatches, with tail > 0 only the run's last tail dispatches."""
     import csv
     agg = {}
     with open(path) as fh:
-        for r in csv.DictReader(fh):
-            key = (_short_kernel(_col(r, "Kernel_Name")), _col(r, "Grid_Size"), _col(r, "Counter_Name"),
-                   int(_col(r, "Dispatch_Id")))
-            agg[key] = agg.get(key, 0.0) + float(_col(r, "Counter_Value"))
+        rows = list(csv.DictReader(fh))
+    keep = None
+    if tail > 0:
+        keep = set(sorted({int(_col(r, "Dispatch_Id")) for r in rows})[-tail:])
+    for r in rows:
+        disp = int(_col(r, "Dispatch_Id"))
+        if keep is not None and disp not in keep:
+            continue
+        key = (_short_kernel(_col(r, "Kernel_Name")), _col(r, "Grid_Size"), _col(r, "Counter_Name"), disp)
+        agg[key] = agg.get(key, 0.0) + float(_col(r, "Counter_Value"))
     by = {}
     for (name, grid, counter, disp), v in agg.items():
         by.setdefault((name, grid, counter), []).append((disp, v))
@@ -407,17 +433,19 @@ def main():
     ap.add_argument("--summarize-trace", metavar="CSV", help="print a per-kernel table of a rocprofv3 kernel trace")
     ap.add_argument("--summarize-counters", metavar="CSV", help="print per-kernel means of a rocprofv3 counter run")
     ap.add_argument("--top", type=int, default=25)
-    ap.add_argument("--last", type=int, default=0, help="--summarize-counters: only the last N dispatches per kernel")
-    ap.add_argument("--replay", type=int, default=0,
-                    help="after timing, run the roofline call N more times at its shape (for counter passes)")
+    ap.add_argument("--last", type=int, default=0, help="--summarize-trace / --summarize-counters: only the last N dispatches per kernel")
+    ap.add_argument("--tail", type=int, default=0,
+                    help="--summarize-trace / --summarize-counters: only the run's last N dispatches")
+    ap.add_argument("--replay", type=int, default=20,
+                    help="launches of the roofline call replayed after the timed steps to time the kernel")
     ap.add_argument("--digest", action="store_true", help="print the kernel source digest")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 1 GiB (3 times), the reference for HBM counters")
     args = ap.parse_args()
     if args.summarize_trace:
-        return summarize_trace(args.summarize_trace, args.top)
+        return summarize_trace(args.summarize_trace, args.top, args.last, args.tail)
     if args.summarize_counters:
-        return summarize_counters(args.summarize_counters, args.top, args.last)
+        return summarize_counters(args.summarize_counters, args.top, args.last, args.tail)
     if args.digest:
         return print(source_digest())
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -440,6 +468,8 @@ def main():
     spec = WORKLOADS[args.workload]
     wl = Mlp(**spec)
     dtype = spec["dtype"]
+    if not args.no_cpu_baseline:
+        wl.host_copies()  # the oracle's inputs, taken before any GPU timing: the replay below is the last GPU work
 
     rates = sorted({0.0, 0.3, 0.5, 0.7, args.p})
     results = {}
@@ -472,12 +502,21 @@ def main():
         g[2] += fl
     shape, (count, ms_sum, fl_sum, shape_it) = max(groups.items(), key=lambda kv: (kv[1][2], kv[0]))
     call_ms, call_flops = ms_sum / count, fl_sum / count
-    achieved = call_flops / (call_ms * 1e-3) / 1e12
+    # the kernel's own launch duration: the same call at the same shape replayed
+    # back to back right after the timed steps (in the steps, a small call's
+    # event bracket also holds the time its launch waits for the host)
+    wl.set_rate(args.p)
+    launch_ms = wl.replay(shape_it, (kind, layer), args.replay)
+    print(f"# replayed {kind} layer {layer} of step {shape_it} ({shape}) {args.replay} times: "
+          f"{launch_ms * 1e3:.2f} us per launch", file=sys.stderr, flush=True)
+    achieved = call_flops / (launch_ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
                 "frac": achieved / PEAK_TFLOPS[dtype],
                 "traffic": traffic_record(spec["name"], kind, layer, shape),
                 "kernel": f"gemm ({kind}, layer {layer}), M x N x K = {shape[0]} x {shape[1]} x {shape[2]}",
-                "launches": count, "avg_launch_us": call_ms * 1e3, "flops_per_launch": call_flops,
+                "avg_launch_us": launch_ms * 1e3, "launches": args.replay, "flops_per_launch": call_flops,
+                "in_step": {"avg_call_us": call_ms * 1e3, "calls": count,
+                            "achieved": call_flops / (call_ms * 1e-3) / 1e12},
                 "call_share_of_step": sum(head["call_ms"]) / head["ms"]}
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
@@ -494,12 +533,6 @@ def main():
                   for p in rates},
         "roofline": roofline,
     }
-    if args.replay > 0:
-        wl.set_rate(args.p)
-        wl.replay(shape_it, (kind, layer), args.replay)
-        torch.cuda.synchronize()
-        print(f"# replayed {kind} layer {layer} of step {shape_it} ({shape}) {args.replay} times",
-              file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.p, args.cpu_budget)
     print(json.dumps(out), flush=True)
