@@ -61,10 +61,10 @@ class Mlp:
         self.plans = [api.ard_row_plan() for _ in range(L - 1)]
         # compact weights of the layers whose inputs are dropped (built once per
         # step, shared by fwd and bwd_data) and one workspace for split-K sums:
-        # at most 256 output tiles of 128 x 128 fp32
+        # at most two rounds of 256 output tiles of 256 x 256 fp32
         self.Wc = [None] + [torch.zeros(dims[l + 1] * ((dims[l] + 7) // 8 * 8), dtype=sdt, device=dev)
                             for l in range(1, L)]
-        self.ws = torch.empty(256 * 128 * 128, dtype=torch.float32, device=dev)
+        self.ws = torch.empty(2 * 256 * 256 * 256, dtype=torch.float32, device=dev)
         self.K = None
         # raw device addresses and the stream handle, resolved once: the step
         # then costs one C call per launch with no per-call tensor lookups

@@ -551,25 +551,39 @@ template <typename T>
 struct FastCfgs;
 template <>
 struct FastCfgs<bf16> {
-  using Huge = FastCfg<bf16, 256, 256, 32, 4, 2, 4, 1>;   // 128 KB LDS, 8 waves (2 per SIMD)
+  using Huge = FastCfg<bf16, 256, 256, 64, 2, 2, 4, 1>;   // 128 KB LDS, 8 waves (2 per SIMD)
+  using Wide = FastCfg<bf16, 128, 256, 32, 4, 2, 4, 1>;   // 96 KB, 8 waves
+  using Tall = FastCfg<bf16, 256, 128, 32, 4, 4, 2, 1>;   // 96 KB, 8 waves
   using Big = FastCfg<bf16, 128, 128, 64, 3, 2, 2, 1>;    // 96 KB
   using Small = FastCfg<bf16, 32, 32, 128, 4, 1, 1, 4>;   // 64 KB
 };
 template <>
 struct FastCfgs<float> {
   using Huge = FastCfg<float, 128, 128, 32, 4, 2, 2, 1>;  // 128 KB
+  using Wide = Huge;
+  using Tall = Huge;
   using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 1>;     // 96 KB
   using Small = FastCfg<float, 32, 32, 64, 4, 1, 1, 4>;   // 64 KB
 };
 
+enum FastKind { FAST_HUGE, FAST_WIDE, FAST_TALL, FAST_BIG, FAST_SMALL };
+
 struct FastPlan {
-  int kind;    // TILE_BIG (Huge), TILE_MEDIUM (Big), TILE_SMALL (Small)
-  int splits;
+  int kind;    // FastKind
+  int splits;  // workgroups per output tile along K (partials reduced by a second kernel)
 };
 
-template <typename T>
-inline FastPlan plan_fast(int M, int N, int K, int kbatch, int batch) {
-  using C = FastCfgs<T>;
+// Split count s for a tile count: the largest power of two that keeps the grid
+// within one round of the chip and every split at least kMinSlabsPerSplit slabs.
+inline int fast_splits(int64_t tiles, int64_t slabs) {
+  int s = 1;
+  while (tiles * s * 2 <= kTargetBlocks && slabs / (s * 2) >= kMinSlabsPerSplit && s * 2 <= kMaxSplits) s *= 2;
+  return s;
+}
+
+// fp32: the largest tile whose grid still covers 5/8 of the chip, then split-K.
+inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
+  using C = FastCfgs<float>;
   auto tiles_of = [&](int bm, int bn) {
     return static_cast<int64_t>((M + bm - 1) / bm) * ((N + bn - 1) / bn) * batch;
   };
@@ -577,23 +591,71 @@ inline FastPlan plan_fast(int M, int N, int K, int kbatch, int batch) {
   int bk;
   int64_t tiles;
   if (tiles_of(C::Huge::BM, C::Huge::BN) >= kTargetBlocks * 5 / 8) {
-    p.kind = TILE_BIG;
+    p.kind = FAST_HUGE;
     bk = C::Huge::BK;
     tiles = tiles_of(C::Huge::BM, C::Huge::BN);
   } else if (tiles_of(C::Big::BM, C::Big::BN) >= kTargetBlocks * 5 / 8) {
-    p.kind = TILE_MEDIUM;
+    p.kind = FAST_BIG;
     bk = C::Big::BK;
     tiles = tiles_of(C::Big::BM, C::Big::BN);
   } else {
-    p.kind = TILE_SMALL;
+    p.kind = FAST_SMALL;
     bk = C::Small::BK;
     tiles = tiles_of(C::Small::BM, C::Small::BN);
   }
-  const int64_t slabs = static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk);
-  int s = 1;
-  while (tiles * s * 2 <= kTargetBlocks && slabs / (s * 2) >= kMinSlabsPerSplit && s * 2 <= kMaxSplits) s *= 2;
-  p.splits = s;
+  p.splits = fast_splits(tiles, static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk));
   return p;
+}
+
+// bf16: the (configuration, split) pair with the smallest modelled time. A
+// workgroup's time is its MFMA work (whole tiles and slabs) over the rate one
+// workgroup of that configuration reaches with the chip full (measured on
+// MI355X), somewhat faster when fewer workgroups than compute units share the
+// chip; workgroups beyond the first 256 run in further rounds; a split adds
+// the partial-sum round trip and its reduction launch.
+inline FastPlan plan_fast_bf16(int M, int N, int K, int kbatch, int batch) {
+  using C = FastCfgs<bf16>;
+  struct Cand {
+    int kind, bm, bn, bk;
+    double rate;  // flop/s per workgroup with 256 workgroups resident
+  };
+  static const Cand cands[] = {
+      {FAST_HUGE, C::Huge::BM, C::Huge::BN, C::Huge::BK, 4.2e12},
+      {FAST_WIDE, C::Wide::BM, C::Wide::BN, C::Wide::BK, 3.5e12},
+      {FAST_TALL, C::Tall::BM, C::Tall::BN, C::Tall::BK, 3.4e12},
+      {FAST_BIG, C::Big::BM, C::Big::BN, C::Big::BK, 2.7e12},
+      {FAST_SMALL, C::Small::BM, C::Small::BN, C::Small::BK, 0.5e12},
+  };
+  const int64_t kb = kbatch > 0 ? kbatch : 1;
+  FastPlan best = {FAST_SMALL, 1};
+  double best_t = 1e300;
+  for (const Cand& c : cands) {
+    const int64_t tiles = static_cast<int64_t>((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn) * batch;
+    const int64_t slabs = kb * ((K + c.bk - 1) / c.bk);
+    for (int s = 1; s <= kMaxSplits; s *= 2) {
+      if (s > 1 && (slabs / s < kMinSlabsPerSplit || tiles * s > 2 * kTargetBlocks)) break;
+      const int64_t wgs = tiles * s;
+      const int64_t rounds = (wgs + kTargetBlocks - 1) / kTargetBlocks;
+      const double occ = wgs < kTargetBlocks ? static_cast<double>(wgs) / kTargetBlocks : 1.0;
+      const double rate = c.rate * (1.0 + 0.3 * (1.0 - occ));
+      const double work = 2.0 * c.bm * c.bn * c.bk * ((slabs + s - 1) / s);
+      double t = rounds * work / rate;
+      if (s > 1) t += 4.0 * M * N * batch * (s + 1) / 5e12 + 3e-6;
+      if (t < best_t) {
+        best_t = t;
+        best = {c.kind, s};
+      }
+    }
+  }
+  return best;
+}
+
+template <typename T>
+inline FastPlan plan_fast(int M, int N, int K, int kbatch, int batch) {
+  if constexpr (sizeof(T) == 2)
+    return plan_fast_bf16(M, N, K, kbatch, batch);
+  else
+    return plan_fast_f32(M, N, K, kbatch, batch);
 }
 
 template <typename T>
@@ -632,9 +694,18 @@ inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float
   g.splits = p.splits;
   g.partial = partial;
   using C = FastCfgs<T>;
-  if (p.kind == TILE_BIG) return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI>(g, batch, stream);
-  if (p.kind == TILE_MEDIUM) return launch_fast<typename C::Big, AMC, BMC, OutT, EPI>(g, batch, stream);
-  return launch_fast<typename C::Small, AMC, BMC, OutT, EPI>(g, batch, stream);
+  switch (p.kind) {
+    case FAST_HUGE:
+      return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI>(g, batch, stream);
+    case FAST_WIDE:
+      return launch_fast<typename C::Wide, AMC, BMC, OutT, EPI>(g, batch, stream);
+    case FAST_TALL:
+      return launch_fast<typename C::Tall, AMC, BMC, OutT, EPI>(g, batch, stream);
+    case FAST_BIG:
+      return launch_fast<typename C::Big, AMC, BMC, OutT, EPI>(g, batch, stream);
+    default:
+      return launch_fast<typename C::Small, AMC, BMC, OutT, EPI>(g, batch, stream);
+  }
 }
 
 }  // namespace ard

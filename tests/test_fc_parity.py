@@ -239,7 +239,17 @@ def test_pregated_gradient_and_input_gate(dtype):
     # fp32 128 x 128 tiles (fwd, bwd_weight) with a partial last K slab
     ("f32", 1024, 2040, 4096, ((1, 0), (1, 0))),
     ("f32", 1024, 2040, 4096, ((2, 1), (3, 0))),
-], ids=["bf16-patterned", "bf16-dense-ragged", "f32-dense-ragged", "f32-patterned"])
+    # bf16 tile configurations and split-K paths the planner takes for these
+    # shapes: 128x128 tiles split 4 (fwd), 128x256 tiles split 16 (bwd_data)
+    ("bf16", 256, 1024, 2048, ((3, 0), (1, 0))),
+    # 256x256 tiles split 4 (fwd, bwd_data)
+    ("bf16", 512, 8192, 8192, ((1, 0), (1, 0))),
+    # 256x128 tiles split 4 (bwd_weight)
+    ("bf16", 2048, 1024, 4096, ((3, 0), (1, 0))),
+    # 32x32 tiles split 4 (bwd_data)
+    ("bf16", 256, 1024, 2048, ((4, 1), (1, 0))),
+], ids=["bf16-patterned", "bf16-dense-ragged", "f32-dense-ragged", "f32-patterned", "bf16-t128-split",
+        "bf16-t256-split", "bf16-t256x128-split", "bf16-t32-split"])
 def test_wide_layer_full_size_sampled(dtype, B, K, N, pats):
     """One hidden layer of the wide MLP in the launch configuration of the
     benchmark (compact weights, SKIP, workspace), against the oracle on sampled
