@@ -90,30 +90,35 @@ class Mlp:
                     api.ARD_DROPPED_SKIP)
             self.descs.append(api.fc_desc(*args))
             self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT) if l > 0 else self.descs[-1])
-        # the calls of one step, in order, with their arguments resolved once
+        # the calls of one step, in order, with their arguments resolved once.
+        # A layer whose inputs are all kept in a step (period 1) needs no
+        # compact weight copy: it reads W itself through the full-layout
+        # descriptor; so every layer has two call sets, picked per step.
         P, st = self.ptr, self.stream
-        Wf = [P["W"][0]] + P["Wc"][1:]
         acts = [P["X0"]] + P["Y"]
         ws = (self.ws.data_ptr(), self.ws.numel() * 4)
-        self.calls, self.seq = {}, []
-        for l in range(self.L):
-            self.calls[("fwd", l)] = (api.ard_fc_fwd, (self.cdescs[l], acts[l], Wf[l], P["bias"][l], P["Y"][l],
-                                                      ws, st), {})
-        # backward: each bwd_data also applies the ReLU derivative of the layer
-        # below (Xgate = that layer's output), so every dY[l] below the top is
-        # already gated and is passed with Yt = None
-        for l in reversed(range(self.L)):
-            self.calls[("bwd_weight", l)] = (api.ard_fc_bwd_weight, (self.cdescs[l], acts[l], P["dY"][l], None,
-                                                                     P["dW"][l], P["db"][l], ws, st), {})
+
+        def layer_calls(l, compact):
+            desc = self.cdescs[l] if compact else self.descs[l]
+            w = P["Wc"][l] if compact else P["W"][l]
+            calls = {("fwd", l): (api.ard_fc_fwd, (desc, acts[l], w, P["bias"][l], P["Y"][l], ws, st), {}),
+                     ("bwd_weight", l): (api.ard_fc_bwd_weight, (desc, acts[l], P["dY"][l], None, P["dW"][l],
+                                                                 P["db"][l], ws, st), {})}
+            # backward: each bwd_data also applies the ReLU derivative of the layer
+            # below (Xgate = that layer's output), so every dY[l] below the top is
+            # already gated and is passed with Yt = None
             if l > 0:
-                self.calls[("bwd_data", l)] = (api.ard_fc_bwd_data, (self.cdescs[l], P["dY"][l], None, Wf[l],
-                                                                     P["dY"][l - 1], ws, st), {"Xgate": acts[l]})
-        order = [("fwd", l) for l in range(self.L)]
+                calls[("bwd_data", l)] = (api.ard_fc_bwd_data, (desc, P["dY"][l], None, w, P["dY"][l - 1], ws, st),
+                                          {"Xgate": acts[l]})
+            return calls
+
+        self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l > 0 else None}
+                            for l in range(self.L)]
+        self.order = [("fwd", l) for l in range(self.L)]
         for l in reversed(range(self.L)):
-            order.append(("bwd_weight", l))
+            self.order.append(("bwd_weight", l))
             if l > 0:
-                order.append(("bwd_data", l))
-        self.seq = [(key,) + self.calls[key] for key in order]
+                self.order.append(("bwd_data", l))
 
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
@@ -150,18 +155,24 @@ class Mlp:
 
     def prepare(self, it):
         """Samples this step's patterns, compacts them on the device and gathers
-        the compact weights of the layers whose inputs are dropped."""
+        the compact weights of the layers whose inputs are dropped. Returns the
+        patterns and the step's calls {key: (fn, args, kwargs)}."""
         api, P, st = self.api, self.ptr, self.stream
         pats = self.patterns(it)
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, P["idx"][l], st, plan=self.plans[l])
+        calls = dict(self.layer_calls[0][False])
         for l in range(1, self.L):
-            api.ard_fc_compact_weights(self.cdescs[l], P["W"][l], P["Wc"][l], st)
-        return pats
+            compact = pats[l - 1][0] > 1
+            if compact:
+                api.ard_fc_compact_weights(self.cdescs[l], P["W"][l], P["Wc"][l], st)
+            calls.update(self.layer_calls[l][compact])
+        return pats, calls
 
     def step(self, it, timed_call=None, events=None):
-        pats = self.prepare(it)
-        for key, fn, args, kw in self.seq:
+        pats, calls = self.prepare(it)
+        for key in self.order:
+            fn, args, kw = calls[key]
             if key == timed_call:
                 events[0].record()
                 fn(*args, **kw)
@@ -175,8 +186,8 @@ class Mlp:
         mean GPU time per launch (ms, HIP events on the call's stream around
         the whole replay)."""
         torch = self.torch
-        self.prepare(it)
-        fn, args, kw = self.calls[key]
+        _, calls = self.prepare(it)
+        fn, args, kw = calls[key]
         fn(*args, **kw)  # the same call once untimed: operands in cache as in the step
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -264,10 +275,10 @@ def roofline_call(wl, first_it, steps):
     totals = {}
     for i in range(steps):
         _, per = wl.kept_flops(wl.patterns(first_it + i))
-        for key in (k for k, *_ in wl.seq):
+        for key in wl.order:
             totals[key] = totals.get(key, 0.0) + per.get(key, 0.0)
     best = max(totals.values())
-    return next(k for k, *_ in wl.seq if totals.get(k, 0.0) == best)
+    return next(k for k in wl.order if totals.get(k, 0.0) == best)
 
 
 def cpu_baseline(wl, p, budget_s):

@@ -43,44 +43,82 @@ __global__ void zero_dropped_weights_kernel(float* __restrict__ dW, int32_t K, i
     if (!row_kept || (c % in_period) != in_offset) row[c] = 0.0f;
 }
 
-// dbias[idx[i]] = sum_b G[idx[i]][b] with G = scale * dY * [Y > 0] (or
-// scale * dY); one block per kept row, fixed-order reduction.
+// dbias[r] = scale * sum_b G[r][b] for the kept rows r = offset + period * i,
+// with G = dY * [Y > 0] when Y is given, else dY. One wave per kept row: each
+// lane sums its 16-byte chunks of the row in order, then the lanes are summed
+// in a fixed tree, so the result does not depend on timing. vec: rows start
+// 16-byte aligned and B is a whole number of chunks.
 template <typename T>
-__global__ void __launch_bounds__(256) dbias_kernel(const T* __restrict__ dYt,
-                                                    const T* __restrict__ Yt, int32_t B,
-                                                    const int32_t* __restrict__ idx, float scale,
-                                                    int32_t relu, float* __restrict__ dbias) {
-  __shared__ float part[256];
-  const int64_t row = idx ? idx[blockIdx.x] : blockIdx.x;
+__global__ void __launch_bounds__(256) dbias_kernel(const T* __restrict__ dYt, const T* __restrict__ Yt, int32_t B,
+                                                    int32_t kept, int32_t period, int32_t offset, float scale,
+                                                    int32_t relu, int32_t vec, float* __restrict__ dbias) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= kept) return;  // whole waves leave together
+  const int lane = threadIdx.x & 63;
+  const int64_t row = offset + static_cast<int64_t>(period) * i;
   const T* dy = dYt + row * B;
   const T* y = Yt ? Yt + row * B : nullptr;
-  float s = 0.0f;
-  for (int b = threadIdx.x; b < B; b += 256) {
-    float g = to_f32(dy[b]);
-    if (relu && !(to_f32(y[b]) > 0.0f)) g = 0.0f;
-    s += g;
+  constexpr int EPC = 16 / static_cast<int>(sizeof(T));
+  float sum = 0.0f;
+  if (vec) {
+    for (int b0 = lane * EPC; b0 < B; b0 += 64 * EPC) {
+      const u32x4 gv = *reinterpret_cast<const u32x4*>(dy + b0);
+      u32x4 yv = u32x4{0u, 0u, 0u, 0u};
+      if (relu) yv = *reinterpret_cast<const u32x4*>(y + b0);
+      const T* ge = reinterpret_cast<const T*>(&gv);
+      const T* ye = reinterpret_cast<const T*>(&yv);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) sum += (relu && !(to_f32(ye[e]) > 0.0f)) ? 0.0f : to_f32(ge[e]);
+    }
+  } else {
+    for (int b = lane; b < B; b += 64) sum += (relu && !(to_f32(y[b]) > 0.0f)) ? 0.0f : to_f32(dy[b]);
   }
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) dbias[row] = scale * part[0];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) sum += __shfl_down(sum, off, 64);
+  if (lane == 0) dbias[row] = scale * sum;
 }
 
 namespace {
 
-// Gathers W[S_out][S_in] into Wc[kout][ldc]; padding columns are 0.
+// Gathers W[S_out][S_in] into Wc[kout][ldc]; padding columns are 0. Kept rows
+// and columns are arithmetic progressions (source row out_offset +
+// out_period * i, source column in_offset + in_period * j). One block per
+// compact row: the source row passes through LDS in segments read with
+// coalesced 16-byte loads (vec: rows start 16-byte aligned and hold whole
+// chunks; else element loads), then consecutive threads write consecutive
+// kept columns.
 template <typename T>
-__global__ void compact_weights_kernel(const T* __restrict__ W, int64_t K, const int32_t* __restrict__ out_idx,
-                                       const int32_t* __restrict__ in_idx, int32_t kin, int64_t ldc,
-                                       T* __restrict__ Wc) {
+__global__ void __launch_bounds__(256) compact_weights_kernel(const T* __restrict__ W, int64_t K, int32_t out_period,
+                                                              int32_t out_offset, int32_t in_period, int32_t in_offset,
+                                                              int32_t kin, int64_t ldc, int32_t vec,
+                                                              T* __restrict__ Wc) {
+  constexpr int SEG = 4096;  // source columns per segment
+  constexpr int EPC = 16 / static_cast<int>(sizeof(T));
+  __shared__ __attribute__((aligned(16))) T seg[SEG];
   const int64_t i = blockIdx.x;
-  const T* row = W + gather(out_idx, i) * K;
+  const T* row = W + (out_offset + static_cast<int64_t>(out_period) * i) * K;
   T* crow = Wc + i * ldc;
-  for (int64_t j = threadIdx.x; j < ldc; j += blockDim.x)
-    crow[j] = j < kin ? row[gather(in_idx, j)] : from_f32<T>(0.0f);
+  const int t = threadIdx.x;
+  if (kin > 0) {
+    const int64_t first = in_offset, last = in_offset + static_cast<int64_t>(in_period) * (kin - 1);
+    for (int64_t s0 = first / SEG * SEG; s0 <= last; s0 += SEG) {
+      const int64_t n = K - s0 < SEG ? K - s0 : SEG;  // columns of this segment
+      __syncthreads();  // the previous segment is no longer read
+      if (vec) {
+        for (int64_t c = t * EPC; c < n; c += 256 * EPC)
+          *reinterpret_cast<u32x4*>(seg + c) = *reinterpret_cast<const u32x4*>(row + s0 + c);
+      } else {
+        for (int64_t c = t; c < n; c += 256) seg[c] = row[s0 + c];
+      }
+      __syncthreads();
+      // kept columns j with source in [s0, s0 + n)
+      int64_t jlo = s0 <= first ? 0 : (s0 - first + in_period - 1) / in_period;
+      int64_t jhi = (s0 + n - 1 - first) / in_period + 1;
+      if (jhi > kin) jhi = kin;
+      for (int64_t j = jlo + t; j < jhi; j += 256) crow[j] = seg[first + in_period * j - s0];
+    }
+  }
+  for (int64_t j = kin + t; j < ldc; j += 256) crow[j] = from_f32<T>(0.0f);
 }
 
 struct FcShape {
@@ -182,8 +220,10 @@ inline bool vec_rows(int64_t ld, size_t esize) { return (ld * static_cast<int64_
 template <typename T>
 hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t stream) {
   if (s.kout == 0) return hipSuccess;
+  const int vec = aligned16(W) && (static_cast<int64_t>(s.K) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
   hipLaunchKernelGGL(compact_weights_kernel<T>, dim3(s.kout), dim3(256), 0, stream, static_cast<const T*>(W),
-                     static_cast<int64_t>(s.K), s.out_idx, s.in_idx, s.kin, s.ldc, static_cast<T*>(Wc));
+                     static_cast<int64_t>(s.K), s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, s.ldc,
+                     vec, static_cast<T*>(Wc));
   return hipGetLastError();
 }
 
@@ -201,6 +241,25 @@ GemmOperand kept_rows(const void* p, const void* y, int64_t ld, int32_t period, 
   o.relu = relu;
   o.scale = 1.0f;
   return o;
+}
+
+// The output view of the fast GEMM: rows offset + period * i of a row-major
+// matrix (row stride ld, elements of esize bytes) and columns col_offset +
+// col_period * j, folded into base and strides like the operands; the bias
+// and the output gate (same layout as the output) follow the rows.
+GemmOutput strided_out(void* p, int64_t ld, size_t esize, int32_t period, int32_t offset, int32_t col_period,
+                       int32_t col_offset, const float* bias, int32_t relu, float scale, const void* gate) {
+  const int64_t skip = static_cast<int64_t>(offset) * ld + col_offset;
+  GemmOutput c = {};
+  c.p = static_cast<char*>(p) + skip * static_cast<int64_t>(esize);
+  c.ld = ld * period;
+  c.bias = bias ? bias + offset : nullptr;
+  c.bias_stride = period;
+  c.relu = relu;
+  c.scale = scale;
+  c.gate = gate ? static_cast<const char*>(gate) + skip * static_cast<int64_t>(esize) : nullptr;
+  c.col_stride = col_period;
+  return c;
 }
 
 // The view of W used by fwd / bwd_data: either the full matrix's kept output
@@ -242,6 +301,8 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   if (fast_ok(g, sizeof(T))) {
+    g.c = strided_out(Yt, s.B, sizeof(T), s.out_period, s.out_offset, 1, 0, bias, d->act == ARD_ACT_RELU,
+                      d->scale, nullptr);
     ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -278,6 +339,7 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   if (fast_ok(g, sizeof(T))) {
+    g.c = strided_out(dXt, s.B, sizeof(T), s.in_period, s.in_offset, 1, 0, nullptr, 0, d->scale, Xgate);
     ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
@@ -311,6 +373,8 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
   if (fast_ok(g, sizeof(T))) {
+    g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
+                      d->scale, nullptr);
     ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD>(g, 1, stream, partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
@@ -320,9 +384,11 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
         g, 1, v, v, stream, partial)));
   }
   if (dbias && s.kout > 0) {
-    hipLaunchKernelGGL(dbias_kernel<T>, dim3(s.kout), dim3(256), 0, stream,
-                       static_cast<const T*>(dYt), static_cast<const T*>(Yt), s.B, s.out_idx,
-                       d->scale, gated ? 1 : 0, dbias);
+    const int vec = aligned16(dYt) && (!gated || aligned16(Yt)) &&
+                    (static_cast<int64_t>(s.B) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
+    hipLaunchKernelGGL(dbias_kernel<T>, dim3((s.kout + 3) / 4), dim3(256), 0, stream,
+                       static_cast<const T*>(dYt), static_cast<const T*>(Yt), s.B, s.kout, s.out_period,
+                       s.out_offset, d->scale, gated ? 1 : 0, vec, dbias);
     ARD_LAUNCH_CHECK();
   }
   if (d->dropped == ARD_DROPPED_ZERO && (s.out_period > 1 || s.in_period > 1)) {

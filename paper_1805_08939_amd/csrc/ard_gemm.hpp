@@ -72,7 +72,17 @@ struct GemmOutput {
                          // dropout scale of the backward passes)
   const void* gate;      // EPI_FWD: if set, multiply by [gate > 0] at the output
                          // position (the ReLU derivative of the layer below)
+  int64_t col_stride;    // elements between consecutive output columns when cidx is NULL (0 = 1)
+  int64_t bias_stride;   // elements between the bias entries of consecutive rows when ridx is NULL (0 = 1)
 };
+
+// Output column offset of compact column n, and bias index of compact row m.
+__device__ __forceinline__ int64_t out_col(const GemmOutput& c, int64_t n) {
+  return c.cidx ? static_cast<int64_t>(c.cidx[n]) : n * (c.col_stride > 1 ? c.col_stride : 1);
+}
+__device__ __forceinline__ int64_t bias_row(const GemmOutput& c, int64_t m) {
+  return c.ridx ? static_cast<int64_t>(c.ridx[m]) : m * (c.bias_stride > 1 ? c.bias_stride : 1);
+}
 
 // The contraction runs over kbatch x K: K batch kb reads both operands at
 // base + kb * kbstride (a sum over time steps of an LSTM, say). kbatch 0 or 1
@@ -352,12 +362,12 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, f32x16 (&acc)[Cfg:
       const int m = m0 + wm * Cfg::TM + 32 * i + 8 * (r >> 2) + 4 * lh + (r & 3);
       if (m >= g.M) continue;
       const int64_t orow = gather(g.c.ridx, m);
-      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
+      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         const int n = n0 + wn * Cfg::TN + 32 * j + lr;
         if (n >= g.N) continue;
-        const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+        const int64_t o = orow * g.c.ld + out_col(g.c, n);
         float v = epilogue<EPI>(g.c, acc[i][j][r], bias);
         if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
           v = 0.0f;
@@ -442,9 +452,9 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs g) {
   for (int s = 0; s < g.splits; ++s) v += part[s * mn];
   const int64_t m = e / g.N, n = e % g.N;
   const int64_t orow = gather(g.c.ridx, m);
-  const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
+  const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
   OutT* out = static_cast<OutT*>(g.c.p) + bz * g.c.bstride;
-  const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+  const int64_t o = orow * g.c.ld + out_col(g.c, n);
   v = epilogue<EPI>(g.c, v, bias);
   if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
     v = 0.0f;
@@ -548,8 +558,8 @@ __global__ void __launch_bounds__(256) gemm_small_kernel(GemmArgs g) {
       continue;
     }
     const int64_t orow = gather(g.c.ridx, m);
-    const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
-    const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+    const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
+    const int64_t o = orow * g.c.ld + out_col(g.c, n);
     v = epilogue<EPI>(g.c, v, bias);
     if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
       v = 0.0f;

@@ -359,6 +359,107 @@ struct SlabLoader {
   }
 };
 
+// Output of one wave's accumulator tile. Each block row of 32 rows passes
+// through the wave's own LDS region in fp32 (epilogue applied on the way in),
+// and every lane then writes 4 consecutive values of one output row (16 bytes
+// fp32, 8 bytes bf16): a store instruction covers whole 128-byte lines instead
+// of one element per lane. The ReLU gate of the layer below is read the same
+// way. Falls back to element stores when the output rows are not contiguous
+// or not aligned for those pieces. Called by all waves (it holds a barrier).
+template <typename OutT, class Cfg, int EPI>
+__device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0,
+                                           int wm, int wn, int64_t bz, int split, char* smem) {
+  const bool part = g.splits > 1;
+  const int64_t es = part ? 4 : static_cast<int64_t>(sizeof(OutT));
+  const int64_t ld = part ? g.N : g.c.ld;
+  char* base = part ? reinterpret_cast<char*>(g.partial + (bz * g.splits + split) * static_cast<int64_t>(g.M) * g.N)
+                    : reinterpret_cast<char*>(static_cast<OutT*>(g.c.p) + bz * g.c.bstride);
+  const char* gate = (!part && EPI == EPI_FWD && g.c.gate)
+                         ? reinterpret_cast<const char*>(static_cast<const OutT*>(g.c.gate) + bz * g.c.bstride)
+                         : nullptr;
+  const int64_t piece = 4 * es;
+  const bool vec = (part || (g.c.cidx == nullptr && g.c.col_stride <= 1 && g.c.ridx == nullptr)) &&
+                   (ld * es) % piece == 0 && reinterpret_cast<uintptr_t>(base) % piece == 0 &&
+                   reinterpret_cast<uintptr_t>(gate) % piece == 0;
+  if (!vec) {
+    store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
+    return;
+  }
+  // fp32 rows of TN values plus 32 bytes: the two half-waves' writes (rows r
+  // and r + 4) then fall on disjoint banks
+  constexpr int ROW = Cfg::TN * 4 + 32;
+  constexpr int CPRW = Cfg::TN / 4;  // 16-byte pieces per row
+  constexpr int RPI = 64 / CPRW;     // rows per read instruction
+  static_assert(Cfg::NW * 32 * ROW <= Cfg::LDS, "epilogue staging exceeds LDS");
+  lds_barrier();  // every wave is done with the stages
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lr = lane & 31, lh = lane >> 5;
+  char* region = smem + wave * 32 * ROW;
+  const int m0w = m0 + wm * Cfg::TM, n0w = n0 + wn * Cfg::TN;
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lh + (r & 3);
+      const int m = m0w + 32 * i + rl;
+      float bias = 0.0f;
+      if (!part && EPI == EPI_FWD && g.c.bias && m < g.M) bias = g.c.bias[bias_row(g.c, m)];
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j) {
+        float v = acc[i][j][r];
+        if (!part) v = epilogue<EPI>(g.c, v, bias);
+        *reinterpret_cast<float*>(region + rl * ROW + (32 * j + lr) * 4) = v;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 32 / RPI; ++t) {
+      const int rl = lane / CPRW + RPI * t, ch = lane % CPRW;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(region + rl * ROW + ch * 16);
+      const int m = m0w + 32 * i + rl, n = n0w + 4 * ch;
+      if (m >= g.M) continue;
+      const int64_t o = static_cast<int64_t>(m) * ld + n;
+      if (part) {
+        float* out = reinterpret_cast<float*>(base) + o;
+        if (n + 3 < g.N) {
+          *reinterpret_cast<f32x4*>(out) = v;
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (n + e < g.N) out[e] = v[e];
+        }
+        continue;
+      }
+      OutT* out = reinterpret_cast<OutT*>(base) + o;
+      const OutT* gt = gate ? reinterpret_cast<const OutT*>(gate) + o : nullptr;
+      if (n + 3 < g.N) {
+        OutT w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = from_f32<OutT>(v[e]);
+        if (gt) {
+          OutT gv[4];
+          if constexpr (sizeof(OutT) == 2)
+            *reinterpret_cast<uint2*>(gv) = *reinterpret_cast<const uint2*>(gt);
+          else
+            *reinterpret_cast<f32x4*>(gv) = *reinterpret_cast<const f32x4*>(gt);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (!(to_f32(gv[e]) > 0.0f)) w[e] = from_f32<OutT>(0.0f);
+        }
+        if constexpr (sizeof(OutT) == 2)
+          *reinterpret_cast<uint2*>(out) = *reinterpret_cast<const uint2*>(w);
+        else
+          *reinterpret_cast<f32x4*>(out) = *reinterpret_cast<const f32x4*>(w);
+      } else {
+        for (int e = 0; e < 4; ++e) {
+          if (n + e >= g.N) break;
+          float x = v[e];
+          if (gt && !(to_f32(gt[e]) > 0.0f)) x = 0.0f;
+          out[e] = from_f32<OutT>(x);
+        }
+      }
+    }
+  }
+}
+
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   using T = typename Cfg::T;
@@ -488,7 +589,7 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   }
   wait_vm<0>();  // no direct load may still write LDS past this point
   if constexpr (Cfg::KSPLIT == 1) {
-    store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
+    fast_store<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split, smem);
   } else {
     // the KSPLIT waves of one output tile reduce through LDS; wave ks finishes
     // the accumulator registers t (flattened over i, j, r) with t % KSPLIT == ks
@@ -520,8 +621,8 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
         continue;
       }
       const int64_t orow = gather(g.c.ridx, m);
-      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[orow] : 0.0f;
-      const int64_t o = orow * g.c.ld + gather(g.c.cidx, n);
+      const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
+      const int64_t o = orow * g.c.ld + out_col(g.c, n);
       v = epilogue<EPI>(g.c, v, bias);
       if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[bz * g.c.bstride + o]) > 0.0f))
         v = 0.0f;
