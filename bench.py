@@ -66,6 +66,8 @@ class Mlp:
                             for l in range(1, L)]
         self.ws = torch.empty(2 * 256 * 256 * 256, dtype=torch.float32, device=dev)
         self.K = None
+        self.config = {"workload": name, "global_batch": batch, "layers": dims,
+                       "patterns": "row-based, sampled per step from K(p), n_max 16", "dropped": "skip"}
         # raw device addresses and the stream handle, resolved once: the step
         # then costs one C call per launch with no per-call tensor lookups
         self.stream = torch.cuda.current_stream().cuda_stream
@@ -142,6 +144,10 @@ class Mlp:
             if l > 0:
                 per[("bwd_data", l)] = f
         return sum(per.values()), per
+
+    @staticmethod
+    def shape_label(shape):
+        return "M x N x K = %d x %d x %d" % tuple(shape)
 
     def gemm_shape(self, pats, kind, l):
         """(M, N, K) of the GEMM a call runs: fwd kept_out x B x kept_in, bwd_data
@@ -227,10 +233,188 @@ class Mlp:
                       "dY": self.dY[-1].double().cpu().numpy().T.copy()}
 
 
+class TileLayer:
+    """One layer under a tile-based pattern: each step samples a Bernoulli(1 - p)
+    keep bitmap over the 64 x 64 tiles of W[N][K], uploads it (its own pinned
+    slot per step), builds the kept-tile lists on the device and runs fwd,
+    bwd_data and bwd_weight, reading and writing only kept tiles."""
+
+    def __init__(self, name, n, k, batch, tile, dtype, seed, w_std):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.N, self.K, self.B, self.tile, self.dtype = name, n, k, batch, tile, dtype
+        self.tn, self.tk = n // tile, k // tile
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        sdt = synth.storage_dtype(dtype)
+        X = synth.to_storage(synth.normal(g, (batch, k)), dtype)
+        W = synth.to_storage(synth.normal(g, (n, k), w_std), dtype)
+        dY = synth.to_storage(synth.normal(g, (batch, n)), dtype)
+        self._host_src = (X, W, dY)
+        self.Xt, self.W, self.dYt = X.T.contiguous().to(dev), W.to(dev), dY.T.contiguous().to(dev)
+        self.Yt = torch.empty(n, batch, dtype=sdt, device=dev)
+        self.dXt = torch.empty(k, batch, dtype=sdt, device=dev)
+        self.dW = torch.empty(n, k, dtype=torch.float32, device=dev)
+        self.words = (self.tn * self.tk + 31) // 32
+        self.bits_dev = torch.empty(self.words, dtype=torch.int32, device=dev)
+        self.plan_ws = torch.empty(max(api.ard_tile_plan_workspace_bytes(self.tn, self.tk), 16) // 4,
+                                   dtype=torch.int32, device=dev)
+        self.pinned = {}
+        self.desc = api.tile_desc(api.ARD_BF16 if dtype == "bf16" else api.ARD_F32, batch, k, n, 1.0,
+                                  api.ARD_DROPPED_SKIP)
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.order = [("fwd", 0), ("bwd_data", 0), ("bwd_weight", 0)]
+        self.config = {"workload": name, "global_batch": batch, "layer": [k, n], "tile": tile,
+                       "patterns": "Bernoulli tile bitmap per step, keep probability 1 - p", "dropped": "skip"}
+
+    def set_rate(self, p):
+        self.p = p
+
+    def patterns(self, it):
+        bits = self.api.ard_tile_bitmap_bernoulli(self.tn, self.tk, self.p, PATTERN_SEED, 0, it)
+        return bits, self.api.ard_bitmap_popcount(bits, self.tn * self.tk)
+
+    def kept_flops(self, pats):
+        f = 2.0 * self.B * self.tile * self.tile * pats[1]
+        per = {key: f for key in self.order}
+        return sum(per.values()), per
+
+    def gemm_shape(self, pats, kind, l):
+        return (self.N, self.B, self.K, pats[1])
+
+    @staticmethod
+    def shape_label(shape):
+        return "N x B x K = %d x %d x %d, %d kept 64 x 64 tiles" % tuple(shape)
+
+    def prepare(self, it):
+        torch, api = self.torch, self.api
+        bits, nnz = self.patterns(it)
+        slot = self.pinned.get(it)
+        if slot is None:  # one pinned buffer per step: the upload below never races the host
+            slot = torch.empty(self.words, dtype=torch.int32, pin_memory=True)
+            self.pinned[it] = slot
+        slot.numpy()[:] = bits.view("int32")
+        self.bits_dev.copy_(slot, non_blocking=True)
+        plan = api.ard_plan_tiles(self.N, self.K, self.tile, self.bits_dev, nnz, self.plan_ws, self.stream)
+        d, st = self.desc, self.stream
+        calls = {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
+                 ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
+                 ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
+        return (bits, nnz), calls
+
+    step = Mlp.step
+    replay = Mlp.replay
+
+    def oracle_step(self, pats):
+        import numpy as np
+        from oracle import patterns as opat
+        from oracle import tdp as otdp
+        grid = opat.bitmap_to_grid(list(pats[0]), self.tn, self.tk).astype(np.float64)
+        M = np.kron(grid, np.ones((self.tile, self.tile)))
+        X, W, dY = self._host
+        otdp.tdp_forward(X, W, M)
+        return otdp.tdp_backward(X, W, dY, M)
+
+    def host_copies(self):
+        from paper_1805_08939_amd import synth
+        self._host = tuple(synth.as_f64(t).numpy() for t in self._host_src)
+
+
+class Lstm:
+    """One LSTM layer whose hidden units take a row-based pattern sampled per
+    sequence from K(p): the gate GEMMs run on the kept hidden set (forward, then
+    BPTT backward)."""
+
+    def __init__(self, name, T, batch, inputs, hidden, dtype, seed):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.T, self.B, self.I, self.H, self.dtype = name, T, batch, inputs, hidden, dtype
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        X = synth.uniform(g, (T, batch, inputs), 0.1)
+        W = synth.uniform(g, (4 * hidden, inputs + hidden), 0.1)
+        b = synth.uniform(g, (4 * hidden,), 0.1)
+        dHs = synth.normal(g, (T, batch, hidden))
+        self._host_src = (X, W, b, dHs)
+        self.X = X.permute(0, 2, 1).contiguous().to(dev)
+        self.W, self.b = W.to(dev), b.to(dev)
+        self.dHs = dHs.permute(0, 2, 1).contiguous().to(dev)
+        self.Hs = torch.empty(T, hidden, batch, device=dev)
+        self.hT = torch.empty(hidden, batch, device=dev)
+        self.cT = torch.empty(hidden, batch, device=dev)
+        self.dX = torch.empty(T, inputs, batch, device=dev)
+        self.dW = torch.empty(4 * hidden, inputs + hidden, device=dev)
+        self.db = torch.empty(4 * hidden, device=dev)
+        self.dh0 = torch.empty(hidden, batch, device=dev)
+        self.dc0 = torch.empty(hidden, batch, device=dev)
+        self.idx = torch.empty(hidden, dtype=torch.int32, device=dev)
+        self.plan = api.ard_row_plan()
+        self.desc = api.lstm_desc(api.ARD_F32, T, batch, inputs, hidden, self.plan)
+        full = api.ard_plan_rows(hidden, 1, 0, self.idx)  # the workspace of the largest kept set
+        nbytes = api.ard_lstm_workspace_bytes(api.lstm_desc(api.ARD_F32, T, batch, inputs, hidden, full))
+        self.ws = torch.empty(max(nbytes, 16) // 4 + 1, device=dev)
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.order = [("fwd", 0), ("bwd", 0)]
+        self.config = {"workload": name, "global_batch": batch, "seq_len": T, "input": inputs, "hidden": hidden,
+                       "patterns": "row-based on hidden units, sampled per sequence from K(p), n_max 16"}
+
+    def set_rate(self, p):
+        self.p = p
+        self.K, _ = self.api.ard_search_distribution(p)
+
+    def patterns(self, it):
+        return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, 1, it)]
+
+    def kept_flops(self, pats):
+        S = self.api.ard_row_kept(self.H, *pats[0])
+        f = 2.0 * self.T * self.B * (self.I + S) * 4 * S  # input projection + recurrence
+        per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
+        return 3.0 * f, per
+
+    def gemm_shape(self, pats, kind, l):
+        return (self.T, self.B, self.I, self.api.ard_row_kept(self.H, *pats[0]))
+
+    @staticmethod
+    def shape_label(shape):
+        return "T, B, I = %d, %d, %d, %d kept hidden units" % tuple(shape)
+
+    def prepare(self, it):
+        api, st = self.api, self.stream
+        pats = self.patterns(it)
+        api.ard_plan_rows(self.H, *pats[0], self.idx, st, plan=self.plan)
+        d = self.desc
+        calls = {("fwd", 0): (api.ard_lstm_fwd, (d, self.X, self.W, self.b, None, None, self.Hs, self.hT,
+                                                  self.cT, self.ws, st), {}),
+                 ("bwd", 0): (api.ard_lstm_bwd, (d, self.X, self.dHs, None, None, self.ws, self.dX, self.dW,
+                                                  self.db, self.dh0, self.dc0, st), {})}
+        return pats, calls
+
+    step = Mlp.step
+    replay = Mlp.replay
+
+    def oracle_step(self, pats):
+        from oracle import lstm as olstm
+        from oracle import patterns as opat
+        X, W, b, dHs = self._host
+        m = opat.row_mask(self.H, *pats[0])
+        Hs, hT, cT, cache = olstm.lstm_forward(X, W, b, m)
+        return olstm.lstm_backward(X, W, m, cache, dHs)
+
+    def host_copies(self):
+        from paper_1805_08939_amd import synth
+        self._host = tuple(synth.as_f64(t).numpy() for t in self._host_src)
+
+
 WORKLOADS = {
-    "mlp784": dict(name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
+    "mlp784": dict(cls="Mlp", name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
                    dtype="f32", init="xavier", seed=1805 + 1),
-    "mlp8192": dict(name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
+    "tile4096": dict(cls="TileLayer", name="tile-4096x4096-bf16-b512-t64", n=4096, k=4096, batch=512, tile=64,
+                     dtype="bf16", seed=1805 + 2, w_std=0.02),
+    "lstm1024": dict(cls="Lstm", name="lstm-t35-b64-i1024-h1024-fp32", T=35, batch=64, inputs=1024, hidden=1024,
+                     dtype="f32", seed=1805 + 3),
+    "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
                     dtype="bf16", init="he", seed=1805 + 4),
 }
 
@@ -476,8 +660,9 @@ def main():
         return
     from paper_1805_08939_amd import _ffi
     _ffi.lib()
-    spec = WORKLOADS[args.workload]
-    wl = Mlp(**spec)
+    spec = dict(WORKLOADS[args.workload])
+    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "Lstm": Lstm}[spec.pop("cls")]
+    wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:
         wl.host_copies()  # the oracle's inputs, taken before any GPU timing: the replay below is the last GPU work
@@ -524,7 +709,7 @@ def main():
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
                 "frac": achieved / PEAK_TFLOPS[dtype],
                 "traffic": traffic_record(spec["name"], kind, layer, shape),
-                "kernel": f"gemm ({kind}, layer {layer}), M x N x K = {shape[0]} x {shape[1]} x {shape[2]}",
+                "kernel": f"{kind} call, layer {layer}, {wl.shape_label(shape)}",
                 "avg_launch_us": launch_ms * 1e3, "launches": args.replay, "flops_per_launch": call_flops,
                 "in_step": {"avg_call_us": call_ms * 1e3, "calls": count,
                             "achieved": call_flops / (call_ms * 1e-3) / 1e12},
@@ -533,9 +718,7 @@ def main():
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms"] / args.steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
-        "config": {"workload": spec["name"], "global_batch": spec["batch"], "layers": spec["dims"],
-                   "p": args.p, "patterns": "row-based, sampled per step from K(p), n_max 16",
-                   "dropped": "skip"},
+        "config": dict(wl.config, p=args.p),
         "speedup_vs_p0": speedup,
         "kept_flop_fraction": kept_frac,
         "per_p": {f"{p}": {"ms_per_step": results[p]["ms"] / args.steps,
