@@ -307,7 +307,10 @@ int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, co
  * Layouts: X[T][I][B], W[4H][I+H] (dtype), bias[4H] fp32, h0, c0, hT, cT
  * [H][B], Hs[T][H][B]. h0/c0 NULL = zeros. Dropped rows of Hs, hT, cT are 0.
  * The workspace carries the compact weights and the saved gates from fwd to
- * bwd; it must not be modified in between.
+ * bwd: bwd must get the workspace of the fwd call with the same desc, plan and
+ * inputs, unmodified in between. With any other workspace (of sufficient
+ * size) the gradients are undefined but every write stays inside the output
+ * arrays and the workspace: bwd takes no indices from the workspace.
  * bwd: dHs[T][H][B] (derivative of the loss w.r.t. every h_t), dhT and dcT
  * (extra derivatives of the final state, NULL = 0) -> dX[T][I][B], dW[4H][I+H]
  * fp32, dbias[4H] fp32, dh0 and dc0 [H][B] (each output may be NULL). Entries

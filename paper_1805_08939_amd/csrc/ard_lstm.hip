@@ -124,6 +124,14 @@ __global__ void fill_kernel(float* __restrict__ p, int64_t n, float v) {
   if (e < n) p[e] = v;
 }
 
+// rowmap[4u + g] = g H + idx[u]: the W row of compact gate row r, from the
+// plan (the backward rebuilds it rather than trust the forward's workspace).
+__global__ void lstm_rowmap_kernel(const int32_t* __restrict__ idx, int32_t H, int32_t rows,
+                                   int32_t* __restrict__ rowmap) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < rows) rowmap[r] = static_cast<int32_t>(static_cast<int64_t>(r & 3) * H + unit_row(idx, r >> 2));
+}
+
 // dbias[rowmap[r]] = sum over t, b of dA[t][r][b]; one block per row r.
 __global__ void __launch_bounds__(256) lstm_dbias_kernel(const float* __restrict__ dA,
                                                          const int32_t* __restrict__ rowmap, int32_t T,
@@ -502,7 +510,12 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     ARD_LAUNCH_CHECK();
   }
 
-  const int32_t* rowmap = reinterpret_cast<const int32_t*>(w + L.rowmap);
+  int32_t* rowmap = reinterpret_cast<int32_t*>(w + L.rowmap);
+  if ((dW || dbias) && L.G4 > 0) {
+    hipLaunchKernelGGL(lstm_rowmap_kernel, grid1d(L.G4, 256), dim3(256), 0, sm, idx, static_cast<int32_t>(L.H),
+                       static_cast<int32_t>(L.G4), rowmap);
+    ARD_LAUNCH_CHECK();
+  }
   const bool bv = L.B % 4 == 0;
   if (dW) {
     // dW[rowmap][:I] = sum_t dA[t] X[t]^T ; dW[rowmap][I + S] = sum_t dA[t] Hc[t]^T

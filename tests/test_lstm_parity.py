@@ -96,6 +96,43 @@ def test_full_config_lstm_1024():
     run_lstm(35, 64, 1024, 1024, (per, off), seed=1805 + 3, with_state=False, with_final_grads=False)
 
 
+def test_bwd_on_workspace_of_another_plan():
+    """A backward call whose workspace holds the forward state of another plan
+    (other kept count, so another workspace layout) gives undefined gradients
+    but writes only inside its outputs; the matching forward and backward run
+    afterwards on the same workspace agree exactly with a fresh workspace."""
+    T, B, I, H = 3, 64, 48, 96
+    g = synth.generator(11)
+    X = to_dev(synth.uniform(g, (T, I, B), 0.1))
+    W, b = to_dev(synth.uniform(g, (4 * H, I + H), 0.1)), to_dev(synth.uniform(g, (4 * H,), 0.1))
+    dHs = to_dev(synth.normal(g, (T, H, B)))
+    da = api.lstm_desc(api.ARD_F32, T, B, I, H, row_plan(H, 2, 1))
+    db_ = api.lstm_desc(api.ARD_F32, T, B, I, H, row_plan(H, 3, 0))
+    n = max(api.ard_lstm_workspace_bytes(da), api.ard_lstm_workspace_bytes(db_)) // 4 + 1
+
+    def outs():
+        return [torch.full(sh, 9.0, device=device()) for sh in ((T, H, B), (T, I, B), (4 * H, I + H), (4 * H,))]
+
+    # guard words after each output catch a write past its end
+    guard = torch.full((4 * H * (I + H) + 4096,), 7.0, device=device())
+    dW_g = guard[:4 * H * (I + H)].view(4 * H, I + H)
+    ws = torch.zeros(n, device=device())
+    Hs, dX, _, dbias = outs()
+    api.ard_lstm_fwd(db_, X, W, b, None, None, Hs, None, None, ws)
+    api.ard_lstm_bwd(da, X, dHs, None, None, ws, dX, dW_g, dbias, None, None)
+    torch.cuda.synchronize()
+    assert (guard[4 * H * (I + H):] == 7.0).all()
+    res = []
+    for w in (ws, torch.zeros(n, device=device())):
+        Hs, dX, dW, dbias = outs()
+        api.ard_lstm_fwd(da, X, W, b, None, None, Hs, None, None, w)
+        api.ard_lstm_bwd(da, X, dHs, None, None, w, dX, dW, dbias, None, None)
+        res.append((Hs, dX, dW, dbias))
+    torch.cuda.synchronize()
+    for x, y in zip(*res):
+        assert torch.equal(x, y)
+
+
 def test_deterministic():
     a = run_lstm(4, 64, 64, 96, (2, 1), seed=5)
     b = run_lstm(4, 64, 64, 96, (2, 1), seed=5)
