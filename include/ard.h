@@ -171,6 +171,10 @@ int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard
  *   row_ptr[tiles_n + 1], row_cols[nnz]  kept tile columns per tile row (CSR)
  *   col_ptr[tiles_k + 1], col_rows[nnz]  kept tile rows per tile column (CSC)
  *   flat[nnz]                            kept linear tile indices
+ *   chunks[1 + 2 * groups]               groups of up to 4 kept tiles of one
+ *                                        tile row: chunks[0] = groups, then
+ *                                        per group its tile row and its first
+ *                                        position in row_cols (row order)
  * all ascending. nnz must equal the popcount of the bitmap (host-known, see
  * ard_bitmap_popcount). tile must be 32 or 64, and n, k multiples of it.
  */
@@ -182,6 +186,7 @@ typedef struct {
   int32_t* d_col_ptr;
   int32_t* d_col_rows;
   int32_t* d_flat;
+  int32_t* d_chunks;
 } ard_tile_plan;
 
 size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k);

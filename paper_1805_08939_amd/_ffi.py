@@ -41,7 +41,7 @@ class ard_row_plan(ctypes.Structure):
 class ard_tile_plan(ctypes.Structure):
     _fields_ = [("n", c_i32), ("k", c_i32), ("tile", c_i32), ("tiles_n", c_i32), ("tiles_k", c_i32),
                 ("nnz", c_i32), ("d_bits", c_vp), ("d_row_ptr", c_vp), ("d_row_cols", c_vp),
-                ("d_col_ptr", c_vp), ("d_col_rows", c_vp), ("d_flat", c_vp)]
+                ("d_col_ptr", c_vp), ("d_col_rows", c_vp), ("d_flat", c_vp), ("d_chunks", c_vp)]
 
 
 class ard_fc_desc(ctypes.Structure):

@@ -192,6 +192,24 @@ struct DmaSrc {
     }
   }
 
+  // A k-contiguous operand whose tile row r is row rowof(r) of the view: a
+  // row gather folded into the lane offsets once, so the main loop reads no
+  // index. Every rowof(r) must be a valid row.
+  template <class F>
+  __device__ __forceinline__ void init_rows(int64_t ld, F rowof, int wave) {
+    static_assert(!MC, "row gather of a k-contiguous operand");
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int pos = (wave * PER_WAVE + i) * 64 + lane;
+      const int r = pos / CPR;
+      const int c = (pos % CPR) ^ kc_swz<CPR>(r);
+      off0[i] = static_cast<uint32_t>(static_cast<int64_t>(rowof(r)) * ld * ES);
+      off[i] = off0[i] + static_cast<uint32_t>(c * 16);
+      k[i] = c * EPC;
+    }
+  }
+
   // Loads the slab whose first element is at sbase (uniform), of which the
   // first kv k (k-rows) are valid, into the LDS region at byte address region.
   __device__ __forceinline__ void issue(const char* sbase, int kv, uint32_t region, int wave) const {
@@ -359,6 +377,94 @@ struct SlabLoader {
   }
 };
 
+// Tile order. Workgroup i runs on XCD i % 8, each XCD with its own L2, so
+// XCD x takes a contiguous run of positions t in a grouped order: kGroupRows
+// tile rows at a time, column by column within the group. The workgroups
+// running together on one XCD then share a few A row panels and a few B
+// column panels instead of each bringing its own. Returns the tile row and
+// column of workgroup bid in a grid of nx columns and ny rows.
+__device__ __forceinline__ void grouped_tile(int bid, int nx, int ny, int& row, int& col) {
+  const int nxy = nx * ny;
+  const int xcd = bid % 8, per = nxy / 8, extra = nxy % 8;
+  const int t = xcd * per + (xcd < extra ? xcd : extra) + bid / 8;
+  constexpr int kGroupRows = 8;
+  const int first_row = (t / (kGroupRows * nx)) * kGroupRows;
+  const int rows = ny - first_row < kGroupRows ? ny - first_row : kGroupRows;
+  const int local = t % (kGroupRows * nx);
+  col = local / rows;
+  row = first_row + local % rows;
+}
+
+// The slab pipeline of one workgroup: nslab slabs that the loader issues one
+// after the other into STAGES LDS stages. Each wave waits only for its own
+// loads of the slab it is about to read (vmcnt: exactly (STAGES - 2) * LPW
+// younger loads are allowed), then a barrier makes every wave's loads of that
+// slab visible and certifies that all waves have finished reading the
+// previous slab, whose stage takes the next load. Fragments are
+// double-buffered in registers: the reads of the next k step (the first step
+// of the next slab, behind the barrier) are issued before the MFMAs of the
+// current one, so LDS latency and the barrier overlap MFMA execution.
+// With TAIL, ck is the first k of the first slab within a contraction of
+// length K (slabs wrap to k 0 past K), and a slab with fewer than BK valid k
+// is zeroed past them in LDS before use. Returns with no direct load in flight.
+template <class Cfg, bool AMC, bool BMC, bool TAIL, class Loader>
+__device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, f32x16 (&acc)[Cfg::FM][Cfg::FN],
+                                          int wm, int wn, int kw0, char* smem) {
+  using Frags = StepFrags<Cfg, AMC, BMC>;
+  constexpr int STEPS = Cfg::KW / Frags::KSTEP;
+  static_assert(STEPS % 2 == 0, "a slab holds an even number of k steps");
+  int cs = 0;  // stage of the slab being computed
+  Frags fr[2];
+  char* st = smem;
+  if (nslab > 0) {
+#pragma unroll
+    for (int s = 0; s < Cfg::STAGES - 1; ++s) ld.issue();
+    wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+    lds_barrier();
+    if (TAIL && K - ck < Cfg::BK) {
+      fast_zero_tail<Cfg, Cfg::BM, AMC>(st, K - ck);
+      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, K - ck);
+      lds_barrier();
+    }
+    ld.issue();
+    fr[0].load(st, wm, wn, kw0);
+  }
+  // all slabs but the last one: the last k step crosses into the next slab
+  for (int q = 0; q < nslab - 1; ++q) {
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (s + 1 < STEPS) {
+        fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
+      } else {
+        cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
+        if (TAIL) {
+          ck += Cfg::BK;
+          if (ck >= K) ck = 0;
+        }
+        st = smem + cs * Cfg::STAGE;
+        wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+        lds_barrier();  // slab q + 1 visible; slab q read by no wave any more
+        if (TAIL && K - ck < Cfg::BK) {
+          fast_zero_tail<Cfg, Cfg::BM, AMC>(st, K - ck);
+          fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, K - ck);
+          lds_barrier();
+        }
+        ld.issue();  // into the stage of slab q
+        fr[(s + 1) & 1].load(st, wm, wn, kw0);
+      }
+      fr[s & 1].mma(acc);
+    }
+  }
+  if (nslab > 0) {  // the last slab (a separate copy keeps the loop body's LDS waits exact)
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (s + 1 < STEPS) fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
+      fr[s & 1].mma(acc);
+    }
+  }
+  wait_vm<0>();  // no direct load may still write LDS past this point
+}
+
 // Output of one wave's accumulator tile. Each block row of 32 rows passes
 // through the wave's own LDS region in fp32 (epilogue applied on the way in),
 // and every lane then writes 4 consecutive values of one output row (16 bytes
@@ -465,22 +571,10 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   using T = typename Cfg::T;
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
-  // Tile order. Workgroup i runs on XCD i % 8, each XCD with its own L2, so
-  // XCD x takes a contiguous run of positions t in a grouped order: kGroupRows
-  // tile rows at a time, column by column within the group. The workgroups
-  // running together on one XCD then share a few A row panels and a few B
-  // column panels instead of each bringing its own.
-  const int nx = gridDim.x, ny = gridDim.y;
-  const int nxy = nx * ny;
-  const int bid = blockIdx.y * nx + blockIdx.x;
-  const int xcd = bid % 8, per = nxy / 8, extra = nxy % 8;
-  const int t = xcd * per + (xcd < extra ? xcd : extra) + bid / 8;
-  constexpr int kGroupRows = 8;
-  const int first_row = (t / (kGroupRows * nx)) * kGroupRows;
-  const int rows = ny - first_row < kGroupRows ? ny - first_row : kGroupRows;
-  const int local = t % (kGroupRows * nx);
-  const int n0 = (local / rows) * Cfg::BN;
-  const int m0 = (first_row + local % rows) * Cfg::BM;
+  int tile_row, tile_col;
+  grouped_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x, gridDim.y, tile_row, tile_col);
+  const int n0 = tile_col * Cfg::BN;
+  const int m0 = tile_row * Cfg::BM;
   const int splits = g.splits > 1 ? g.splits : 1;
   const int64_t bz = blockIdx.z / splits;
   const int split = blockIdx.z % splits;
@@ -506,15 +600,7 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int q0 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * split) / splits));
   const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits));
 
-  // Slabs q0 .. q1 - 1 of this split, in STAGES LDS stages. Each wave waits
-  // only for its own loads of the slab it is about to read (vmcnt: exactly
-  // (STAGES - 2) * LPW younger loads are allowed), then a barrier makes every
-  // wave's loads of that slab visible and certifies that all waves have
-  // finished reading the previous slab, whose stage takes the next load.
-  // Fragments are double-buffered in registers: the reads of the next k step
-  // (the first step of the next slab, behind the barrier) are issued before
-  // the MFMAs of the current one, so LDS latency and the barrier overlap MFMA
-  // execution.
+  // slabs q0 .. q1 - 1 of this split
   SlabLoader<Cfg, AMC, BMC> ld;
   ld.wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
@@ -535,59 +621,7 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   ld.left = q1 - q0 - 1;
   ld.na = uniform_ptr(reinterpret_cast<const char*>(abase) + (ib * g.a.kbstride) * ES + ld.ik / Cfg::BK * ld.a_step);
   ld.nb = uniform_ptr(reinterpret_cast<const char*>(bbase) + (ib * g.b.kbstride) * ES + ld.ik / Cfg::BK * ld.b_step);
-  int ck = ld.ik, cs = 0;  // first k and stage of the slab being computed
-
-  using Frags = StepFrags<Cfg, AMC, BMC>;
-  constexpr int STEPS = Cfg::KW / Frags::KSTEP;
-  static_assert(STEPS % 2 == 0, "a slab holds an even number of k steps");
-  const int kw0 = ks * Cfg::KW;
-  Frags fr[2];
-  char* st = smem;
-  if (q0 < q1) {
-#pragma unroll
-    for (int s = 0; s < Cfg::STAGES - 1; ++s) ld.issue();
-    wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
-    lds_barrier();
-    if (g.K - ck < Cfg::BK) {
-      fast_zero_tail<Cfg, Cfg::BM, AMC>(st, g.K - ck);
-      fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, g.K - ck);
-      lds_barrier();
-    }
-    ld.issue();
-    fr[0].load(st, wm, wn, kw0);
-  }
-  // all slabs but the last one: the last k step crosses into the next slab
-  for (int q = q0; q < q1 - 1; ++q) {
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      if (s + 1 < STEPS) {
-        fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
-      } else {
-        cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
-        ck += Cfg::BK;
-        if (ck >= g.K) ck = 0;
-        st = smem + cs * Cfg::STAGE;
-        wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
-        lds_barrier();  // slab q + 1 visible; slab q read by no wave any more
-        if (g.K - ck < Cfg::BK) {
-          fast_zero_tail<Cfg, Cfg::BM, AMC>(st, g.K - ck);
-          fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, g.K - ck);
-          lds_barrier();
-        }
-        ld.issue();  // into the stage of slab q
-        fr[(s + 1) & 1].load(st, wm, wn, kw0);
-      }
-      fr[s & 1].mma(acc);
-    }
-  }
-  if (q0 < q1) {  // the last slab (a separate copy keeps the loop body's LDS waits exact)
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      if (s + 1 < STEPS) fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
-      fr[s & 1].mma(acc);
-    }
-  }
-  wait_vm<0>();  // no direct load may still write LDS past this point
+  run_slabs<Cfg, AMC, BMC, true>(ld, q1 - q0, g.K, ld.ik, acc, wm, wn, ks * Cfg::KW, smem);
   if constexpr (Cfg::KSPLIT == 1) {
     fast_store<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split, smem);
   } else {

@@ -3,95 +3,174 @@
 //
 // Sec. III-B fetches only non-dropped tiles and lets each processing element
 // multiply one tile pair. Here a workgroup owns one tile row (fwd) or one tile
-// column (bwd_data) of W and walks that row's (column's) list of kept tiles,
-// each a dense tile x tile MFMA slab; bwd_weight runs one workgroup per kept
-// tile. Dropped tiles are never read or computed.
+// column (bwd_data) of W and one block of the batch, and walks that row's
+// (column's) list of kept tiles: each kept tile is one slab of the direct-load
+// pipeline of the fast GEMM, its base taken from the list. bwd_weight runs one
+// workgroup per group of up to kTdpChunk kept tiles of one tile row, which
+// share their dY rows; the X rows of the group's tiles are gathered through
+// the lanes' load offsets. Dropped tiles are never read or computed.
 
 #include <hip/hip_runtime.h>
 
 #include "ard_gemm.hpp"
+#include "ard_gemm_fast.hpp"
 #include "ard_internal.hpp"
 
 namespace ard {
 
 constexpr int kScanThreads = 1024;
-constexpr int kMaxTileDim = 8192;  // tiles per side handled by the scan kernel
+constexpr int kMaxTileDim = 8192;    // tiles per side handled by the scan kernel
+constexpr int kLdsBitWords = 4096;   // bitmaps of up to 131072 tiles are scanned from LDS
+constexpr int kTdpChunk = 4;         // kept tiles of one tile row per bwd_weight workgroup
 
-// Exclusive scan of cnt[0..n) (LDS, n >= 1): writes the n+1 prefix sums to out
-// and leaves the exclusive prefix in cnt.
-__device__ void block_exclusive_scan(int32_t* cnt, int n, int32_t* out, int32_t* part) {
+// Exclusive prefix sum of one value per thread over the workgroup (wave scans
+// by shuffles, then the 16 wave totals). Returns the prefix; total receives
+// the sum of all values. wsum: kScanThreads / 64 + 1 entries of LDS.
+__device__ int32_t block_prefix(int32_t v, int32_t* wsum, int32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kWaves = kScanThreads / 64;
+  int32_t inc = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t t = __shfl_up(inc, d, 64);
+    if (lane >= d) inc += t;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t run = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      const int32_t x = wsum[w];
+      wsum[w] = run;
+      run += x;
+    }
+    wsum[kWaves] = run;
+  }
+  __syncthreads();
+  const int32_t out = wsum[wave] + inc - v;
+  total = wsum[kWaves];
+  __syncthreads();  // wsum may be reused right away
+  return out;
+}
+
+// Exclusive scan of cnt[0..n) (LDS, n >= 1), each thread summing a contiguous
+// run of entries: writes the n + 1 prefix sums to out (if not NULL), leaves
+// the exclusive prefix in cnt and returns the total.
+__device__ int32_t block_exclusive_scan(int32_t* cnt, int n, int32_t* out, int32_t* wsum) {
   const int tid = threadIdx.x;
   const int per = (n + kScanThreads - 1) / kScanThreads;
   const int lo = min(n, tid * per), hi = min(n, lo + per);
   int32_t s = 0;
   for (int i = lo; i < hi; ++i) s += cnt[i];
-  part[tid] = s;
-  __syncthreads();
-  if (tid == 0) {  // kScanThreads partial sums
-    int32_t run = 0;
-    for (int i = 0; i < kScanThreads; ++i) {
-      const int32_t v = part[i];
-      part[i] = run;
-      run += v;
-    }
-  }
-  __syncthreads();
-  int32_t run = part[tid];
+  int32_t total;
+  int32_t run = block_prefix(s, wsum, total);
   for (int i = lo; i < hi; ++i) {
     const int32_t c = cnt[i];
-    out[i] = run;
+    if (out) out[i] = run;
     cnt[i] = run;  // the prefix stays in LDS for the list-writing pass
     run += c;
   }
-  if (hi == n && lo < hi) out[n] = run;
+  if (out && tid == 0) out[n] = total;
   __syncthreads();
+  return total;
 }
+
+// Bitmap words, from LDS when the bitmap was staged there.
+struct BitSrc {
+  const uint32_t* g;
+  const uint32_t* s;
+  __device__ __forceinline__ uint32_t word(int64_t w) const { return s ? s[w] : g[w]; }
+  __device__ __forceinline__ bool bit(int64_t t) const { return (word(t >> 5) >> (t & 31)) & 1u; }
+  // the bits of word w that lie in [lo, hi)
+  __device__ __forceinline__ uint32_t masked(int64_t w, int64_t lo, int64_t hi) const {
+    uint32_t x = word(w);
+    const int64_t b0 = w * 32;
+    if (lo > b0) x &= ~0u << (lo - b0);
+    if (hi < b0 + 32) x &= (hi - b0 <= 0) ? 0u : (~0u >> (32 - (hi - b0)));
+    return x;
+  }
+  __device__ __forceinline__ int32_t count(int64_t lo, int64_t hi) const {
+    int32_t c = 0;
+    if (hi <= lo) return 0;
+    for (int64_t w = lo >> 5; w <= (hi - 1) >> 5; ++w) c += __popc(masked(w, lo, hi));
+    return c;
+  }
+};
 
 __device__ __forceinline__ bool tile_bit(const uint32_t* bits, int64_t t) {
   return (bits[t >> 5] >> (t & 31)) & 1u;
 }
 
-// One workgroup: bitmap -> row_ptr/row_cols (CSR), col_ptr/col_rows (CSC), flat.
+// One workgroup: bitmap -> row_ptr/row_cols (CSR), col_ptr/col_rows (CSC),
+// flat, and the bwd_weight groups: chunks[0] = their number, then for group c
+// chunks[1 + 2c] = its tile row and chunks[2 + 2c] = its first position in
+// row_cols; the groups of a row take its kept tiles kTdpChunk at a time, in
+// row order.
 __global__ void __launch_bounds__(kScanThreads)
     plan_tiles_kernel(const uint32_t* __restrict__ bits, int32_t tiles_n, int32_t tiles_k,
                       int32_t* __restrict__ row_ptr, int32_t* __restrict__ row_cols,
                       int32_t* __restrict__ col_ptr, int32_t* __restrict__ col_rows,
-                      int32_t* __restrict__ flat) {
+                      int32_t* __restrict__ flat, int32_t* __restrict__ chunks) {
   __shared__ int32_t cnt[kMaxTileDim];
-  __shared__ int32_t part[kScanThreads];
+  __shared__ int32_t wsum[kScanThreads / 64 + 1];
+  __shared__ uint32_t sbits[kLdsBitWords];
   const int tid = threadIdx.x;
-  // rows
-  for (int r = tid; r < tiles_n; r += kScanThreads) {
-    int32_t c = 0;
-    for (int k = 0; k < tiles_k; ++k) c += tile_bit(bits, static_cast<int64_t>(r) * tiles_k + k);
-    cnt[r] = c;
+  const int64_t nbits = static_cast<int64_t>(tiles_n) * tiles_k;
+  const int64_t nwords = (nbits + 31) / 32;
+  BitSrc src = {bits, nullptr};
+  if (nwords <= kLdsBitWords) {
+    for (int w = tid; w < nwords; w += kScanThreads) sbits[w] = bits[w];
+    src.s = sbits;
+    __syncthreads();
   }
+  // rows
+  for (int r = tid; r < tiles_n; r += kScanThreads)
+    cnt[r] = src.count(static_cast<int64_t>(r) * tiles_k, static_cast<int64_t>(r + 1) * tiles_k);
   __syncthreads();
-  block_exclusive_scan(cnt, tiles_n, row_ptr, part);
+  block_exclusive_scan(cnt, tiles_n, row_ptr, wsum);
   for (int r = tid; r < tiles_n; r += kScanThreads) {
-    int32_t w = cnt[r];
-    for (int k = 0; k < tiles_k; ++k) {
-      const int64_t t = static_cast<int64_t>(r) * tiles_k + k;
-      if (tile_bit(bits, t)) {
-        row_cols[w] = k;
-        flat[w] = static_cast<int32_t>(t);
-        ++w;
+    int32_t pos = cnt[r];
+    const int64_t lo = static_cast<int64_t>(r) * tiles_k, hi = lo + tiles_k;
+    for (int64_t w = lo >> 5; w <= (hi - 1) >> 5; ++w) {
+      uint32_t x = src.masked(w, lo, hi);
+      while (x) {
+        const int64_t t = w * 32 + (__ffs(x) - 1);
+        row_cols[pos] = static_cast<int32_t>(t - lo);
+        flat[pos] = static_cast<int32_t>(t);
+        ++pos;
+        x &= x - 1;
       }
     }
   }
   __syncthreads();
+  // bwd_weight groups: ceil(kept / kTdpChunk) per row
+  for (int r = tid; r < tiles_n; r += kScanThreads) {
+    const int32_t kept = src.count(static_cast<int64_t>(r) * tiles_k, static_cast<int64_t>(r + 1) * tiles_k);
+    cnt[r] = (kept + kTdpChunk - 1) / kTdpChunk;
+  }
+  __syncthreads();
+  const int32_t groups = block_exclusive_scan(cnt, tiles_n, nullptr, wsum);
+  for (int r = tid; r < tiles_n; r += kScanThreads) {
+    const int32_t first = row_ptr[r], kept = row_ptr[r + 1] - first;
+    for (int32_t j = 0; j * kTdpChunk < kept; ++j) {
+      chunks[1 + 2 * (cnt[r] + j)] = r;
+      chunks[2 + 2 * (cnt[r] + j)] = first + j * kTdpChunk;
+    }
+  }
+  if (tid == 0) chunks[0] = groups;
+  __syncthreads();
   // columns
   for (int k = tid; k < tiles_k; k += kScanThreads) {
     int32_t c = 0;
-    for (int r = 0; r < tiles_n; ++r) c += tile_bit(bits, static_cast<int64_t>(r) * tiles_k + k);
+    for (int r = 0; r < tiles_n; ++r) c += src.bit(static_cast<int64_t>(r) * tiles_k + k);
     cnt[k] = c;
   }
   __syncthreads();
-  block_exclusive_scan(cnt, tiles_k, col_ptr, part);
+  block_exclusive_scan(cnt, tiles_k, col_ptr, wsum);
   for (int k = tid; k < tiles_k; k += kScanThreads) {
     int32_t w = cnt[k];
     for (int r = 0; r < tiles_n; ++r)
-      if (tile_bit(bits, static_cast<int64_t>(r) * tiles_k + k)) col_rows[w++] = r;
+      if (src.bit(static_cast<int64_t>(r) * tiles_k + k)) col_rows[w++] = r;
   }
 }
 
@@ -187,6 +266,194 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_kernel(TdpArgs a) {
   store_tile<OutT, Cfg, EPI_FWD>(st, acc, 0, n0, wm, wn, 0, 0);
 }
 
+// Direct loads of one operand pair whose slabs follow a list of kept tiles:
+// slab q is part q % SPT (BK wide in k) of the tile named by entry q / SPT of
+// the workgroup's list, at a0 + entry * a_tile + part * a_part (B alike).
+// Entry e sits in lane e - wbase of the per-lane window win and is read with
+// readlane, so the main loop makes no memory access for the list but one
+// window refill per 64 entries. Past the last slab the last one is loaded
+// again, so every wave issues the same number of loads per slab.
+template <class Cfg, bool AMC, bool BMC, int SPT>
+struct ListLoader {
+  DmaSrc<Cfg, Cfg::BM, AMC> da;
+  DmaSrc<Cfg, Cfg::BN, BMC> db;
+  const char* a0;
+  const char* b0;
+  int64_t a_tile, b_tile, a_part, b_part;
+  const int32_t* list;
+  int n, q, nq, wbase, win, is, wv;
+  uint32_t lds0;
+
+  // The load waits for itself inside the statement: a compiler-visible load
+  // here would make every later readlane wait for all direct loads in flight.
+  // Lanes past the list read its last entry.
+  __device__ __forceinline__ void refill() {
+    const int lane = threadIdx.x & 63;
+    const int32_t* p = list + (wbase + lane < n ? wbase + lane : n - 1);
+    int32_t v;
+    asm volatile("global_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(p) : "memory");
+    win = v;
+  }
+
+  __device__ __forceinline__ void issue() {
+    const int e = q / SPT, part = q % SPT;
+    if (e - wbase >= 64) {
+      wbase += 64;
+      refill();
+    }
+    const int64_t t = __builtin_amdgcn_readlane(win, e - wbase);
+    const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
+    da.issue(a0 + t * a_tile + part * a_part, Cfg::BK, st, wv);
+    db.issue(b0 + t * b_tile + part * b_part, Cfg::BK, st + Cfg::ABYTES, wv);
+    is = is + 1 == Cfg::STAGES ? 0 : is + 1;
+    if (q + 1 < nq) ++q;
+  }
+};
+
+struct TdpFastArgs {
+  const void* act;      // Xt (fwd, bwd_weight) or dYt (bwd_data)
+  const void* act2;     // dYt (bwd_weight)
+  const void* W;
+  void* out;            // Yt, dXt or dW
+  int32_t B, K;         // batch; in_features (row stride of W and dW)
+  int32_t nx, ny;       // fwd / bwd_data grid: batch blocks x tile rows (columns)
+  const int32_t* ptr;   // row_ptr (fwd, bwd_weight) or col_ptr (bwd_data)
+  const int32_t* list;  // row_cols (fwd, bwd_weight) or col_rows (bwd_data)
+  const int32_t* chunks;
+  float scale;
+};
+
+constexpr int kFastTile = 64;
+
+// fwd:       Yt[tn block][n0 ..] = scale * sum over kept tk of row tn: W(tn, tk) Xt[tk block][n0 ..]
+// bwd_data:  dXt[tk block][n0 ..] = scale * sum over kept tn of column tk: W(tn, tk)^T dYt[tn block][n0 ..]
+// A tile row (column) without kept tiles gets zeros.
+template <class Cfg, int PASS, typename OutT>
+__global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
+  constexpr int TT = kFastTile, ES = Cfg::ES, SPT = TT / Cfg::BK;
+  constexpr bool AMC = PASS == TDP_BWD_DATA;
+  static_assert(Cfg::BM == TT && TT % Cfg::BK == 0 && Cfg::KSPLIT == 1, "one tile row per workgroup");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  int own, col;
+  grouped_tile(blockIdx.x, a.nx, a.ny, own, col);
+  const int n0 = col * Cfg::BN;
+  const int p0 = __builtin_amdgcn_readfirstlane(a.ptr[own]);
+  const int p1 = __builtin_amdgcn_readfirstlane(a.ptr[own + 1]);
+
+  f32x16 acc[Cfg::FM][Cfg::FN];
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  ListLoader<Cfg, AMC, true, SPT> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(wave);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  ld.list = a.list + p0;
+  ld.n = p1 - p0;
+  ld.q = 0;
+  ld.nq = ld.n * SPT;
+  ld.wbase = 0;
+  ld.is = 0;
+  const char* W = static_cast<const char*>(a.W);
+  const int64_t K = a.K, B = a.B;
+  if constexpr (PASS == TDP_FWD) {
+    ld.a0 = W + own * TT * K * ES;  // W(tn, tk) at column tk * TT of the tile row
+    ld.a_tile = TT * ES;
+    ld.a_part = Cfg::BK * ES;
+  } else {
+    ld.a0 = W + own * TT * ES;      // W(tn, tk)^T: k-rows tn * TT .. of the tile column
+    ld.a_tile = TT * K * ES;
+    ld.a_part = Cfg::BK * K * ES;
+  }
+  ld.b0 = static_cast<const char*>(a.act);
+  ld.b_tile = TT * B * ES;
+  ld.b_part = Cfg::BK * B * ES;
+  if (ld.nq > 0) {
+    ld.refill();
+    ld.da.init(K, 0, TT, ld.wv);
+    ld.db.init(B, n0, a.B, ld.wv);
+  }
+  (void)lane;
+  run_slabs<Cfg, AMC, true, false>(ld, ld.nq, 0, 0, acc, wm, wn, 0, smem);
+
+  GemmArgs g = {};
+  g.M = TT;
+  g.N = a.B;
+  g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(own) * TT * B;
+  g.c.ld = B;
+  g.c.scale = a.scale;
+  fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, n0, wm, wn, 0, 0, smem);
+}
+
+// bwd_weight: dW(tn, tk) = scale * dYt[tn block] Xt[tk block]^T (contraction
+// over the batch) for a group of up to kTdpChunk kept tiles of tile row tn;
+// wave column wn computes the group's tile wn.
+template <class Cfg, typename OutT>
+__global__ void __launch_bounds__(Cfg::NT) tdp_fast_dw_kernel(TdpFastArgs a) {
+  constexpr int TT = kFastTile, ES = Cfg::ES;
+  static_assert(Cfg::BM == TT && Cfg::TN == TT && Cfg::BN == TT * kTdpChunk && Cfg::KSPLIT == 1,
+                "one kept tile per wave column");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  int unused, c;
+  grouped_tile(blockIdx.x, gridDim.x, 1, unused, c);
+  if (c >= a.chunks[0]) return;  // the grid is an upper bound on the number of groups
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  const int tn = __builtin_amdgcn_readfirstlane(a.chunks[1 + 2 * c]);
+  const int p = __builtin_amdgcn_readfirstlane(a.chunks[2 + 2 * c]);
+  const int end = __builtin_amdgcn_readfirstlane(a.ptr[tn + 1]);
+  const int cnt = end - p < kTdpChunk ? end - p : kTdpChunk;
+  const int32_t* cols = a.list + p;
+
+  f32x16 acc[Cfg::FM][Cfg::FN];
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int64_t B = a.B, K = a.K;
+  SlabLoader<Cfg, false, false> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(wave);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  ld.da.init(B, 0, TT, ld.wv);
+  // row r of the B tile: row r % TT of X block cols[r / TT] (the last kept one
+  // for the unused wave columns of a short group, whose results are dropped)
+  ld.db.init_rows(B, [&](int r) {
+    const int j = r / TT < cnt ? r / TT : cnt - 1;
+    return cols[j] * TT + r % TT;
+  }, ld.wv);
+  const int nslab = (a.B + Cfg::BK - 1) / Cfg::BK;
+  ld.K = a.B;
+  ld.ik = 0;
+  ld.is = 0;
+  ld.left = nslab - 1;
+  ld.a_step = Cfg::BK * ES;
+  ld.b_step = Cfg::BK * ES;
+  ld.a_wrap = 0;
+  ld.b_wrap = 0;
+  ld.na = uniform_ptr(static_cast<const char*>(a.act2) + static_cast<int64_t>(tn) * TT * B * ES);
+  ld.nb = uniform_ptr(static_cast<const char*>(a.act));
+  run_slabs<Cfg, false, false, true>(ld, nslab, a.B, 0, acc, wm, wn, 0, smem);
+
+  // wave column wn writes tile cols[wn]: its columns wn * TT .. land at column
+  // cols[wn] * TT of dW (cols ascend, so cols[wn] >= wn)
+  const int j = wn < cnt ? wn : cnt - 1;
+  GemmArgs g = {};
+  g.M = TT;
+  g.N = cnt * TT;
+  g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(tn) * TT * K + static_cast<int64_t>(cols[j] - j) * TT;
+  g.c.ld = K;
+  g.c.scale = a.scale;
+  fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, 0, wm, wn, 0, 0, smem);
+}
+
 // ZERO mode: clears every dropped tile of dW.
 __global__ void zero_dropped_tiles_kernel(const uint32_t* __restrict__ bits, float* __restrict__ dW,
                                           int32_t K, int32_t tile, int32_t tiles_k) {
@@ -242,6 +509,65 @@ hipError_t run_tdp(int pass, const TdpArgs& a, int owners, int nnz, hipStream_t 
   return launch_tdp<T, T, typename C::Rows32, TDP_BWD_DATA>(a, grid, vec, s);
 }
 
+// Direct-load configurations of the fast path (64 x 64 tiles): one tile row
+// (column) by 128 batch columns for fwd / bwd_data, one tile row by a group of
+// kTdpChunk kept tiles for bwd_weight.
+template <typename T>
+struct TdpFastCfgs;
+template <>
+struct TdpFastCfgs<bf16> {
+  using Rows = FastCfg<bf16, 64, 128, 64, 4, 2, 2, 1>;  // 96 KB LDS
+  using Group = FastCfg<bf16, 64, 256, 64, 3, 1, 4, 1>; // 120 KB
+};
+template <>
+struct TdpFastCfgs<float> {
+  using Rows = FastCfg<float, 64, 128, 32, 4, 2, 2, 1>; // 96 KB
+  using Group = FastCfg<float, 64, 256, 32, 3, 1, 4, 1>;// 120 KB
+};
+
+template <class Cfg, class Kern>
+hipError_t launch_with_lds(Kern kern, dim3 grid, const TdpFastArgs& a, hipStream_t s) {
+  static bool attr_set = false;  // per instantiation: allow more than 64 KB of dynamic LDS
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, grid, dim3(Cfg::NT), Cfg::LDS, s, a);
+  return hipGetLastError();
+}
+
+// The fast path takes 64 x 64 tiles, batch rows of whole 16-byte chunks, and
+// operands whose chunk offsets from a slab's first element stay below 2^31.
+template <typename T>
+bool tdp_fast_ok(const TdpArgs& a) {
+  const int64_t es = sizeof(T);
+  return a.tile == kFastTile && (static_cast<int64_t>(a.B) * es) % 16 == 0 &&
+         static_cast<int64_t>(a.K) * a.B * es < (int64_t{1} << 31) &&
+         static_cast<int64_t>(a.N) * a.B * es < (int64_t{1} << 31) &&
+         static_cast<int64_t>(kFastTile + 1) * a.K * es < (int64_t{1} << 31);
+}
+
+template <typename T>
+hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int owners, int nnz, hipStream_t s) {
+  using C = TdpFastCfgs<T>;
+  TdpFastArgs f = {a.act, a.act2, a.W, a.out, a.B, a.K, 0, 0, a.ptr, a.list, chunks, a.scale};
+  if (pass == TDP_BWD_WEIGHT) {
+    if (nnz == 0) return hipSuccess;
+    // groups: sum over rows of ceil(kept / kTdpChunk) <= (nnz + (kTdpChunk - 1) * rows with a kept tile) / kTdpChunk
+    const int64_t rows = owners < nnz ? owners : nnz;
+    const int64_t bound = (nnz + (kTdpChunk - 1) * rows) / kTdpChunk;
+    return launch_with_lds<typename C::Group>(tdp_fast_dw_kernel<typename C::Group, float>,
+                                             dim3(static_cast<unsigned>(bound)), f, s);
+  }
+  f.nx = (a.B + C::Rows::BN - 1) / C::Rows::BN;
+  f.ny = owners;
+  const dim3 grid(static_cast<unsigned>(f.nx * f.ny));
+  if (pass == TDP_FWD) return launch_with_lds<typename C::Rows>(tdp_fast_kernel<typename C::Rows, TDP_FWD, T>, grid, f, s);
+  return launch_with_lds<typename C::Rows>(tdp_fast_kernel<typename C::Rows, TDP_BWD_DATA, T>, grid, f, s);
+}
+
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 int check_tile_call(const ard_tile_desc* d, const ard_tile_plan* p) {
@@ -260,7 +586,8 @@ int check_tile_call(const ard_tile_desc* d, const ard_tile_plan* p) {
   if (p->tiles_n != p->n / p->tile || p->tiles_k != p->k / p->tile || p->n % p->tile || p->k % p->tile)
     return fail(ARD_ERR_INVALID_ARG, "plan tile grid is inconsistent");
   if (p->nnz < 0 || p->nnz > p->tiles_n * p->tiles_k) return fail(ARD_ERR_INVALID_ARG, "plan nnz out of range");
-  if (!p->d_bits || !p->d_row_ptr || !p->d_row_cols || !p->d_col_ptr || !p->d_col_rows || !p->d_flat)
+  if (!p->d_bits || !p->d_row_ptr || !p->d_row_cols || !p->d_col_ptr || !p->d_col_rows || !p->d_flat ||
+      !p->d_chunks)
     return fail(ARD_ERR_INVALID_ARG, "plan has NULL lists");
   return ARD_OK;
 }
@@ -281,7 +608,8 @@ extern "C" {
 size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k) {
   if (tiles_n < 1 || tiles_k < 1) return 0;
   const size_t nnz = static_cast<size_t>(tiles_n) * tiles_k;
-  return align256(4 * (tiles_n + 1)) + align256(4 * (tiles_k + 1)) + 3 * align256(4 * nnz);
+  return align256(4 * (tiles_n + 1)) + align256(4 * (tiles_k + 1)) + 3 * align256(4 * nnz) +
+         align256(4 * (1 + 2 * nnz));
 }
 
 int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, int32_t nnz, void* d_ws,
@@ -319,9 +647,11 @@ int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, i
   plan->d_col_rows = reinterpret_cast<int32_t*>(w);
   w += align256(4 * full);
   plan->d_flat = reinterpret_cast<int32_t*>(w);
+  w += align256(4 * full);
+  plan->d_chunks = reinterpret_cast<int32_t*>(w);
   hipLaunchKernelGGL(plan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, static_cast<hipStream_t>(stream),
                      d_bits, tn, tk, plan->d_row_ptr, plan->d_row_cols, plan->d_col_ptr,
-                     plan->d_col_rows, plan->d_flat);
+                     plan->d_col_rows, plan->d_flat, plan->d_chunks);
   ARD_LAUNCH_CHECK();
   return ARD_OK;
 }
@@ -337,9 +667,15 @@ int ard_tile_fwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const voi
                plan->d_row_ptr, plan->d_row_cols, desc->scale};
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
-    ARD_HIP_CHECK(run_tdp<bf16>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
+    if (tdp_fast_ok<bf16>(a))
+      ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_FWD, a, plan->d_chunks, plan->tiles_n, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
   } else {
-    ARD_HIP_CHECK(run_tdp<float>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
+    if (tdp_fast_ok<float>(a))
+      ARD_HIP_CHECK(run_tdp_fast<float>(TDP_FWD, a, plan->d_chunks, plan->tiles_n, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<float>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
   }
   return ARD_OK;
 }
@@ -355,9 +691,15 @@ int ard_tile_bwd_data(const ard_tile_desc* desc, const ard_tile_plan* plan, cons
                plan->d_col_ptr, plan->d_col_rows, desc->scale};
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
-    ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
+    if (tdp_fast_ok<bf16>(a))
+      ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_BWD_DATA, a, plan->d_chunks, plan->tiles_k, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
   } else {
-    ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
+    if (tdp_fast_ok<float>(a))
+      ARD_HIP_CHECK(run_tdp_fast<float>(TDP_BWD_DATA, a, plan->d_chunks, plan->tiles_k, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
   }
   return ARD_OK;
 }
@@ -371,11 +713,20 @@ int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, co
     return st;
   TdpArgs a = {Xt, dYt, nullptr, dW, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
                nullptr, plan->d_flat, desc->scale};
+  TdpArgs f = a;  // the fast path walks the groups of row_cols
+  f.ptr = plan->d_row_ptr;
+  f.list = plan->d_row_cols;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
-    ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
+    if (tdp_fast_ok<bf16>(a))
+      ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_BWD_WEIGHT, f, plan->d_chunks, plan->tiles_n, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
   } else {
-    ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
+    if (tdp_fast_ok<float>(a))
+      ARD_HIP_CHECK(run_tdp_fast<float>(TDP_BWD_WEIGHT, f, plan->d_chunks, plan->tiles_n, plan->nnz, s));
+    else
+      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
   }
   if (desc->dropped == ARD_DROPPED_ZERO && plan->nnz < plan->tiles_n * plan->tiles_k) {
     hipLaunchKernelGGL(zero_dropped_tiles_kernel, dim3(plan->tiles_k, plan->tiles_n), dim3(256), 0, s,

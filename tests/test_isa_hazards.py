@@ -69,12 +69,13 @@ def hazards(lines):
 
 
 @pytest.mark.skipif(not all(os.path.exists(t) for t in TOOLS), reason="ROCm LLVM tools not found")
-def test_direct_load_wait_states(tmp_path):
-    obj = os.path.join(BUILD, "ard_fc.hip.o")
+@pytest.mark.parametrize("src", ["ard_fc.hip", "ard_tile.hip"])
+def test_direct_load_wait_states(tmp_path, src):
+    obj = os.path.join(BUILD, src + ".o")
     if not os.path.exists(obj):
         pytest.skip("library objects not built")
     n, bad = hazards(_disassemble(obj, tmp_path))
-    assert n > 0, "no direct loads found in the FC kernels"
+    assert n > 0, f"no direct loads found in the kernels of {src}"
     assert not bad, "\n".join(bad[:10])
 
 

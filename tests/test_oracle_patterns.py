@@ -91,6 +91,30 @@ def test_tile_lists_reconstruct_the_grid(seed):
     assert (g1 == grid).all() and (g2 == grid).all() and (g3 == grid).all()
     assert L["flat"] == sorted(L["flat"])
     assert patterns.bitmap_popcount(words, tn * tk) == int(grid.sum()) == len(L["flat"])
+    # the weight-gradient groups cover every kept tile once, each within one
+    # tile row, at most 4 tiles, in row order, only the last of a row short
+    ch = L["chunks"]
+    groups = [(ch[1 + 2 * i], ch[2 + 2 * i]) for i in range(ch[0])]
+    assert len(ch) == 1 + 2 * ch[0]
+    g4 = np.zeros_like(grid)
+    seen = []
+    for i, (r, first) in enumerate(groups):
+        end = min(first + 4, L["row_ptr"][r + 1])
+        assert L["row_ptr"][r] <= first < end
+        if end - first < 4:
+            assert end == L["row_ptr"][r + 1]
+        for pos in range(first, end):
+            assert not g4[r, L["row_cols"][pos]]
+            g4[r, L["row_cols"][pos]] = True
+        seen.append((r, first))
+    assert seen == sorted(seen) and (g4 == grid).all()
+
+
+def test_row_groups_by_hand():
+    # rows with 0, 5, 4 and 1 kept tiles
+    assert patterns.row_groups([0, 0, 5, 9, 10], 4) == [4, 1, 0, 1, 4, 2, 5, 3, 9]
+    assert patterns.row_groups([0, 0, 0], 4) == [0]
+    assert patterns.row_groups([0, 3], 1) == [3, 0, 0, 0, 1, 0, 2]
 
 
 def test_tile_mask_expansion():

@@ -31,6 +31,7 @@ def tile_plan(n, k, tile, words, check=True):
         assert arr(plan.d_row_cols, nnz) == L["row_cols"]
         assert arr(plan.d_col_rows, nnz) == L["col_rows"]
         assert arr(plan.d_flat, nnz) == L["flat"]
+        assert arr(plan.d_chunks, len(L["chunks"])) == L["chunks"]
     return plan
 
 
@@ -93,6 +94,15 @@ def test_ragged_batch_and_skip(dtype):
 def test_dropped_tiles_never_read(dtype):
     words = oprng.tile_bitmap_bernoulli(4, 4, 0.5, 8, 0, 0)
     run_tile(dtype, 64, 256, 256, 64, words, poison=True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lists_longer_than_64_tiles(dtype):
+    """Tile rows and columns with more than 64 kept tiles (the workgroup's list
+    window is refilled) and short last weight-gradient groups."""
+    tn, tk = 70, 66
+    for words in (oprng.tile_bitmap_tdp(tn, tk, 1, 0), oprng.tile_bitmap_bernoulli(tn, tk, 0.02, 5, 0, 0)):
+        run_tile(dtype, 16, tn * 64, tk * 64, 64, words, scale=0.5)
 
 
 def test_full_config_bf16_4096():
