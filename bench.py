@@ -234,10 +234,11 @@ class Mlp:
 
 
 class TileLayer:
-    """One layer under a tile-based pattern: each step samples a Bernoulli(1 - p)
-    keep bitmap over the 64 x 64 tiles of W[N][K], uploads it (its own pinned
-    slot per step), builds the kept-tile lists on the device and runs fwd,
-    bwd_data and bwd_weight, reading and writing only kept tiles."""
+    """One layer under a tile-based pattern: each step draws a Bernoulli(1 - p)
+    keep bitmap over the 64 x 64 tiles of W[N][K] on the device together with
+    the kept-tile lists (one kernel; the same draws as the host sampler, which
+    the FLOP count and the oracle use), then runs fwd, bwd_data and bwd_weight,
+    reading and writing only kept tiles."""
 
     def __init__(self, name, n, k, batch, tile, dtype, seed, w_std):
         import torch
@@ -260,7 +261,6 @@ class TileLayer:
         self.bits_dev = torch.empty(self.words, dtype=torch.int32, device=dev)
         self.plan_ws = torch.empty(max(api.ard_tile_plan_workspace_bytes(self.tn, self.tk), 16) // 4,
                                    dtype=torch.int32, device=dev)
-        self.pinned = {}
         self.desc = api.tile_desc(api.ARD_BF16 if dtype == "bf16" else api.ARD_F32, batch, k, n, 1.0,
                                   api.ARD_DROPPED_SKIP)
         self.stream = torch.cuda.current_stream().cuda_stream
@@ -276,11 +276,15 @@ class TileLayer:
         return bits, self.api.ard_bitmap_popcount(bits, self.tn * self.tk)
 
     def kept_flops(self, pats):
+        if isinstance(pats, int):  # a step number: its pattern from the host sampler
+            pats = self.patterns(pats)
         f = 2.0 * self.B * self.tile * self.tile * pats[1]
         per = {key: f for key in self.order}
         return sum(per.values()), per
 
     def gemm_shape(self, pats, kind, l):
+        if isinstance(pats, int):
+            pats = self.patterns(pats)
         return (self.N, self.B, self.K, pats[1])
 
     @staticmethod
@@ -288,20 +292,14 @@ class TileLayer:
         return "N x B x K = %d x %d x %d, %d kept 64 x 64 tiles" % tuple(shape)
 
     def prepare(self, it):
-        torch, api = self.torch, self.api
-        bits, nnz = self.patterns(it)
-        slot = self.pinned.get(it)
-        if slot is None:  # one pinned buffer per step: the upload below never races the host
-            slot = torch.empty(self.words, dtype=torch.int32, pin_memory=True)
-            self.pinned[it] = slot
-        slot.numpy()[:] = bits.view("int32")
-        self.bits_dev.copy_(slot, non_blocking=True)
-        plan = api.ard_plan_tiles(self.N, self.K, self.tile, self.bits_dev, nnz, self.plan_ws, self.stream)
+        api = self.api
+        plan = api.ard_plan_tiles_bernoulli(self.N, self.K, self.tile, self.p, PATTERN_SEED, 0, it, self.bits_dev,
+                                            self.plan_ws, self.stream)
         d, st = self.desc, self.stream
         calls = {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
                  ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
                  ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
-        return (bits, nnz), calls
+        return it, calls
 
     step = Mlp.step
     replay = Mlp.replay
@@ -435,16 +433,16 @@ def time_steps(wl, steps, warmup, it0, timed_call=None):
     end = torch.cuda.Event(enable_timing=True)
     start.record()
     shapes = []
-    for i in range(steps):
-        pats = wl.step(it0 + warmup + i, timed_call, ev[i] if ev else None)
+    all_pats = [wl.step(it0 + warmup + i, timed_call, ev[i] if ev else None) for i in range(steps)]
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for i, pats in enumerate(all_pats):  # FLOP accounting off the timed path
         f, per = wl.kept_flops(pats)
         total_flops += f
         if timed_call is not None:
             call_flops += per[timed_call]
             shapes.append((wl.gemm_shape(pats, *timed_call), per[timed_call], it0 + warmup + i))
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     gpu_ms = start.elapsed_time(end)
     if ev:
         durs = [a.elapsed_time(b) for a, b in ev]

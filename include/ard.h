@@ -171,15 +171,20 @@ int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard
  *   row_ptr[tiles_n + 1], row_cols[nnz]  kept tile columns per tile row (CSR)
  *   col_ptr[tiles_k + 1], col_rows[nnz]  kept tile rows per tile column (CSC)
  *   flat[nnz]                            kept linear tile indices
- *   chunks[1 + 2 * groups]               groups of up to 4 kept tiles of one
- *                                        tile row: chunks[0] = groups, then
- *                                        per group its tile row and its first
- *                                        position in row_cols (row order)
+ *   chunks[4 + 8 * groups]               groups of up to 4 kept tiles of one
+ *                                        tile row, in row order: chunks[0] =
+ *                                        groups, chunks[1..3] = 0, then per
+ *                                        group 8 ints: tile row, first position
+ *                                        in row_cols, tile count n, 0, the n
+ *                                        tile columns and the last of them
+ *                                        repeated up to 4 entries
  * all ascending. nnz must equal the popcount of the bitmap (host-known, see
- * ard_bitmap_popcount). tile must be 32 or 64, and n, k multiples of it.
+ * ard_bitmap_popcount). tile must be 32 or 64, n and k multiples of it, and
+ * the tile grid at most 4096 tiles per side.
  */
 typedef struct {
-  int32_t n, k, tile, tiles_n, tiles_k, nnz;
+  int32_t n, k, tile, tiles_n, tiles_k;
+  int32_t nnz;  /* kept tiles, or -1 when known on the device only */
   const uint32_t* d_bits;
   int32_t* d_row_ptr;
   int32_t* d_row_cols;
@@ -192,6 +197,22 @@ typedef struct {
 size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k);
 int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, int32_t nnz,
                    void* d_ws, size_t ws_bytes, ard_tile_plan* plan, void* stream);
+
+/*
+ * The same plan with the bitmap sampled on the device, in the plan kernel:
+ * the bits of ard_tile_bitmap_bernoulli(tiles_n, tiles_k, p, seed, stream_id,
+ * iter) exactly (each tile's draw of the counter-based stream computed on its
+ * own), written to d_bits (device, ceil(tiles_n * tiles_k / 32) words,
+ * caller-owned, read by the layer calls in ZERO mode). For patterns drawn
+ * every step with no host sampling or upload. The kept count then exists on
+ * the device only: plan->nnz = -1, row_ptr[tiles_n] holds it, and the layer
+ * calls launch for the largest possible count (surplus workgroups exit at
+ * once). Errors as for ard_plan_tiles, and for p outside [0, 1], stream_id
+ * >= 2^24 or iter >= 2^40.
+ */
+int ard_plan_tiles_bernoulli(int32_t n, int32_t k, int32_t tile, double p, uint64_t seed,
+                             uint32_t stream_id, uint64_t iter, uint32_t* d_bits, void* d_ws,
+                             size_t ws_bytes, ard_tile_plan* plan, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Fully connected layer under row patterns (device).                       */

@@ -80,6 +80,9 @@ SIGNATURES = {
     "ard_tile_plan_workspace_bytes": (c_size, [c_i32, c_i32]),
     "ard_plan_tiles": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, c_i32, c_vp, c_size,
                                       ctypes.POINTER(ard_tile_plan), c_vp]),
+    "ard_plan_tiles_bernoulli": (ctypes.c_int, [c_i32, c_i32, c_i32, ctypes.c_double, ctypes.c_uint64,
+                                                c_u32, ctypes.c_uint64, c_vp, c_vp, c_size,
+                                                ctypes.POINTER(ard_tile_plan), c_vp]),
     "ard_fc_compact_ld": (c_i32, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_compact_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_compact_weights": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp]),

@@ -152,6 +152,17 @@ def ard_plan_tiles(n, k, tile, d_bits, nnz, ws, stream=None):
     return plan
 
 
+def ard_plan_tiles_bernoulli(n, k, tile, p, seed, stream_id, iteration, d_bits, ws, stream=None):
+    """Samples the Bernoulli tile bitmap into d_bits on the device and plans from
+    it (plan.nnz = -1: the kept count stays on the device)."""
+    plan = ard_tile_plan()
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(_ffi.lib().ard_plan_tiles_bernoulli(n, k, tile, float(p), seed, stream_id, iteration, _ptr(d_bits),
+                                               _ptr(ws), nbytes, ctypes.byref(plan), _stream(stream)))
+    plan._keep = (d_bits, ws)
+    return plan
+
+
 # --------------------------------------------------------------------------- FC layer
 
 def fc_desc(dtype, batch, in_features, out_features, in_plan=None, out_plan=None, scale=1.0,

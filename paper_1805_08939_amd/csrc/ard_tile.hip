@@ -19,9 +19,10 @@
 namespace ard {
 
 constexpr int kScanThreads = 1024;
-constexpr int kMaxTileDim = 8192;    // tiles per side handled by the scan kernel
-constexpr int kLdsBitWords = 4096;   // bitmaps of up to 131072 tiles are scanned from LDS
+constexpr int kMaxTileDim = 4096;    // tiles per side handled by the scan kernel
+constexpr int kLdsBitWords = 2048;   // bitmaps of up to 65536 tiles are scanned from LDS
 constexpr int kTdpChunk = 4;         // kept tiles of one tile row per bwd_weight workgroup
+constexpr int kTdpRec = 4 + kTdpChunk;  // ints per bwd_weight group record
 
 // Exclusive prefix sum of one value per thread over the workgroup (wave scans
 // by shuffles, then the 16 wave totals). Returns the prefix; total receives
@@ -37,14 +38,16 @@ __device__ int32_t block_prefix(int32_t v, int32_t* wsum, int32_t& total) {
   }
   if (lane == 63) wsum[wave] = inc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t run = 0;
-    for (int w = 0; w < kWaves; ++w) {
-      const int32_t x = wsum[w];
-      wsum[w] = run;
-      run += x;
+  if (wave == 0) {  // the wave totals, scanned by the first kWaves lanes
+    const int32_t x = lane < kWaves ? wsum[lane] : 0;
+    int32_t y = x;
+#pragma unroll
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const int32_t t = __shfl_up(y, d, 64);
+      if (lane >= d) y += t;
     }
-    wsum[kWaves] = run;
+    if (lane < kWaves) wsum[lane] = y - x;
+    if (lane == kWaves - 1) wsum[kWaves] = y;
   }
   __syncthreads();
   const int32_t out = wsum[wave] + inc - v;
@@ -101,63 +104,164 @@ __device__ __forceinline__ bool tile_bit(const uint32_t* bits, int64_t t) {
   return (bits[t >> 5] >> (t & 31)) & 1u;
 }
 
+// Draw t (0-based) of the SplitMix64 stream with start state s0 (Steele, Lea
+// & Flood, OOPSLA 2014): the Weyl state after t + 1 golden-ratio steps, put
+// through the 64-bit finaliser. The host sampler walks the same sequence one
+// draw after the other; here every tile computes its own draw.
+__device__ __forceinline__ uint64_t splitmix_draw(uint64_t s0, uint64_t t) {
+  uint64_t z = s0 + (t + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Keep-bitmap sampling of the plan kernel: tile t is kept iff its draw as a
+// 53-bit uniform in [0, 1) is >= p.
+struct TileSampler {
+  int enabled;
+  double p;
+  uint64_t s0;
+};
+
 // One workgroup: bitmap -> row_ptr/row_cols (CSR), col_ptr/col_rows (CSC),
-// flat, and the bwd_weight groups: chunks[0] = their number, then for group c
-// chunks[1 + 2c] = its tile row and chunks[2 + 2c] = its first position in
-// row_cols; the groups of a row take its kept tiles kTdpChunk at a time, in
-// row order.
+// flat, and the bwd_weight groups: the groups of a row take its kept tiles
+// kTdpChunk at a time, in row order. chunks[0] = their number (chunks[1..3]
+// = 0); group c is the record at chunks + 4 + c * kTdpRec: tile row, first
+// position in row_cols, tile count n, 0, then the n tile columns followed by
+// the last one repeated up to kTdpChunk entries.
+// Small bitmaps are staged in LDS together with their transpose (built with
+// LDS atomics while the rows are listed), so both list passes walk whole words
+// (popcount, find-first-set); larger ones are read bit by bit from memory.
 __global__ void __launch_bounds__(kScanThreads)
-    plan_tiles_kernel(const uint32_t* __restrict__ bits, int32_t tiles_n, int32_t tiles_k,
+    plan_tiles_kernel(uint32_t* bits, TileSampler smp, int32_t tiles_n, int32_t tiles_k,
                       int32_t* __restrict__ row_ptr, int32_t* __restrict__ row_cols,
                       int32_t* __restrict__ col_ptr, int32_t* __restrict__ col_rows,
                       int32_t* __restrict__ flat, int32_t* __restrict__ chunks) {
-  __shared__ int32_t cnt[kMaxTileDim];
+  __shared__ int32_t cnt[kMaxTileDim];   // per row, then per column: count, then exclusive prefix
+  __shared__ int32_t gpre[kMaxTileDim];  // per row: groups, then their exclusive prefix
   __shared__ int32_t wsum[kScanThreads / 64 + 1];
   __shared__ uint32_t sbits[kLdsBitWords];
+  __shared__ uint32_t tbits[kLdsBitWords];  // column c, rows 32w .. 32w + 31 at word c * wpc + w
+  __shared__ int32_t wpre[kLdsBitWords];    // set bits before each word of sbits, then of tbits
   const int tid = threadIdx.x;
   const int64_t nbits = static_cast<int64_t>(tiles_n) * tiles_k;
   const int64_t nwords = (nbits + 31) / 32;
+  const int wpc = (tiles_n + 31) / 32;
+  const bool in_lds = nwords <= kLdsBitWords && static_cast<int64_t>(tiles_k) * wpc <= kLdsBitWords;
+  if (smp.enabled) {  // sample the bitmap first (written out, and kept in LDS when it fits)
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int64_t base = 0; base < nbits; base += kScanThreads) {
+      const int64_t t = base + tid;
+      bool keep = false;
+      if (t < nbits)
+        keep = static_cast<double>(splitmix_draw(smp.s0, static_cast<uint64_t>(t)) >> 11) * 0x1.0p-53 >= smp.p;
+      const uint64_t m = __ballot(keep);  // the wave's 64 consecutive tiles, two words
+      const int64_t w0 = (base + 64 * wave) / 32;
+      if (lane < 2 && w0 + lane < nwords) {
+        const uint32_t x = static_cast<uint32_t>(m >> (32 * lane));
+        bits[w0 + lane] = x;
+        if (in_lds) sbits[w0 + lane] = x;
+      }
+    }
+    __syncthreads();
+  }
   BitSrc src = {bits, nullptr};
-  if (nwords <= kLdsBitWords) {
-    for (int w = tid; w < nwords; w += kScanThreads) sbits[w] = bits[w];
+  if (in_lds) {
+    if (!smp.enabled)
+      for (int w = tid; w < nwords; w += kScanThreads) sbits[w] = bits[w];
+    for (int w = tid; w < tiles_k * wpc; w += kScanThreads) tbits[w] = 0u;
     src.s = sbits;
     __syncthreads();
   }
-  // rows
-  for (int r = tid; r < tiles_n; r += kScanThreads)
-    cnt[r] = src.count(static_cast<int64_t>(r) * tiles_k, static_cast<int64_t>(r + 1) * tiles_k);
-  __syncthreads();
-  block_exclusive_scan(cnt, tiles_n, row_ptr, wsum);
+  // rows: counts, groups, prefixes
   for (int r = tid; r < tiles_n; r += kScanThreads) {
-    int32_t pos = cnt[r];
+    const int32_t kept = src.count(static_cast<int64_t>(r) * tiles_k, static_cast<int64_t>(r + 1) * tiles_k);
+    cnt[r] = kept;
+    gpre[r] = (kept + kTdpChunk - 1) / kTdpChunk;
+  }
+  __syncthreads();
+  const int32_t total = block_exclusive_scan(cnt, tiles_n, row_ptr, wsum);
+  const int32_t groups = block_exclusive_scan(gpre, tiles_n, nullptr, wsum);
+  if (tid < 4) chunks[tid] = tid == 0 ? groups : 0;
+  if (in_lds) {
+    // rows, one thread per tile: kept tile t of word w lands at position
+    // (set bits before word w) + (set bits of word w below t)
+    for (int w = tid; w < nwords; w += kScanThreads) wpre[w] = __popc(sbits[w]);
+    __syncthreads();
+    block_exclusive_scan(wpre, static_cast<int>(nwords), nullptr, wsum);
+    for (int t = tid; t < nbits; t += kScanThreads) {
+      const int w = t >> 5, b = t & 31;
+      const uint32_t x = sbits[w];
+      if (!((x >> b) & 1u)) continue;
+      const int32_t pos = wpre[w] + __popc(x & ((1u << b) - 1u));
+      const int r = t / tiles_k;
+      const int32_t col = t - r * tiles_k;
+      row_cols[pos] = col;
+      flat[pos] = t;
+      atomicOr(&tbits[col * wpc + (r >> 5)], 1u << (r & 31));
+      const int32_t rank = pos - cnt[r];
+      const int32_t kept = (r + 1 < tiles_n ? cnt[r + 1] : total) - cnt[r];
+      int32_t* rec = chunks + 4 + static_cast<int64_t>(gpre[r] + rank / kTdpChunk) * kTdpRec;
+      const int slot = rank % kTdpChunk;
+      if (slot == 0) {
+        rec[0] = r;
+        rec[1] = pos;
+        rec[2] = kept - rank < kTdpChunk ? kept - rank : kTdpChunk;
+        rec[3] = 0;
+      }
+      rec[4 + slot] = col;
+      if (rank == kept - 1)  // the row's last tile pads its group
+        for (int i = slot + 1; i < kTdpChunk; ++i) rec[4 + i] = col;
+    }
+    __syncthreads();
+    // columns, one thread per bit of the transpose (column-major words, so the
+    // positions run in column order)
+    const int ntw = tiles_k * wpc;
+    for (int w = tid; w < ntw; w += kScanThreads) wpre[w] = __popc(tbits[w]);
+    __syncthreads();
+    block_exclusive_scan(wpre, ntw, nullptr, wsum);
+    for (int k = tid; k < tiles_k; k += kScanThreads) col_ptr[k] = wpre[k * wpc];
+    if (tid == 0) col_ptr[tiles_k] = total;
+    for (int u = tid; u < ntw * 32; u += kScanThreads) {
+      const int w = u >> 5, b = u & 31;
+      const uint32_t x = tbits[w];
+      if ((x >> b) & 1u) col_rows[wpre[w] + __popc(x & ((1u << b) - 1u))] = 32 * (w % wpc) + b;
+    }
+    return;
+  }
+  // rows: lists and group records (bitmap in memory)
+  for (int r = tid; r < tiles_n; r += kScanThreads) {
+    const int32_t first = cnt[r];
+    int32_t pos = first, last = 0;
     const int64_t lo = static_cast<int64_t>(r) * tiles_k, hi = lo + tiles_k;
     for (int64_t w = lo >> 5; w <= (hi - 1) >> 5; ++w) {
       uint32_t x = src.masked(w, lo, hi);
       while (x) {
         const int64_t t = w * 32 + (__ffs(x) - 1);
-        row_cols[pos] = static_cast<int32_t>(t - lo);
+        const int32_t col = static_cast<int32_t>(t - lo);
+        row_cols[pos] = col;
         flat[pos] = static_cast<int32_t>(t);
+        const int32_t rank = pos - first;
+        int32_t* rec = chunks + 4 + static_cast<int64_t>(gpre[r] + rank / kTdpChunk) * kTdpRec;
+        if (rank % kTdpChunk == 0) {
+          rec[0] = r;
+          rec[1] = pos;
+          rec[3] = 0;
+        }
+        rec[4 + rank % kTdpChunk] = col;
+        last = col;
         ++pos;
         x &= x - 1;
       }
     }
-  }
-  __syncthreads();
-  // bwd_weight groups: ceil(kept / kTdpChunk) per row
-  for (int r = tid; r < tiles_n; r += kScanThreads) {
-    const int32_t kept = src.count(static_cast<int64_t>(r) * tiles_k, static_cast<int64_t>(r + 1) * tiles_k);
-    cnt[r] = (kept + kTdpChunk - 1) / kTdpChunk;
-  }
-  __syncthreads();
-  const int32_t groups = block_exclusive_scan(cnt, tiles_n, nullptr, wsum);
-  for (int r = tid; r < tiles_n; r += kScanThreads) {
-    const int32_t first = row_ptr[r], kept = row_ptr[r + 1] - first;
-    for (int32_t j = 0; j * kTdpChunk < kept; ++j) {
-      chunks[1 + 2 * (cnt[r] + j)] = r;
-      chunks[2 + 2 * (cnt[r] + j)] = first + j * kTdpChunk;
+    const int32_t kept = pos - first;
+    for (int32_t g = 0; g * kTdpChunk < kept; ++g) {
+      int32_t* rec = chunks + 4 + static_cast<int64_t>(gpre[r] + g) * kTdpRec;
+      const int32_t n = kept - g * kTdpChunk < kTdpChunk ? kept - g * kTdpChunk : kTdpChunk;
+      rec[2] = n;
+      for (int i = n; i < kTdpChunk; ++i) rec[4 + i] = last;  // only the row's last group is short
     }
   }
-  if (tid == 0) chunks[0] = groups;
   __syncthreads();
   // columns
   for (int k = tid; k < tiles_k; k += kScanThreads) {
@@ -168,9 +272,9 @@ __global__ void __launch_bounds__(kScanThreads)
   __syncthreads();
   block_exclusive_scan(cnt, tiles_k, col_ptr, wsum);
   for (int k = tid; k < tiles_k; k += kScanThreads) {
-    int32_t w = cnt[k];
+    int32_t pos = cnt[k];
     for (int r = 0; r < tiles_n; ++r)
-      if (src.bit(static_cast<int64_t>(r) * tiles_k + k)) col_rows[w++] = r;
+      if (src.bit(static_cast<int64_t>(r) * tiles_k + k)) col_rows[pos++] = r;
   }
 }
 
@@ -185,6 +289,7 @@ struct TdpArgs {
   const int32_t* ptr;   // row_ptr (fwd) or col_ptr (bwd_data)
   const int32_t* list;  // row_cols (fwd), col_rows (bwd_data) or flat (bwd_weight)
   float scale;
+  const int32_t* count;  // kept tiles (device), the length of flat
 };
 
 template <typename T, typename OutT, class Cfg, int PASS, bool VEC>
@@ -245,6 +350,7 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_kernel(TdpArgs a) {
     st.c.ld = a.B;
   } else {
     // bwd_weight: dW(tn, tk) = dYt[tn-block][:] Xt[tk-block][:]^T for one kept tile
+    if (static_cast<int>(blockIdx.x) >= *a.count) return;  // the grid may be an upper bound
     const int t = a.list[blockIdx.x];
     const int tn = t / a.tiles_k, tk = t % a.tiles_k;
     const T* Ab = static_cast<const T*>(a.act2) + static_cast<int64_t>(tn) * T_ * a.B;
@@ -332,10 +438,11 @@ template <class Cfg, int PASS, typename OutT>
 __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
   constexpr int TT = kFastTile, ES = Cfg::ES, SPT = TT / Cfg::BK;
   constexpr bool AMC = PASS == TDP_BWD_DATA;
-  static_assert(Cfg::BM == TT && TT % Cfg::BK == 0 && Cfg::KSPLIT == 1, "one tile row per workgroup");
+  static_assert(Cfg::BM == TT && TT % Cfg::BK == 0, "one tile row per workgroup");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
+  const int wave = threadIdx.x >> 6;
+  const int ks = wave / (Cfg::WGM * Cfg::WGN), wmn = wave % (Cfg::WGM * Cfg::WGN);
+  const int wm = wmn / Cfg::WGN, wn = wmn % Cfg::WGN;
   int own, col;
   grouped_tile(blockIdx.x, a.nx, a.ny, own, col);
   const int n0 = col * Cfg::BN;
@@ -378,11 +485,40 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
     ld.da.init(K, 0, TT, ld.wv);
     ld.db.init(B, n0, a.B, ld.wv);
   }
-  (void)lane;
-  run_slabs<Cfg, AMC, true, false>(ld, ld.nq, 0, 0, acc, wm, wn, 0, smem);
+  run_slabs<Cfg, AMC, true, false>(ld, ld.nq, 0, 0, acc, wm, wn, ks * Cfg::KW, smem);
+  if constexpr (Cfg::KSPLIT > 1) {
+    // the waves of k slices 1.. hand their sums to slice 0 through LDS
+    constexpr int NREG = Cfg::FM * Cfg::FN * 16;
+    static_assert((Cfg::KSPLIT - 1) * Cfg::WGM * Cfg::WGN * NREG * 64 * 4 <= Cfg::LDS, "reduction buffer exceeds LDS");
+    float* red = reinterpret_cast<float*>(smem);
+    const int lane = threadIdx.x & 63;
+    lds_barrier();  // every wave is done with the stages
+    if (ks > 0) {
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            red[(((ks - 1) * Cfg::WGM * Cfg::WGN + wmn) * NREG + (i * Cfg::FN + j) * 16 + r) * 64 + lane] =
+                acc[i][j][r];
+    }
+    lds_barrier();
+    if (ks == 0) {
+#pragma unroll
+      for (int u = 1; u < Cfg::KSPLIT; ++u)
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              acc[i][j][r] += red[(((u - 1) * Cfg::WGM * Cfg::WGN + wmn) * NREG + (i * Cfg::FN + j) * 16 + r) * 64 + lane];
+    }
+  }
 
   GemmArgs g = {};
-  g.M = TT;
+  g.M = ks == 0 ? TT : 0;  // only k slice 0 writes
   g.N = a.B;
   g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(own) * TT * B;
   g.c.ld = B;
@@ -392,66 +528,68 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
 
 // bwd_weight: dW(tn, tk) = scale * dYt[tn block] Xt[tk block]^T (contraction
 // over the batch) for a group of up to kTdpChunk kept tiles of tile row tn;
-// wave column wn computes the group's tile wn.
+// wave column wn computes the group's tile wn. Each workgroup takes the groups
+// t, t + gridDim.x, ... of the list (t its position in the XCD-aware order),
+// so the grid can stay at what the chip holds at once.
 template <class Cfg, typename OutT>
 __global__ void __launch_bounds__(Cfg::NT) tdp_fast_dw_kernel(TdpFastArgs a) {
   constexpr int TT = kFastTile, ES = Cfg::ES;
   static_assert(Cfg::BM == TT && Cfg::TN == TT && Cfg::BN == TT * kTdpChunk && Cfg::KSPLIT == 1,
                 "one kept tile per wave column");
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  int unused, c;
-  grouped_tile(blockIdx.x, gridDim.x, 1, unused, c);
-  if (c >= a.chunks[0]) return;  // the grid is an upper bound on the number of groups
+  int unused, c0;
+  grouped_tile(blockIdx.x, gridDim.x, 1, unused, c0);
+  const int count = __builtin_amdgcn_readfirstlane(a.chunks[0]);
   const int wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
-  const int tn = __builtin_amdgcn_readfirstlane(a.chunks[1 + 2 * c]);
-  const int p = __builtin_amdgcn_readfirstlane(a.chunks[2 + 2 * c]);
-  const int end = __builtin_amdgcn_readfirstlane(a.ptr[tn + 1]);
-  const int cnt = end - p < kTdpChunk ? end - p : kTdpChunk;
-  const int32_t* cols = a.list + p;
-
-  f32x16 acc[Cfg::FM][Cfg::FN];
-#pragma unroll
-  for (int i = 0; i < Cfg::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < Cfg::FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
   const int64_t B = a.B, K = a.K;
-  SlabLoader<Cfg, false, false> ld;
-  ld.wv = __builtin_amdgcn_readfirstlane(wave);
-  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
-  ld.da.init(B, 0, TT, ld.wv);
-  // row r of the B tile: row r % TT of X block cols[r / TT] (the last kept one
-  // for the unused wave columns of a short group, whose results are dropped)
-  ld.db.init_rows(B, [&](int r) {
-    const int j = r / TT < cnt ? r / TT : cnt - 1;
-    return cols[j] * TT + r % TT;
-  }, ld.wv);
   const int nslab = (a.B + Cfg::BK - 1) / Cfg::BK;
-  ld.K = a.B;
-  ld.ik = 0;
-  ld.is = 0;
-  ld.left = nslab - 1;
-  ld.a_step = Cfg::BK * ES;
-  ld.b_step = Cfg::BK * ES;
-  ld.a_wrap = 0;
-  ld.b_wrap = 0;
-  ld.na = uniform_ptr(static_cast<const char*>(a.act2) + static_cast<int64_t>(tn) * TT * B * ES);
-  ld.nb = uniform_ptr(static_cast<const char*>(a.act));
-  run_slabs<Cfg, false, false, true>(ld, nslab, a.B, 0, acc, wm, wn, 0, smem);
 
-  // wave column wn writes tile cols[wn]: its columns wn * TT .. land at column
-  // cols[wn] * TT of dW (cols ascend, so cols[wn] >= wn)
-  const int j = wn < cnt ? wn : cnt - 1;
-  GemmArgs g = {};
-  g.M = TT;
-  g.N = cnt * TT;
-  g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(tn) * TT * K + static_cast<int64_t>(cols[j] - j) * TT;
-  g.c.ld = K;
-  g.c.scale = a.scale;
-  fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, 0, wm, wn, 0, 0, smem);
+  for (int c = c0; c < count; c += gridDim.x) {
+    const int32_t* rec = a.chunks + 4 + static_cast<int64_t>(c) * kTdpRec;
+    const int tn = __builtin_amdgcn_readfirstlane(rec[0]);
+    const int cnt = __builtin_amdgcn_readfirstlane(rec[2]);
+    const int32_t* cols = rec + 4;  // padded with the last column up to kTdpChunk
+
+    f32x16 acc[Cfg::FM][Cfg::FN];
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    SlabLoader<Cfg, false, false> ld;
+    ld.wv = __builtin_amdgcn_readfirstlane(wave);
+    ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+    ld.da.init(B, 0, TT, ld.wv);
+    // row r of the B tile: row r % TT of X block cols[r / TT]
+    ld.db.init_rows(B, [&](int r) { return cols[r / TT] * TT + r % TT; }, ld.wv);
+    ld.K = a.B;
+    ld.ik = 0;
+    ld.is = 0;
+    ld.left = nslab - 1;
+    ld.a_step = Cfg::BK * ES;
+    ld.b_step = Cfg::BK * ES;
+    ld.a_wrap = 0;
+    ld.b_wrap = 0;
+    ld.na = uniform_ptr(static_cast<const char*>(a.act2) + static_cast<int64_t>(tn) * TT * B * ES);
+    ld.nb = uniform_ptr(static_cast<const char*>(a.act));
+    run_slabs<Cfg, false, false, true>(ld, nslab, a.B, 0, acc, wm, wn, 0, smem);
+
+    // wave column wn writes tile cols[wn]: its columns wn * TT .. land at
+    // column cols[wn] * TT of dW (cols ascend, so cols[wn] >= wn)
+    const int j = wn < cnt ? wn : 0;  // wave columns past the group write nothing
+    GemmArgs g = {};
+    g.M = TT;
+    g.N = cnt * TT;
+    g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(tn) * TT * K + static_cast<int64_t>(cols[j]) * TT -
+            static_cast<int64_t>(j) * TT;
+    g.c.ld = K;
+    g.c.scale = a.scale;
+    fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, 0, wm, wn, 0, 0, smem);
+    lds_barrier();  // the next group's loads overwrite the epilogue's staging
+  }
 }
 
 // ZERO mode: clears every dropped tile of dW.
@@ -492,13 +630,14 @@ hipError_t launch_tdp(const TdpArgs& a, dim3 grid, bool vec, hipStream_t s) {
 }
 
 template <typename T>
-hipError_t run_tdp(int pass, const TdpArgs& a, int owners, int nnz, hipStream_t s) {
+hipError_t run_tdp(int pass, const TdpArgs& a, int owners, int nnz, int tiles, hipStream_t s) {
   const bool vec = (static_cast<int64_t>(a.B) * sizeof(T)) % 16 == 0;
   using C = TdpCfgs<T>;
   if (pass == TDP_BWD_WEIGHT) {
     if (nnz == 0) return hipSuccess;
-    if (a.tile == 64) return launch_tdp<T, float, typename C::Tile64, TDP_BWD_WEIGHT>(a, dim3(nnz), vec, s);
-    return launch_tdp<T, float, typename C::Tile32, TDP_BWD_WEIGHT>(a, dim3(nnz), vec, s);
+    const dim3 grid(static_cast<unsigned>(nnz > 0 ? nnz : tiles));  // nnz < 0: known on the device only
+    if (a.tile == 64) return launch_tdp<T, float, typename C::Tile64, TDP_BWD_WEIGHT>(a, grid, vec, s);
+    return launch_tdp<T, float, typename C::Tile32, TDP_BWD_WEIGHT>(a, grid, vec, s);
   }
   const dim3 grid((a.B + 127) / 128, owners);
   if (pass == TDP_FWD) {
@@ -514,15 +653,18 @@ hipError_t run_tdp(int pass, const TdpArgs& a, int owners, int nnz, hipStream_t 
 // kTdpChunk kept tiles for bwd_weight.
 template <typename T>
 struct TdpFastCfgs;
+// Rows: four waves of 64 x 64 outputs, two of them per k half of each slab
+// (fewer LDS bytes per MFMA than 32 x 64 wave tiles over the whole slab).
+// Group: one workgroup per compute unit walking the groups.
 template <>
 struct TdpFastCfgs<bf16> {
-  using Rows = FastCfg<bf16, 64, 128, 64, 4, 2, 2, 1>;  // 96 KB LDS
-  using Group = FastCfg<bf16, 64, 256, 64, 3, 1, 4, 1>; // 120 KB
+  using Rows = FastCfg<bf16, 64, 128, 64, 4, 1, 2, 2>;   // 96 KB LDS
+  using Group = FastCfg<bf16, 64, 256, 64, 3, 1, 4, 1>;  // 120 KB
 };
 template <>
 struct TdpFastCfgs<float> {
-  using Rows = FastCfg<float, 64, 128, 32, 4, 2, 2, 1>; // 96 KB
-  using Group = FastCfg<float, 64, 256, 32, 3, 1, 4, 1>;// 120 KB
+  using Rows = FastCfg<float, 64, 128, 32, 4, 1, 2, 2>;  // 96 KB
+  using Group = FastCfg<float, 64, 256, 32, 3, 1, 4, 1>; // 120 KB
 };
 
 template <class Cfg, class Kern>
@@ -555,9 +697,13 @@ hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int o
   TdpFastArgs f = {a.act, a.act2, a.W, a.out, a.B, a.K, 0, 0, a.ptr, a.list, chunks, a.scale};
   if (pass == TDP_BWD_WEIGHT) {
     if (nnz == 0) return hipSuccess;
-    // groups: sum over rows of ceil(kept / kTdpChunk) <= (nnz + (kTdpChunk - 1) * rows with a kept tile) / kTdpChunk
+    // groups: sum over rows of ceil(kept / kTdpChunk) <= (nnz + (kTdpChunk - 1) * rows with a kept tile) / kTdpChunk;
+    // with the count known on the device only (nnz < 0), every row full
     const int64_t rows = owners < nnz ? owners : nnz;
-    const int64_t bound = (nnz + (kTdpChunk - 1) * rows) / kTdpChunk;
+    int64_t bound = nnz > 0 ? (nnz + (kTdpChunk - 1) * rows) / kTdpChunk
+                            : static_cast<int64_t>(owners) * ((a.tiles_k + kTdpChunk - 1) / kTdpChunk);
+    // one workgroup per compute unit, each walking several groups
+    if (bound > kTargetBlocks) bound = kTargetBlocks;
     return launch_with_lds<typename C::Group>(tdp_fast_dw_kernel<typename C::Group, float>,
                                              dim3(static_cast<unsigned>(bound)), f, s);
   }
@@ -585,7 +731,7 @@ int check_tile_call(const ard_tile_desc* d, const ard_tile_plan* p) {
                 d->in_features, d->out_features, p->n, p->k);
   if (p->tiles_n != p->n / p->tile || p->tiles_k != p->k / p->tile || p->n % p->tile || p->k % p->tile)
     return fail(ARD_ERR_INVALID_ARG, "plan tile grid is inconsistent");
-  if (p->nnz < 0 || p->nnz > p->tiles_n * p->tiles_k) return fail(ARD_ERR_INVALID_ARG, "plan nnz out of range");
+  if (p->nnz < -1 || p->nnz > p->tiles_n * p->tiles_k) return fail(ARD_ERR_INVALID_ARG, "plan nnz out of range");
   if (!p->d_bits || !p->d_row_ptr || !p->d_row_cols || !p->d_col_ptr || !p->d_col_rows || !p->d_flat ||
       !p->d_chunks)
     return fail(ARD_ERR_INVALID_ARG, "plan has NULL lists");
@@ -598,23 +744,10 @@ int check_dev_ptr(const void* p, const char* name) {
   return ARD_OK;
 }
 
-}  // namespace
-}  // namespace ard
-
-using namespace ard;
-
-extern "C" {
-
-size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k) {
-  if (tiles_n < 1 || tiles_k < 1) return 0;
-  const size_t nnz = static_cast<size_t>(tiles_n) * tiles_k;
-  return align256(4 * (tiles_n + 1)) + align256(4 * (tiles_k + 1)) + 3 * align256(4 * nnz) +
-         align256(4 * (1 + 2 * nnz));
-}
-
-int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, int32_t nnz, void* d_ws,
-                   size_t ws_bytes, ard_tile_plan* plan, void* stream) {
-  clear_error();
+// Shared by both plan entry points: validates, lays the lists out in the
+// workspace and launches the plan kernel (sampling the bitmap first if asked).
+int plan_tiles(int32_t n, int32_t k, int32_t tile, uint32_t* d_bits, int32_t nnz, TileSampler smp, void* d_ws,
+               size_t ws_bytes, ard_tile_plan* plan, void* stream) {
   if (!plan) return fail(ARD_ERR_INVALID_ARG, "plan is NULL");
   if (tile != 32 && tile != 64) return fail(ARD_ERR_INVALID_ARG, "tile must be 32 or 64, got %d", tile);
   if (n < tile || k < tile || n % tile || k % tile)
@@ -622,7 +755,7 @@ int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, i
   const int32_t tn = n / tile, tk = k / tile;
   if (tn > kMaxTileDim || tk > kMaxTileDim)
     return fail(ARD_ERR_UNSUPPORTED, "tile grid %d x %d exceeds %d per side", tn, tk, kMaxTileDim);
-  if (nnz < 0 || static_cast<int64_t>(nnz) > static_cast<int64_t>(tn) * tk)
+  if (static_cast<int64_t>(nnz) > static_cast<int64_t>(tn) * tk)
     return fail(ARD_ERR_INVALID_ARG, "nnz %d out of range", nnz);
   if (!d_bits) return fail(ARD_ERR_INVALID_ARG, "d_bits is NULL");
   const size_t need = ard_tile_plan_workspace_bytes(tn, tk);
@@ -650,10 +783,43 @@ int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, i
   w += align256(4 * full);
   plan->d_chunks = reinterpret_cast<int32_t*>(w);
   hipLaunchKernelGGL(plan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, static_cast<hipStream_t>(stream),
-                     d_bits, tn, tk, plan->d_row_ptr, plan->d_row_cols, plan->d_col_ptr,
+                     d_bits, smp, tn, tk, plan->d_row_ptr, plan->d_row_cols, plan->d_col_ptr,
                      plan->d_col_rows, plan->d_flat, plan->d_chunks);
   ARD_LAUNCH_CHECK();
   return ARD_OK;
+}
+
+}  // namespace
+}  // namespace ard
+
+using namespace ard;
+
+extern "C" {
+
+size_t ard_tile_plan_workspace_bytes(int32_t tiles_n, int32_t tiles_k) {
+  if (tiles_n < 1 || tiles_k < 1) return 0;
+  const size_t nnz = static_cast<size_t>(tiles_n) * tiles_k;
+  return align256(4 * (tiles_n + 1)) + align256(4 * (tiles_k + 1)) + 3 * align256(4 * nnz) +
+         align256(4 * (4 + kTdpRec * nnz));
+}
+
+int ard_plan_tiles(int32_t n, int32_t k, int32_t tile, const uint32_t* d_bits, int32_t nnz, void* d_ws,
+                   size_t ws_bytes, ard_tile_plan* plan, void* stream) {
+  clear_error();
+  if (nnz < 0) return fail(ARD_ERR_INVALID_ARG, "nnz %d out of range", nnz);
+  return plan_tiles(n, k, tile, const_cast<uint32_t*>(d_bits), nnz, TileSampler{0, 0.0, 0}, d_ws, ws_bytes, plan,
+                    stream);
+}
+
+int ard_plan_tiles_bernoulli(int32_t n, int32_t k, int32_t tile, double p, uint64_t seed, uint32_t stream_id,
+                             uint64_t iter, uint32_t* d_bits, void* d_ws, size_t ws_bytes, ard_tile_plan* plan,
+                             void* stream) {
+  clear_error();
+  if (!(p >= 0.0 && p <= 1.0)) return fail(ARD_ERR_INVALID_ARG, "p must lie in [0, 1]");
+  if (stream_id >= (1u << 24)) return fail(ARD_ERR_INVALID_ARG, "stream %u must be < 2^24", stream_id);
+  if (iter >= (uint64_t{1} << 40)) return fail(ARD_ERR_INVALID_ARG, "iter must be < 2^40");
+  const TileSampler smp = {1, p, seed ^ ((static_cast<uint64_t>(stream_id) << 40) | iter)};
+  return plan_tiles(n, k, tile, d_bits, -1, smp, d_ws, ws_bytes, plan, stream);
 }
 
 int ard_tile_fwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt, const void* W,
@@ -664,18 +830,19 @@ int ard_tile_fwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const voi
   if ((st = check_dev_ptr(Xt, "Xt")) || (st = check_dev_ptr(W, "W")) || (st = check_dev_ptr(Yt, "Yt")))
     return st;
   TdpArgs a = {Xt, nullptr, W, Yt, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
-               plan->d_row_ptr, plan->d_row_cols, desc->scale};
+               plan->d_row_ptr, plan->d_row_cols, desc->scale, plan->d_row_ptr + plan->tiles_n};
+  const int full = plan->tiles_n * plan->tiles_k;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
     if (tdp_fast_ok<bf16>(a))
       ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_FWD, a, plan->d_chunks, plan->tiles_n, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<bf16>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_FWD, a, plan->tiles_n, plan->nnz, full, s));
   } else {
     if (tdp_fast_ok<float>(a))
       ARD_HIP_CHECK(run_tdp_fast<float>(TDP_FWD, a, plan->d_chunks, plan->tiles_n, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<float>(TDP_FWD, a, plan->tiles_n, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<float>(TDP_FWD, a, plan->tiles_n, plan->nnz, full, s));
   }
   return ARD_OK;
 }
@@ -688,18 +855,19 @@ int ard_tile_bwd_data(const ard_tile_desc* desc, const ard_tile_plan* plan, cons
   if ((st = check_dev_ptr(dYt, "dYt")) || (st = check_dev_ptr(W, "W")) || (st = check_dev_ptr(dXt, "dXt")))
     return st;
   TdpArgs a = {dYt, nullptr, W, dXt, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
-               plan->d_col_ptr, plan->d_col_rows, desc->scale};
+               plan->d_col_ptr, plan->d_col_rows, desc->scale, plan->d_row_ptr + plan->tiles_n};
+  const int full = plan->tiles_n * plan->tiles_k;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
     if (tdp_fast_ok<bf16>(a))
       ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_BWD_DATA, a, plan->d_chunks, plan->tiles_k, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, full, s));
   } else {
     if (tdp_fast_ok<float>(a))
       ARD_HIP_CHECK(run_tdp_fast<float>(TDP_BWD_DATA, a, plan->d_chunks, plan->tiles_k, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, full, s));
   }
   return ARD_OK;
 }
@@ -712,7 +880,8 @@ int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, co
   if ((st = check_dev_ptr(Xt, "Xt")) || (st = check_dev_ptr(dYt, "dYt")) || (st = check_dev_ptr(dW, "dW")))
     return st;
   TdpArgs a = {Xt, dYt, nullptr, dW, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
-               nullptr, plan->d_flat, desc->scale};
+               nullptr, plan->d_flat, desc->scale, plan->d_row_ptr + plan->tiles_n};
+  const int full = plan->tiles_n * plan->tiles_k;
   TdpArgs f = a;  // the fast path walks the groups of row_cols
   f.ptr = plan->d_row_ptr;
   f.list = plan->d_row_cols;
@@ -721,14 +890,14 @@ int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, co
     if (tdp_fast_ok<bf16>(a))
       ARD_HIP_CHECK(run_tdp_fast<bf16>(TDP_BWD_WEIGHT, f, plan->d_chunks, plan->tiles_n, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<bf16>(TDP_BWD_WEIGHT, a, 0, plan->nnz, full, s));
   } else {
     if (tdp_fast_ok<float>(a))
       ARD_HIP_CHECK(run_tdp_fast<float>(TDP_BWD_WEIGHT, f, plan->d_chunks, plan->tiles_n, plan->nnz, s));
     else
-      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_WEIGHT, a, 0, plan->nnz, s));
+      ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_WEIGHT, a, 0, plan->nnz, full, s));
   }
-  if (desc->dropped == ARD_DROPPED_ZERO && plan->nnz < plan->tiles_n * plan->tiles_k) {
+  if (desc->dropped == ARD_DROPPED_ZERO && plan->nnz != full) {
     hipLaunchKernelGGL(zero_dropped_tiles_kernel, dim3(plan->tiles_k, plan->tiles_n), dim3(256), 0, s,
                        plan->d_bits, dW, plan->k, plan->tile, plan->tiles_k);
     ARD_LAUNCH_CHECK();

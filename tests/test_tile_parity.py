@@ -35,8 +35,37 @@ def tile_plan(n, k, tile, words, check=True):
     return plan
 
 
+def check_lists(plan, ws, L, tn, tk, nnz):
+    def arr(ptr, count):
+        base = ptr - ws.data_ptr()
+        return ws[base // 4: base // 4 + count].cpu().tolist()
+
+    assert arr(plan.d_row_ptr, tn + 1) == L["row_ptr"]
+    assert arr(plan.d_col_ptr, tk + 1) == L["col_ptr"]
+    assert arr(plan.d_row_cols, nnz) == L["row_cols"]
+    assert arr(plan.d_col_rows, nnz) == L["col_rows"]
+    assert arr(plan.d_flat, nnz) == L["flat"]
+    assert arr(plan.d_chunks, len(L["chunks"])) == L["chunks"]
+
+
+def sampled_plan(n, k, tile, p, seed, stream, it):
+    """Plan with the Bernoulli bitmap drawn on the device; checks the bitmap
+    bit for bit and every list against the oracle. Returns (plan, words)."""
+    tn, tk = n // tile, k // tile
+    words = oprng.tile_bitmap_bernoulli(tn, tk, p, seed, stream, it)
+    nnz = opat.bitmap_popcount(words, tn * tk)
+    bits = torch.full(((tn * tk + 31) // 32,), -1, dtype=torch.int32, device=device())
+    ws = torch.zeros(api.ard_tile_plan_workspace_bytes(tn, tk) // 4, dtype=torch.int32, device=device())
+    plan = api.ard_plan_tiles_bernoulli(n, k, tile, p, seed, stream, it, bits, ws)
+    torch.cuda.synchronize()
+    assert plan.nnz == -1
+    assert bits.cpu().numpy().view(np.uint32).tolist() == [int(w) for w in words]
+    check_lists(plan, ws, opat.tile_lists(words, tn, tk), tn, tk, nnz)
+    return plan, words
+
+
 def run_tile(dtype, B, N, K, tile, words, scale=1.0, dropped=api.ARD_DROPPED_ZERO, seed=0,
-             sentinel=0.0, poison=False):
+             sentinel=0.0, poison=False, plan=None):
     g = synth.generator(seed)
     X = synth.to_storage(synth.normal(g, (B, K)), dtype)
     W = synth.to_storage(synth.normal(g, (N, K), 0.02), dtype)
@@ -45,7 +74,8 @@ def run_tile(dtype, B, N, K, tile, words, scale=1.0, dropped=api.ARD_DROPPED_ZER
     M = opat.tile_mask(words, tn, tk, tile)
     Y64 = otdp.tdp_forward(f64(X), f64(W), M, scale)
     dX64, dW64 = otdp.tdp_backward(f64(X), f64(W), f64(dY), M, scale)
-    plan = tile_plan(N, K, tile, words)
+    if plan is None:
+        plan = tile_plan(N, K, tile, words)
     desc = api.tile_desc(ard_dtype(dtype), B, K, N, scale, dropped)
     Xt, Wd, dYt = to_dev(X.T), to_dev(W), to_dev(dY.T)
     if poison:
@@ -142,6 +172,34 @@ def test_full_config_bf16_4096():
             2e-2, "dW")
 
 
+@pytest.mark.parametrize("grid", [(260, 260), (33, 1100), (1, 4096)])
+def test_plan_lists_of_large_grids(grid):
+    """Plans of bitmaps too large to stage in LDS (more than 65536 tiles, or a
+    transpose of more than 2048 words) read the bitmap from memory."""
+    tn, tk = grid
+    words = oprng.tile_bitmap_bernoulli(tn, tk, 0.6, 17, 0, 0)
+    tile_plan(tn * 32, tk * 32, 32, words)
+
+
+@pytest.mark.parametrize("grid,p", [((64, 64), 0.5), ((3, 5), 0.4), ((70, 66), 0.02), ((260, 260), 0.6),
+                                    ((33, 1100), 0.3), ((4, 4), 0.0), ((4, 4), 1.0)])
+def test_device_sampled_bitmap_and_lists(grid, p):
+    tn, tk = grid
+    sampled_plan(tn * 32, tk * 32, 32, p, 8939, 0, 5)
+    sampled_plan(tn * 32, tk * 32, 32, p, 1805, 7, (1 << 40) - 1)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tile", [32, 64])
+@pytest.mark.parametrize("p,dropped", [(0.5, api.ARD_DROPPED_ZERO), (0.3, api.ARD_DROPPED_SKIP),
+                                       (1.0, api.ARD_DROPPED_ZERO), (0.0, api.ARD_DROPPED_SKIP)])
+def test_layer_on_device_sampled_plan(dtype, tile, p, dropped):
+    """Kept count on the device only: launches sized for every tile kept."""
+    N, K, B = 5 * tile, 7 * tile, 40
+    plan, words = sampled_plan(N, K, tile, p, 42, 3, 11)
+    run_tile(dtype, B, N, K, tile, words, scale=2.0, dropped=dropped, sentinel=-3.0, plan=plan)
+
+
 def test_plan_validation():
     words = oprng.tile_bitmap_tdp(2, 2, 2, 0)
     bits = torch.tensor(np.array(words, dtype=np.uint32).view(np.int32), device=device())
@@ -154,3 +212,9 @@ def test_plan_validation():
         api.ard_plan_tiles(128, 128, 64, bits, 5, ws)      # nnz out of range
     with pytest.raises(api.ArdError):
         api.ard_plan_tiles(128, 128, 64, bits, 2, ws[:4])  # workspace too small
+    for bad in (dict(p=1.5), dict(p=-0.1), dict(stream_id=1 << 24), dict(iteration=1 << 40)):
+        args = dict(p=0.5, stream_id=0, iteration=0)
+        args.update(bad)
+        with pytest.raises(api.ArdError):
+            api.ard_plan_tiles_bernoulli(128, 128, 64, args["p"], 1, args["stream_id"], args["iteration"],
+                                         bits, ws)
