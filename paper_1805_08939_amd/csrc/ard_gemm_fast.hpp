@@ -716,7 +716,8 @@ inline int fast_splits(int64_t tiles, int64_t slabs) {
   return s;
 }
 
-// fp32: the largest tile whose grid still covers 5/8 of the chip, then split-K.
+// fp32: the largest tile that the output fills along both sides and whose
+// grid still covers 5/8 of the chip, then split-K.
 inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
   using C = FastCfgs<float>;
   auto tiles_of = [&](int bm, int bn) {
@@ -725,7 +726,7 @@ inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
   FastPlan p;
   int bk;
   int64_t tiles;
-  if (tiles_of(C::Huge::BM, C::Huge::BN) >= kTargetBlocks * 5 / 8) {
+  if (M > C::Big::BM && N > C::Big::BN && tiles_of(C::Huge::BM, C::Huge::BN) >= kTargetBlocks * 5 / 8) {
     p.kind = FAST_HUGE;
     bk = C::Huge::BK;
     tiles = tiles_of(C::Huge::BM, C::Huge::BN);

@@ -14,15 +14,18 @@
 // in), then per step a kernel computing Wc_h h_{t-1} for a 32-row x 32-column
 // tile (four waves split the contraction and reduce through LDS) fused with
 // the gate nonlinearities and the state update.
-// bwd: per step a kernel computing dh = Wc_h^T dA_{t+1} fused with the
-// pointwise backward of step t; then K-batched GEMMs over all steps for the
-// weight gradients and one batched GEMM for dX.
+// bwd: per step a split-K kernel for dh = Wc_h^T dA_{t+1} (the contraction
+// over the 4 |S| gate rows cut into slices, one partial sum each, so that the
+// small product still fills the chip), then the pointwise backward of step t,
+// which adds the partial sums in a fixed order; then K-batched GEMMs over all
+// steps for the weight gradients and one batched GEMM for dX.
 
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 
 #include "ard_gemm.hpp"
+#include "ard_gemm_fast.hpp"
 #include "ard_internal.hpp"
 
 namespace ard {
@@ -30,9 +33,20 @@ namespace ard {
 namespace {
 
 struct Layout {
-  int64_t T, B, I, H, ns, G4, KW;
-  size_t wc, bc, rowmap, z, cc, hc, da, dc, total;
+  int64_t T, B, I, H, ns, G4, KW, S;
+  size_t wc, bc, rowmap, z, cc, hc, da, dc, part, total;
 };
+
+// Splits of the backward recurrent contraction (length 4 ns): enough
+// workgroups of 32 x 32 outputs to fill the chip twice, each split at least
+// one 64-wide slab.
+int64_t bwd_splits(int64_t ns, int64_t B) {
+  const int64_t tiles = ((ns + 31) / 32) * ((B + 31) / 32);
+  const int64_t slabs = (4 * ns + 63) / 64;
+  int64_t sp = 512 / (tiles > 0 ? tiles : 1);
+  if (sp > slabs) sp = slabs;
+  return sp < 1 ? 1 : sp;
+}
 
 size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -45,6 +59,7 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
   L.ns = ns;
   L.G4 = 4 * static_cast<int64_t>(ns);
   L.KW = L.I + ns;
+  L.S = bwd_splits(ns, L.B);
   size_t off = 0;
   L.wc = off;     off += al256(4 * L.G4 * L.KW);
   L.bc = off;     off += al256(4 * L.G4 + 4);
@@ -54,6 +69,7 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
   L.hc = off;     off += al256(4 * (L.T + 1) * ns * L.B);
   L.da = off;     off += al256(4 * L.T * L.G4 * L.B);
   L.dc = off;     off += al256(4 * static_cast<int64_t>(ns) * L.B + 4);
+  L.part = off;   off += al256(4 * L.S * ns * L.B + 4);
   L.total = off;
   return L;
 }
@@ -273,32 +289,53 @@ __global__ void lstm_bwd_last_kernel(LstmStep s, const float* __restrict__ dhT, 
   lstm_point_bwd(s, s.t, u, b, dh);
 }
 
-// dh_rec = Wc_h^T dA[t] for 32 units x 32 samples, then the pointwise backward
-// of step t - 1 (or, at t = 0, dh0).
-template <bool AVEC, bool BVEC, bool FINAL>
-__global__ void __launch_bounds__(256) lstm_bwd_step_kernel(LstmStep s) {
+// Partial sums of dh_rec = Wc_h^T dA[t]: workgroup (x, y, z) computes 32
+// units x 32 samples over gate rows [z * ks, (z + 1) * ks) into part[z].
+template <bool AVEC, bool BVEC>
+__global__ void __launch_bounds__(256) lstm_bwd_rec_kernel(LstmStep s, float* __restrict__ part, int32_t ks) {
   const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t k0 = static_cast<int64_t>(blockIdx.z) * ks;
+  const int klen = static_cast<int>(s.G4 - k0 < ks ? s.G4 - k0 : ks);
   GemmOperand a = {}, b = {};
   a.ld = s.KW;
   b.ld = s.B;
   const float* dAt = s.dA + static_cast<int64_t>(s.t) * s.G4 * s.B;
   float z[4];
-  splitk_32x32<AVEC ? MC_VEC : MC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I, b, dAt, m0, n0, s.ns, s.B,
-                                                                  s.G4, z);
+  splitk_32x32<AVEC ? MC_VEC : MC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I + k0 * s.KW, b, dAt + k0 * s.B, m0,
+                                                                  n0, s.ns, s.B, klen, z);
   const int64_t col = n0 + (lane & 31);
   if (col >= s.B) return;
+  float* out = part + static_cast<int64_t>(blockIdx.z) * s.ns * s.B;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int64_t u = m0 + 8 * w + 4 * (lane >> 5) + q;
-    if (u >= s.ns) continue;
-    const int64_t j = unit_row(s.idx, u);
-    if (FINAL) {
-      if (s.dh0) s.dh0[j * s.B + col] = z[q];
-    } else {
-      const float dh = s.dHs[(static_cast<int64_t>(s.t - 1) * s.H + j) * s.B + col] + z[q];
-      lstm_point_bwd(s, s.t - 1, u, col, dh);
-    }
+    if (u < s.ns) out[u * s.B + col] = z[q];
+  }
+}
+
+// dh_rec of unit u, sample b: the splits' partial sums added in split order.
+__device__ __forceinline__ float rec_sum(const float* __restrict__ part, int32_t splits, int64_t nsB, int64_t e) {
+  float v = 0.0f;
+  for (int z = 0; z < splits; ++z) v += part[z * nsB + e];
+  return v;
+}
+
+// Pointwise backward of step t - 1 with dh = dHs[t - 1] + dh_rec (FINAL:
+// dh0 = dh_rec instead), one thread per unit and sample.
+template <bool FINAL>
+__global__ void __launch_bounds__(256) lstm_bwd_point_kernel(LstmStep s, const float* __restrict__ part,
+                                                             int32_t splits) {
+  const int64_t nsB = static_cast<int64_t>(s.ns) * s.B;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= nsB) return;
+  const int64_t u = e / s.B, b = e % s.B;
+  const int64_t j = unit_row(s.idx, u);
+  const float r = rec_sum(part, splits, nsB, e);
+  if (FINAL) {
+    if (s.dh0) s.dh0[j * s.B + b] = r;
+  } else {
+    lstm_point_bwd(s, s.t - 1, u, b, s.dHs[(static_cast<int64_t>(s.t - 1) * s.H + j) * s.B + b] + r);
   }
 }
 
@@ -415,8 +452,12 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   g.c = {s.Z, L.B, nullptr, nullptr, L.G4 * L.B, reinterpret_cast<const float*>(w + L.bc), 0, 1.0f};
   const bool kw_vec = L.KW % 4 == 0;
   const bool b_vec = L.B % 4 == 0 && L.I % 4 == 0;
-  ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-      g, static_cast<int>(L.T), kw_vec, b_vec, sm)));
+  if (fast_ok(g, sizeof(float))) {
+    ARD_HIP_CHECK((run_fast_gemm<float, false, true, float, EPI_FWD>(g, static_cast<int>(L.T), sm, nullptr)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+        g, static_cast<int>(L.T), kw_vec, b_vec, sm)));
+  }
 
   const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((L.G4 + 31) / 32));
   const bool avec = kw_vec && L.I % 4 == 0, bvec = L.B % 4 == 0;
@@ -480,29 +521,33 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   hipLaunchKernelGGL(lstm_bwd_last_kernel, grid1d(nsB, 256), dim3(256), 0, sm, s,
                      static_cast<const float*>(dhT), static_cast<const float*>(dcT));
   ARD_LAUNCH_CHECK();
-  const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32));
+  // dh_rec(t) by split-K partial sums, then the pointwise backward of step t - 1
+  const int32_t ks = static_cast<int32_t>(((L.G4 + L.S - 1) / L.S + 63) / 64 * 64);  // whole slabs per split
+  const int32_t splits = static_cast<int32_t>((L.G4 + ks - 1) / ks);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  const dim3 rgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32),
+                   static_cast<unsigned>(splits));
   const bool vec = L.KW % 4 == 0 && L.I % 4 == 0 && L.B % 4 == 0;
-  for (int t = static_cast<int>(L.T) - 1; t >= 1; --t) {
+  for (int t = static_cast<int>(L.T) - 1; t >= 0; --t) {
+    if (t == 0 && !dh0) break;
     s.t = t;
     if (vec)
-      hipLaunchKernelGGL((lstm_bwd_step_kernel<true, true, false>), sgrid, dim3(256), 0, sm, s);
+      hipLaunchKernelGGL((lstm_bwd_rec_kernel<true, true>), rgrid, dim3(256), 0, sm, s, part, ks);
     else
-      hipLaunchKernelGGL((lstm_bwd_step_kernel<false, false, false>), sgrid, dim3(256), 0, sm, s);
+      hipLaunchKernelGGL((lstm_bwd_rec_kernel<false, false>), rgrid, dim3(256), 0, sm, s, part, ks);
+    ARD_LAUNCH_CHECK();
+    if (t > 0) {
+      hipLaunchKernelGGL((lstm_bwd_point_kernel<false>), grid1d(nsB, 256), dim3(256), 0, sm, s, part, splits);
+    } else {
+      s.dh0 = static_cast<float*>(dh0);
+      hipLaunchKernelGGL((lstm_bwd_point_kernel<true>), grid1d(nsB, 256), dim3(256), 0, sm, s, part, splits);
+    }
     ARD_LAUNCH_CHECK();
   }
-  if (dh0) {
-    s.t = 0;
-    s.dh0 = static_cast<float*>(dh0);
-    if (vec)
-      hipLaunchKernelGGL((lstm_bwd_step_kernel<true, true, true>), sgrid, dim3(256), 0, sm, s);
-    else
-      hipLaunchKernelGGL((lstm_bwd_step_kernel<false, false, true>), sgrid, dim3(256), 0, sm, s);
+  if (dh0 && period > 1) {
+    hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(L.H)), dim3(256), 0, sm,
+                       static_cast<float*>(dh0), L.H, s.B, s.H, period, offset);
     ARD_LAUNCH_CHECK();
-    if (period > 1) {
-      hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(L.H)), dim3(256), 0, sm,
-                         static_cast<float*>(dh0), L.H, s.B, s.H, period, offset);
-      ARD_LAUNCH_CHECK();
-    }
   }
   if (dc0) {
     hipLaunchKernelGGL(lstm_scatter_state_kernel, grid1d(HB, 256), dim3(256), 0, sm, s.dc, s.H, s.B, period,
@@ -517,7 +562,33 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     ARD_LAUNCH_CHECK();
   }
   const bool bv = L.B % 4 == 0;
+  // Per gate q the compact rows 4u + q of dA are every fourth row, and the
+  // output rows q H + S(u) and recurrent columns I + S(v) of a row pattern are
+  // strided views of dW: the weight gradient runs as four plain strided
+  // GEMMs (one launch, batched over the gates) when the operands allow.
+  bool dw_done = false;
   if (dW) {
+    GemmArgs g = {};
+    g.M = ns;
+    g.N = s.I;
+    g.K = s.B;
+    g.kbatch = static_cast<int32_t>(L.T);
+    g.a = {s.dA, nullptr, 4 * L.B, nullptr, nullptr, L.B, 0, 1.0f, L.G4 * L.B};
+    g.b = {X, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
+    g.c = {dW + static_cast<int64_t>(offset) * colsW, period * colsW, nullptr, nullptr, L.H * colsW, nullptr, 0,
+           1.0f};
+    GemmArgs gr = g;  // recurrent columns
+    gr.N = ns;
+    gr.b = {s.Hc, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, nsB};
+    gr.c.p = dW + static_cast<int64_t>(offset) * colsW + L.I + offset;
+    gr.c.col_stride = period;
+    if (fast_ok(g, sizeof(float)) && fast_ok(gr, sizeof(float))) {
+      ARD_HIP_CHECK((run_fast_gemm<float, false, false, float, EPI_FWD>(g, 4, sm, nullptr)));
+      ARD_HIP_CHECK((run_fast_gemm<float, false, false, float, EPI_FWD>(gr, 4, sm, nullptr)));
+      dw_done = true;
+    }
+  }
+  if (dW && !dw_done) {
     // dW[rowmap][:I] = sum_t dA[t] X[t]^T ; dW[rowmap][I + S] = sum_t dA[t] Hc[t]^T
     GemmArgs g = {};
     g.M = static_cast<int32_t>(L.G4);
@@ -559,8 +630,12 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     g.a = {s.Wc, nullptr, L.KW, nullptr, nullptr, 0, 0, 1.0f, 0};
     g.b = {s.dA, nullptr, L.B, nullptr, nullptr, L.G4 * L.B, 0, 1.0f, 0};
     g.c = {dX, L.B, nullptr, nullptr, L.I * L.B, nullptr, 0, 1.0f};
-    ARD_HIP_CHECK((run_gemm<float, float, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-        g, static_cast<int>(L.T), L.KW % 4 == 0 && L.I % 4 == 0, bv, sm)));
+    if (fast_ok(g, sizeof(float))) {
+      ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(g, static_cast<int>(L.T), sm, nullptr)));
+    } else {
+      ARD_HIP_CHECK((run_gemm<float, float, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+          g, static_cast<int>(L.T), L.KW % 4 == 0 && L.I % 4 == 0, bv, sm)));
+    }
   }
   return ARD_OK;
 }
