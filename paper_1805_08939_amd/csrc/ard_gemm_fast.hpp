@@ -681,7 +681,7 @@ inline bool fast_ok(const GemmArgs& g, size_t esize) {
 }
 
 // Configurations: large tiles for large grids, 32x32 tiles with the k of each
-// slab split over the 4 waves for small grids.
+// slab split over the waves (4 for bf16, 8 for fp32) for small grids.
 template <typename T>
 struct FastCfgs;
 template <>
@@ -698,7 +698,7 @@ struct FastCfgs<float> {
   using Wide = Huge;
   using Tall = Huge;
   using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 1>;     // 96 KB
-  using Small = FastCfg<float, 32, 32, 64, 4, 1, 1, 4>;   // 64 KB
+  using Small = FastCfg<float, 32, 32, 128, 4, 1, 1, 8>;  // 128 KB, 8 waves on 16-deep k shares
 };
 
 enum FastKind { FAST_HUGE, FAST_WIDE, FAST_TALL, FAST_BIG, FAST_SMALL };
@@ -739,7 +739,10 @@ inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
     bk = C::Small::BK;
     tiles = tiles_of(C::Small::BM, C::Small::BN);
   }
-  p.splits = fast_splits(tiles, static_cast<int64_t>(kbatch > 0 ? kbatch : 1) * ((K + bk - 1) / bk));
+  // split-K pays for its partial-sum round trip and reduction launch only on
+  // long contractions (measured on MI355X: never below K = 2048)
+  const int64_t kb = kbatch > 0 ? kbatch : 1;
+  p.splits = kb * K >= 8192 ? fast_splits(tiles, kb * ((K + bk - 1) / bk)) : 1;
   return p;
 }
 

@@ -248,8 +248,10 @@ def test_pregated_gradient_and_input_gate(dtype):
     ("bf16", 2048, 1024, 4096, ((3, 0), (1, 0))),
     # 32x32 tiles split 4 (bwd_data)
     ("bf16", 256, 1024, 2048, ((4, 1), (1, 0))),
+    # fp32 32x32 tiles (8 waves) and the fp32 split-K path of a long contraction (fwd)
+    ("f32", 128, 16384, 256, ((1, 0), (1, 0))),
 ], ids=["bf16-patterned", "bf16-dense-ragged", "f32-dense-ragged", "f32-patterned", "bf16-t128-split",
-        "bf16-t256-split", "bf16-t256x128-split", "bf16-t32-split"])
+        "bf16-t256-split", "bf16-t256x128-split", "bf16-t32-split", "f32-t32-split"])
 def test_wide_layer_full_size_sampled(dtype, B, K, N, pats):
     """One hidden layer of the wide MLP in the launch configuration of the
     benchmark (compact weights, SKIP, workspace), against the oracle on sampled
