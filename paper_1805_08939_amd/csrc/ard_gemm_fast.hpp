@@ -807,13 +807,10 @@ template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
 inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) {
   const int splits = g.splits > 1 ? g.splits : 1;
   auto kern = fast_gemm_kernel<Cfg, AMC, BMC, OutT, EPI>;
-  static bool attr_set = false;  // per instantiation: allow more than 64 KB of dynamic LDS
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  // per instantiation, once (thread-safe static initialisation): allow more than 64 KB of dynamic LDS
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
+  if (attr != hipSuccess) return attr;
   dim3 grid((g.N + Cfg::BN - 1) / Cfg::BN, (g.M + Cfg::BM - 1) / Cfg::BM, batch * splits);
   hipLaunchKernelGGL(kern, grid, dim3(Cfg::NT), Cfg::LDS, stream, g);
   hipError_t e = hipGetLastError();

@@ -667,15 +667,14 @@ struct TdpFastCfgs<float> {
   using Group = FastCfg<float, 64, 256, 32, 3, 1, 4, 1>; // 120 KB
 };
 
-template <class Cfg, class Kern>
-hipError_t launch_with_lds(Kern kern, dim3 grid, const TdpFastArgs& a, hipStream_t s) {
-  static bool attr_set = false;  // per instantiation: allow more than 64 KB of dynamic LDS
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+// One instantiation per kernel, so each kernel's attribute is set once
+// (thread-safe static initialisation) to allow more than 64 KB of dynamic LDS.
+template <class Cfg, void (*KERN)(TdpFastArgs)>
+hipError_t launch_with_lds(dim3 grid, const TdpFastArgs& a, hipStream_t s) {
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(KERN),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
+  if (attr != hipSuccess) return attr;
+  auto kern = KERN;
   hipLaunchKernelGGL(kern, grid, dim3(Cfg::NT), Cfg::LDS, s, a);
   return hipGetLastError();
 }
@@ -704,14 +703,14 @@ hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int o
                             : static_cast<int64_t>(owners) * ((a.tiles_k + kTdpChunk - 1) / kTdpChunk);
     // one workgroup per compute unit, each walking several groups
     if (bound > kTargetBlocks) bound = kTargetBlocks;
-    return launch_with_lds<typename C::Group>(tdp_fast_dw_kernel<typename C::Group, float>,
-                                             dim3(static_cast<unsigned>(bound)), f, s);
+    return launch_with_lds<typename C::Group, tdp_fast_dw_kernel<typename C::Group, float>>(
+        dim3(static_cast<unsigned>(bound)), f, s);
   }
   f.nx = (a.B + C::Rows::BN - 1) / C::Rows::BN;
   f.ny = owners;
   const dim3 grid(static_cast<unsigned>(f.nx * f.ny));
-  if (pass == TDP_FWD) return launch_with_lds<typename C::Rows>(tdp_fast_kernel<typename C::Rows, TDP_FWD, T>, grid, f, s);
-  return launch_with_lds<typename C::Rows>(tdp_fast_kernel<typename C::Rows, TDP_BWD_DATA, T>, grid, f, s);
+  if (pass == TDP_FWD) return launch_with_lds<typename C::Rows, tdp_fast_kernel<typename C::Rows, TDP_FWD, T>>(grid, f, s);
+  return launch_with_lds<typename C::Rows, tdp_fast_kernel<typename C::Rows, TDP_BWD_DATA, T>>(grid, f, s);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }

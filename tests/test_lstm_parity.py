@@ -81,7 +81,9 @@ def test_tiny_patterns(pattern):
 
 
 @pytest.mark.parametrize("shape,pattern", [((4, 40, 68, 100), (3, 1)), ((3, 37, 33, 70), (2, 0)),
-                                           ((5, 96, 128, 160), (4, 3)), ((1, 8, 12, 64), (5, 2))])
+                                           ((5, 96, 128, 160), (4, 3)), ((1, 8, 12, 64), (5, 2)),
+                                           # split forward recurrence on unaligned operands (KW = 370)
+                                           ((3, 36, 70, 600), (2, 1))])
 def test_multi_tile_and_unaligned(shape, pattern):
     T, B, I, H = shape
     run_lstm(T, B, I, H, pattern, seed=B)
