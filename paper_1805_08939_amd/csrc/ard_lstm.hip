@@ -521,20 +521,48 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   hipLaunchKernelGGL(lstm_bwd_last_kernel, grid1d(nsB, 256), dim3(256), 0, sm, s,
                      static_cast<const float*>(dhT), static_cast<const float*>(dcT));
   ARD_LAUNCH_CHECK();
-  // dh_rec(t) by split-K partial sums, then the pointwise backward of step t - 1
-  const int32_t ks = static_cast<int32_t>(((L.G4 + L.S - 1) / L.S + 63) / 64 * 64);  // whole slabs per split
-  const int32_t splits = static_cast<int32_t>((L.G4 + ks - 1) / ks);
+  // dh_rec(t) by split-K partial sums, then the pointwise backward of step t - 1.
+  // With a split count that divides the 4 |S| gate rows, the splits are the
+  // batch of one strided direct-load GEMM (slice z: Wc_h^T rows z ks .. and
+  // dA rows z ks .., output part[z]); otherwise the 32 x 32 split kernel.
+  int32_t ks = static_cast<int32_t>(((L.G4 + L.S - 1) / L.S + 63) / 64 * 64);  // whole slabs per split
+  int32_t splits = static_cast<int32_t>((L.G4 + ks - 1) / ks);
   float* part = reinterpret_cast<float*>(w + L.part);
+  int32_t fs = 0;  // exact split count for the direct-load GEMM, 0 = none
+  for (int32_t d = static_cast<int32_t>(L.S); d >= 1; --d)
+    if (L.G4 % d == 0 && L.G4 / d >= 256) {
+      fs = d;
+      break;
+    }
+  GemmArgs gr = {};
+  bool rec_fast = false;
+  if (fs > 0) {
+    gr.M = ns;
+    gr.N = s.B;
+    gr.K = static_cast<int32_t>(L.G4 / fs);
+    gr.a = {s.Wc + L.I, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
+    gr.b = {s.dA, nullptr, L.B, nullptr, nullptr, gr.K * L.B, 0, 1.0f, 0};
+    gr.c = {part, L.B, nullptr, nullptr, nsB, nullptr, 0, 1.0f};
+    rec_fast = fast_ok(gr, sizeof(float));
+    if (rec_fast) {
+      ks = gr.K;
+      splits = fs;
+    }
+  }
   const dim3 rgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32),
                    static_cast<unsigned>(splits));
   const bool vec = L.KW % 4 == 0 && L.I % 4 == 0 && L.B % 4 == 0;
   for (int t = static_cast<int>(L.T) - 1; t >= 0; --t) {
     if (t == 0 && !dh0) break;
     s.t = t;
-    if (vec)
+    if (rec_fast) {
+      gr.b.p = s.dA + static_cast<int64_t>(t) * L.G4 * L.B;
+      ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(gr, splits, sm, nullptr)));
+    } else if (vec) {
       hipLaunchKernelGGL((lstm_bwd_rec_kernel<true, true>), rgrid, dim3(256), 0, sm, s, part, ks);
-    else
+    } else {
       hipLaunchKernelGGL((lstm_bwd_rec_kernel<false, false>), rgrid, dim3(256), 0, sm, s, part, ks);
+    }
     ARD_LAUNCH_CHECK();
     if (t > 0) {
       hipLaunchKernelGGL((lstm_bwd_point_kernel<false>), grid1d(nsB, 256), dim3(256), 0, sm, s, part, splits);
