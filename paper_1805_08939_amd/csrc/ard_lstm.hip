@@ -259,6 +259,71 @@ __global__ void __launch_bounds__(256) lstm_fwd_step_kernel(LstmStep s) {
   s.Hs[(static_cast<int64_t>(s.t) * s.H + unit_row(s.idx, u)) * s.B + col] = h;
 }
 
+// The same forward step on the direct-load pipeline: 32 gate rows x 32
+// samples, the four waves splitting each slab's k; after the LDS reduction
+// wave w holds the four gates of units r0 / 4 + 2 w + lane / 32. Needs
+// 16-byte aligned rows (I, KW and B multiples of 4).
+using StepCfg = FastCfg<float, 32, 32, 64, 4, 1, 1, 4>;  // 64 KB LDS
+
+__global__ void __launch_bounds__(StepCfg::NT) lstm_fwd_step_fast_kernel(LstmStep s) {
+  using Cfg = StepCfg;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int r0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  f32x16 acc[1][1];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[0][0][r] = 0.0f;
+  const int nslab = (s.ns + Cfg::BK - 1) / Cfg::BK;
+  SlabLoader<Cfg, false, true> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(w);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  ld.da.init(s.KW, r0, s.G4, ld.wv);
+  ld.db.init(s.B, n0, s.B, ld.wv);
+  ld.K = s.ns;
+  ld.ik = 0;
+  ld.is = 0;
+  ld.left = nslab - 1;
+  ld.a_step = Cfg::BK * 4;
+  ld.b_step = static_cast<int64_t>(s.B) * Cfg::BK * 4;
+  ld.a_wrap = 0;
+  ld.b_wrap = 0;
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B));
+  run_slabs<Cfg, false, true, true>(ld, nslab, s.ns, 0, acc, 0, 0, w * Cfg::KW, smem);
+  // wave v's registers 4 w' .. 4 w' + 3 (rows 8 w' + 4 (lane / 32) + q) go to wave w'
+  float* red = reinterpret_cast<float*>(smem);
+  lds_barrier();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) red[(w * 16 + r) * 64 + lane] = acc[0][0][r];
+  lds_barrier();
+  float z[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float v = 0.0f;
+#pragma unroll
+    for (int u = 0; u < Cfg::KSPLIT; ++u) v += red[(u * 16 + 4 * w + q) * 64 + lane];
+    z[q] = v;
+  }
+  const int64_t u = r0 / 4 + 2 * w + (lane >> 5);
+  const int64_t col = n0 + (lane & 31);
+  if (u >= s.ns || col >= s.B) return;
+  float* Zt = s.Z + static_cast<int64_t>(s.t) * s.G4 * s.B;
+  float gate[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) gate[q] = z[q] + Zt[(4 * u + q) * s.B + col];
+  const float ig = sigm(gate[0]), fg = sigm(gate[1]), gg = tanhf(gate[2]), og = sigm(gate[3]);
+  const float cp = s.Cc[(static_cast<int64_t>(s.t) * s.ns + u) * s.B + col];
+  const float c = fg * cp + ig * gg;
+  const float h = og * tanhf(c);
+  Zt[(4 * u + 0) * s.B + col] = ig;
+  Zt[(4 * u + 1) * s.B + col] = fg;
+  Zt[(4 * u + 2) * s.B + col] = gg;
+  Zt[(4 * u + 3) * s.B + col] = og;
+  s.Cc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = c;
+  s.Hc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = h;
+  s.Hs[(static_cast<int64_t>(s.t) * s.H + unit_row(s.idx, u)) * s.B + col] = h;
+}
+
 // Pointwise backward of step t for unit u, sample b, given dL/dh_t.
 __device__ __forceinline__ void lstm_point_bwd(const LstmStep& s, int t, int64_t u, int64_t b, float dh) {
   const float* Zt = s.Z + static_cast<int64_t>(t) * s.G4 * s.B;
@@ -461,9 +526,19 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
 
   const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((L.G4 + 31) / 32));
   const bool avec = kw_vec && L.I % 4 == 0, bvec = L.B % 4 == 0;
+  // direct loads: aligned rows, and every chunk offset of a slab below 2^31 bytes
+  const bool step_fast = avec && bvec && aligned16(s.Wc) &&
+                         (L.G4 + 1) * L.KW * 4 < (int64_t{1} << 31) && (L.ns + 64) * L.B * 4 < (int64_t{1} << 31);
+  if (step_fast) {
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(lstm_fwd_step_fast_kernel),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, StepCfg::LDS);
+    ARD_HIP_CHECK(attr);
+  }
   for (int t = 0; t < L.T; ++t) {
     s.t = t;
-    if (avec && bvec)
+    if (step_fast)
+      hipLaunchKernelGGL(lstm_fwd_step_fast_kernel, sgrid, dim3(StepCfg::NT), StepCfg::LDS, sm, s);
+    else if (avec && bvec)
       hipLaunchKernelGGL((lstm_fwd_step_kernel<true, true>), sgrid, dim3(256), 0, sm, s);
     else
       hipLaunchKernelGGL((lstm_fwd_step_kernel<false, false>), sgrid, dim3(256), 0, sm, s);

@@ -69,7 +69,7 @@ def hazards(lines):
 
 
 @pytest.mark.skipif(not all(os.path.exists(t) for t in TOOLS), reason="ROCm LLVM tools not found")
-@pytest.mark.parametrize("src", ["ard_fc.hip", "ard_tile.hip"])
+@pytest.mark.parametrize("src", ["ard_fc.hip", "ard_tile.hip", "ard_lstm.hip"])
 def test_direct_load_wait_states(tmp_path, src):
     obj = os.path.join(BUILD, src + ".o")
     if not os.path.exists(obj):
