@@ -111,7 +111,7 @@ def test_tiny_all_pattern_pairs(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("shape", [(200, 300, 260), (130, 1000, 70), (64, 96, 520), (8, 4104, 36)])
+@pytest.mark.parametrize("shape", [(200, 300, 260), (130, 1000, 70), (64, 96, 520), (8, 4104, 36), (1, 130, 70)])
 def test_multi_tile_ragged(dtype, shape):
     B, K, N = shape
     X, W, b, dY = make_inputs(dtype, B, K, N, seed=sum(shape))
