@@ -666,6 +666,15 @@ def main():
         wl.host_copies()  # the oracle's inputs, taken before any GPU timing: the replay below is the last GPU work
 
     rates = sorted({0.0, 0.3, 0.5, 0.7, args.p})
+    # Alg. 1 on the host, once per rate (a one-time cost, outside the timed steps)
+    from paper_1805_08939_amd import api
+    k_search = {}
+    for p in rates:
+        t_s = time.perf_counter()
+        _, info = api.ard_search_distribution(p)
+        k_search[f"{p}"] = {"ms": (time.perf_counter() - t_s) * 1e3, "iters": int(info.iters),
+                            "loss": float(info.loss), "p_global": float(info.p_global),
+                            "converged": bool(info.converged)}
     results = {}
     for i, p in enumerate(rates):
         wl.set_rate(p)
@@ -724,6 +733,7 @@ def main():
                            "tflops_kept": results[p]["flops"] / (results[p]["ms"] * 1e-3) / 1e12}
                   for p in rates},
         "roofline": roofline,
+        "k_search": k_search,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.p, args.cpu_budget)
