@@ -6,6 +6,8 @@
 // weights once per sequence into the workspace:
 //   Wc[4u + g][c] = W[g*H + S(u)][c]          for input columns c < I
 //   Wc[4u + g][I + v] = W[g*H + S(u)][I + S(v)]  for recurrent columns
+// with rows padded with zeros to a multiple of 4 entries (16-byte rows for
+// the direct-load GEMMs whatever |S| is)
 // Rows are unit-major (4u + g, g = i, f, g, o), so in the 32x32 MFMA
 // accumulator layout each lane holds the four gates of one unit in four
 // consecutive registers, and the cell update runs in registers.
@@ -58,7 +60,7 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
   L.H = d->hidden_size;
   L.ns = ns;
   L.G4 = 4 * static_cast<int64_t>(ns);
-  L.KW = L.I + ns;
+  L.KW = (L.I + ns + 3) / 4 * 4;  // compact rows padded to 16 bytes (zeros past I + |S|)
   L.S = bwd_splits(ns, L.B);
   size_t off = 0;
   L.wc = off;     off += al256(4 * L.G4 * L.KW);
@@ -79,18 +81,19 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
 __device__ __forceinline__ int64_t unit_row(const int32_t* idx, int64_t u) { return idx ? idx[u] : u; }
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
 
-// Compact weights, bias and row map; one block per compact row 4u + g.
+// Compact weights (rows of KW >= I + |S| entries, zero past I + |S|), bias
+// and row map; one block per compact row 4u + g.
 __global__ void lstm_prepare_kernel(const float* __restrict__ W, const float* __restrict__ bias,
                                     const int32_t* __restrict__ idx, int32_t I, int32_t H, int32_t ns,
-                                    float* __restrict__ Wc, float* __restrict__ bc,
+                                    int32_t KW, float* __restrict__ Wc, float* __restrict__ bc,
                                     int32_t* __restrict__ rowmap) {
   const int r = blockIdx.x;
   const int u = r >> 2, g = r & 3;
   const int64_t src = static_cast<int64_t>(g) * H + unit_row(idx, u);
   const float* wrow = W + src * (I + H);
-  float* crow = Wc + static_cast<int64_t>(r) * (I + ns);
-  for (int c = threadIdx.x; c < I + ns; c += blockDim.x)
-    crow[c] = c < I ? wrow[c] : wrow[I + unit_row(idx, c - I)];
+  float* crow = Wc + static_cast<int64_t>(r) * KW;
+  for (int c = threadIdx.x; c < KW; c += blockDim.x)
+    crow[c] = c < I ? wrow[c] : c < I + ns ? wrow[I + unit_row(idx, c - I)] : 0.0f;
   if (threadIdx.x == 0) {
     bc[r] = bias ? bias[src] : 0.0f;
     rowmap[r] = static_cast<int32_t>(src);
@@ -497,7 +500,7 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   }
 
   hipLaunchKernelGGL(lstm_prepare_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm,
-                     static_cast<const float*>(W), bias, idx, s.I, s.H, ns, const_cast<float*>(s.Wc),
+                     static_cast<const float*>(W), bias, idx, s.I, s.H, ns, s.KW, const_cast<float*>(s.Wc),
                      reinterpret_cast<float*>(w + L.bc), reinterpret_cast<int32_t*>(w + L.rowmap));
   ARD_LAUNCH_CHECK();
   const int64_t nsB = static_cast<int64_t>(ns) * L.B;
