@@ -372,10 +372,16 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
+  bool dbias_done = false;
   if (fast_ok(g, sizeof(T))) {
     g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
                       d->scale, nullptr);
-    ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD>(g, 1, stream, partial)));
+    // dbias = scale * G 1: the row sums of A, taken by the same kernel
+    if (dbias) {
+      g.rsum = dbias + s.out_offset;
+      g.rsum_ld = s.out_period;
+    }
+    ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD, true>(g, 1, stream, partial, &dbias_done)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
         g, 1, v, v, stream, partial)));
@@ -383,7 +389,7 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
     ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
         g, 1, v, v, stream, partial)));
   }
-  if (dbias && s.kout > 0) {
+  if (dbias && s.kout > 0 && !dbias_done) {
     const int vec = aligned16(dYt) && (!gated || aligned16(Yt)) &&
                     (static_cast<int64_t>(s.B) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
     hipLaunchKernelGGL(dbias_kernel<T>, dim3((s.kout + 3) / 4), dim3(256), 0, stream,

@@ -89,6 +89,10 @@ __device__ __forceinline__ int64_t bias_row(const GemmOutput& c, int64_t m) {
 // is a plain GEMM. splits > 1 divides the kbatch x ceil(K / BK) slabs over
 // that many workgroups per output tile; `partial` then receives
 // [batch][splits][M][N] fp32 sums for the reduction kernel.
+// rsum, when set (fast kernel with a k-contiguous A and no split only), also
+// receives c.scale times the sum of row m of A over the whole contraction at
+// rsum[bz * rsum_bstride + m * rsum_ld]: a bias gradient taken from the A
+// operand of the weight-gradient product that reads it anyway.
 struct GemmArgs {
   int32_t M, N, K;
   GemmOperand a, b;
@@ -96,6 +100,8 @@ struct GemmArgs {
   int32_t kbatch;
   int32_t splits;
   float* partial;
+  float* rsum;
+  int64_t rsum_ld, rsum_bstride;
 };
 
 template <typename T>

@@ -328,6 +328,19 @@ struct StepFrags {
     }
   }
 
+  // Adds the A values of this k step to per-lane row sums: with a
+  // k-contiguous A, lane l holds k values of row rb + l % 32 only.
+  __device__ __forceinline__ void rowsum(float (&rs)[Cfg::FM]) const {
+    static_assert(!AMC, "row sums need a k-contiguous A");
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i) {
+      float v = 0.0f;
+#pragma unroll
+      for (int e = 0; e < (Cfg::ES == 2 ? 8 : 4); ++e) v += static_cast<float>(a[i][e]);
+      rs[i] += v;
+    }
+  }
+
   __device__ __forceinline__ void mma(f32x16 (&acc)[Cfg::FM][Cfg::FN]) const {
     if constexpr (Cfg::ES == 2) {
 #pragma unroll
@@ -406,10 +419,12 @@ __device__ __forceinline__ void grouped_tile(int bid, int nx, int ny, int& row, 
 // current one, so LDS latency and the barrier overlap MFMA execution.
 // With TAIL, ck is the first k of the first slab within a contraction of
 // length K (slabs wrap to k 0 past K), and a slab with fewer than BK valid k
-// is zeroed past them in LDS before use. Returns with no direct load in flight.
-template <class Cfg, bool AMC, bool BMC, bool TAIL, class Loader>
+// is zeroed past them in LDS before use. With RSUM, rs[i] also sums the A
+// values the lane reads (StepFrags::rowsum). Returns with no direct load in
+// flight.
+template <class Cfg, bool AMC, bool BMC, bool TAIL, bool RSUM = false, class Loader>
 __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, f32x16 (&acc)[Cfg::FM][Cfg::FN],
-                                          int wm, int wn, int kw0, char* smem) {
+                                          int wm, int wn, int kw0, char* smem, float* rs = nullptr) {
   using Frags = StepFrags<Cfg, AMC, BMC>;
   constexpr int STEPS = Cfg::KW / Frags::KSTEP;
   static_assert(STEPS % 2 == 0, "a slab holds an even number of k steps");
@@ -453,6 +468,7 @@ __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, 
         fr[(s + 1) & 1].load(st, wm, wn, kw0);
       }
       fr[s & 1].mma(acc);
+      if constexpr (RSUM) fr[s & 1].rowsum(*reinterpret_cast<float(*)[Cfg::FM]>(rs));
     }
   }
   if (nslab > 0) {  // the last slab (a separate copy keeps the loop body's LDS waits exact)
@@ -460,6 +476,7 @@ __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, 
     for (int s = 0; s < STEPS; ++s) {
       if (s + 1 < STEPS) fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
       fr[s & 1].mma(acc);
+      if constexpr (RSUM) fr[s & 1].rowsum(*reinterpret_cast<float(*)[Cfg::FM]>(rs));
     }
   }
   wait_vm<0>();  // no direct load may still write LDS past this point
@@ -566,7 +583,10 @@ __device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg:
   }
 }
 
-template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
+// Row sums of A (RSUM, see GemmArgs::rsum) for the tile row of a workgroup
+// in tile column 0: lanes l and l + 32 of a wave hold the two k halves of
+// row 32 i + l % 32, the waves of a k split are added in LDS in split order.
+template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   using T = typename Cfg::T;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -621,8 +641,25 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   ld.left = q1 - q0 - 1;
   ld.na = uniform_ptr(reinterpret_cast<const char*>(abase) + (ib * g.a.kbstride) * ES + ld.ik / Cfg::BK * ld.a_step);
   ld.nb = uniform_ptr(reinterpret_cast<const char*>(bbase) + (ib * g.b.kbstride) * ES + ld.ik / Cfg::BK * ld.b_step);
-  run_slabs<Cfg, AMC, BMC, true>(ld, q1 - q0, g.K, ld.ik, acc, wm, wn, ks * Cfg::KW, smem);
+  float rs[Cfg::FM];
+#pragma unroll
+  for (int i = 0; i < Cfg::FM; ++i) rs[i] = 0.0f;
+  run_slabs<Cfg, AMC, BMC, true, RSUM>(ld, q1 - q0, g.K, ld.ik, acc, wm, wn, ks * Cfg::KW, smem, rs);
+  const int rlane = threadIdx.x & 63;
+  if constexpr (RSUM) {
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i) rs[i] += __shfl_xor(rs[i], 32);
+  }
+  const bool rs_out = RSUM && splits == 1 && tile_col == 0 && wn == 0 && rlane < 32;
+  auto put_rsum = [&](int i, float v) {
+    const int m = m0 + wm * Cfg::TM + 32 * i + rlane;
+    if (m < g.M) g.rsum[bz * g.rsum_bstride + static_cast<int64_t>(m) * g.rsum_ld] = g.c.scale * v;
+  };
   if constexpr (Cfg::KSPLIT == 1) {
+    if (rs_out) {
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) put_rsum(i, rs[i]);
+    }
     fast_store<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split, smem);
   } else {
     // the KSPLIT waves of one output tile reduce through LDS; wave ks finishes
@@ -639,7 +676,27 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           red[((ks * Cfg::WGM * Cfg::WGN + wmn) * NREG + (i * Cfg::FN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    // row sums of the k splits after the accumulators: [KSPLIT][WGM][FM][32]
+    float* rred = red + Cfg::KSPLIT * Cfg::WGM * Cfg::WGN * NREG * 64;
+    if constexpr (RSUM) {
+      static_assert((Cfg::KSPLIT * Cfg::WGM * Cfg::WGN * NREG * 64 + Cfg::KSPLIT * Cfg::WGM * Cfg::FM * 32) * 4 <=
+                        Cfg::LDS,
+                    "row-sum buffer exceeds LDS");
+      if (wn == 0 && lane < 32) {
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i) rred[((ks * Cfg::WGM + wm) * Cfg::FM + i) * 32 + lane] = rs[i];
+      }
+    }
     __syncthreads();
+    if (rs_out && ks == 0) {
+#pragma unroll
+      for (int i = 0; i < Cfg::FM; ++i) {
+        float v = 0.0f;
+#pragma unroll
+        for (int u = 0; u < Cfg::KSPLIT; ++u) v += rred[((u * Cfg::WGM + wm) * Cfg::FM + i) * 32 + lane];
+        put_rsum(i, v);
+      }
+    }
     const int lr = lane & 31, lh = lane >> 5;
 #pragma unroll
     for (int t = ks; t < NREG; t += Cfg::KSPLIT) {
@@ -803,10 +860,10 @@ inline size_t fast_partial_floats(int M, int N, int K, int kbatch, int batch) {
   return p.splits > 1 ? static_cast<size_t>(p.splits) * batch * M * N : 0;
 }
 
-template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI>
+template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
 inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) {
   const int splits = g.splits > 1 ? g.splits : 1;
-  auto kern = fast_gemm_kernel<Cfg, AMC, BMC, OutT, EPI>;
+  auto kern = fast_gemm_kernel<Cfg, AMC, BMC, OutT, EPI, RSUM>;
   // per instantiation, once (thread-safe static initialisation): allow more than 64 KB of dynamic LDS
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
@@ -821,27 +878,41 @@ inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) 
   return hipGetLastError();
 }
 
-// Runs a GEMM on the fast kernel; the caller has checked fast_ok().
-template <typename T, bool AMC, bool BMC, typename OutT, int EPI>
-inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float* partial) {
+template <typename T, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM>
+inline hipError_t launch_planned(const GemmArgs& g, int kind, int batch, hipStream_t stream) {
+  using C = FastCfgs<T>;
+  switch (kind) {
+    case FAST_HUGE:
+      return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+    case FAST_WIDE:
+      return launch_fast<typename C::Wide, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+    case FAST_TALL:
+      return launch_fast<typename C::Tall, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+    case FAST_BIG:
+      return launch_fast<typename C::Big, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+    default:
+      return launch_fast<typename C::Small, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+  }
+}
+
+// Runs a GEMM on the fast kernel; the caller has checked fast_ok(). With
+// RSUM, g.rsum receives the row sums of A when the plan has no k split, and
+// *rsum_done says whether it did (else the caller computes them itself).
+template <typename T, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
+inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float* partial,
+                                bool* rsum_done = nullptr) {
+  if (rsum_done) *rsum_done = false;
   if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
   FastPlan p = plan_fast<T>(g.M, g.N, g.K, g.kbatch, batch);
   if (!partial) p.splits = 1;
   g.splits = p.splits;
   g.partial = partial;
-  using C = FastCfgs<T>;
-  switch (p.kind) {
-    case FAST_HUGE:
-      return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI>(g, batch, stream);
-    case FAST_WIDE:
-      return launch_fast<typename C::Wide, AMC, BMC, OutT, EPI>(g, batch, stream);
-    case FAST_TALL:
-      return launch_fast<typename C::Tall, AMC, BMC, OutT, EPI>(g, batch, stream);
-    case FAST_BIG:
-      return launch_fast<typename C::Big, AMC, BMC, OutT, EPI>(g, batch, stream);
-    default:
-      return launch_fast<typename C::Small, AMC, BMC, OutT, EPI>(g, batch, stream);
+  if (RSUM && g.rsum && p.splits == 1) {
+    if (rsum_done) *rsum_done = true;
+    return launch_planned<T, AMC, BMC, OutT, EPI, RSUM>(g, p.kind, batch, stream);
   }
+  g.rsum = nullptr;
+  return launch_planned<T, AMC, BMC, OutT, EPI, false>(g, p.kind, batch, stream);
 }
 
 }  // namespace ard

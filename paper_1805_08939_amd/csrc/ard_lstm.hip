@@ -661,18 +661,21 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     ARD_LAUNCH_CHECK();
   }
 
+  // rowmap: built when a product below scatters through it
   int32_t* rowmap = reinterpret_cast<int32_t*>(w + L.rowmap);
-  if ((dW || dbias) && L.G4 > 0) {
+  auto build_rowmap = [&]() -> hipError_t {
+    if (L.G4 <= 0) return hipSuccess;
     hipLaunchKernelGGL(lstm_rowmap_kernel, grid1d(L.G4, 256), dim3(256), 0, sm, idx, static_cast<int32_t>(L.H),
                        static_cast<int32_t>(L.G4), rowmap);
-    ARD_LAUNCH_CHECK();
-  }
+    return hipGetLastError();
+  };
+  bool rowmap_built = false;
   const bool bv = L.B % 4 == 0;
   // Per gate q the compact rows 4u + q of dA are every fourth row, and the
   // output rows q H + S(u) and recurrent columns I + S(v) of a row pattern are
   // strided views of dW: the weight gradient runs as four plain strided
   // GEMMs (one launch, batched over the gates) when the operands allow.
-  bool dw_done = false;
+  bool dw_done = false, dbias_done = false;
   if (dW) {
     GemmArgs g = {};
     g.M = ns;
@@ -689,13 +692,21 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     gr.c.p = dW + static_cast<int64_t>(offset) * colsW + L.I + offset;
     gr.c.col_stride = period;
     if (fast_ok(g, sizeof(float)) && fast_ok(gr, sizeof(float))) {
-      ARD_HIP_CHECK((run_fast_gemm<float, false, false, float, EPI_FWD>(g, 4, sm, nullptr)));
+      // dbias[q H + S(u)] = sum over t, b of dA: the row sums of the first product's A
+      if (dbias) {
+        g.rsum = dbias + offset;
+        g.rsum_ld = period;
+        g.rsum_bstride = L.H;
+      }
+      ARD_HIP_CHECK((run_fast_gemm<float, false, false, float, EPI_FWD, true>(g, 4, sm, nullptr, &dbias_done)));
       ARD_HIP_CHECK((run_fast_gemm<float, false, false, float, EPI_FWD>(gr, 4, sm, nullptr)));
       dw_done = true;
     }
   }
   if (dW && !dw_done) {
     // dW[rowmap][:I] = sum_t dA[t] X[t]^T ; dW[rowmap][I + S] = sum_t dA[t] Hc[t]^T
+    ARD_HIP_CHECK(build_rowmap());
+    rowmap_built = true;
     GemmArgs g = {};
     g.M = static_cast<int32_t>(L.G4);
     g.N = s.I;
@@ -712,7 +723,8 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
         g, 1, bv, bv, sm)));
   }
-  if (dbias) {
+  if (dbias && !dbias_done) {
+    if (!rowmap_built) ARD_HIP_CHECK(build_rowmap());
     hipLaunchKernelGGL(lstm_dbias_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm, s.dA, rowmap,
                        static_cast<int32_t>(L.T), static_cast<int32_t>(L.G4), s.B, dbias);
     ARD_LAUNCH_CHECK();

@@ -200,6 +200,25 @@ def test_bf16_large_tiles(shape, pin, pout):
     run_layer("bf16", X, W, b, dY, pin, pout, "none", 2.0, api.ARD_DROPPED_ZERO)
 
 
+@pytest.mark.parametrize("dtype,B,K,N,pout", [
+    ("f32", 128, 1024, 1024, (1, 0)),   # 64x64 tiles: one wave per output block, no k split
+    ("f32", 96, 2048, 2048, (3, 1)),    # 128x128 tiles
+    ("f32", 256, 300, 260, (2, 1)),     # 32x32 tiles, k split over 8 waves, ragged rows
+    ("f32", 8192, 64, 72, (1, 0)),      # contraction split over workgroups: separate bias kernel
+    ("bf16", 256, 1024, 2048, (5, 4)),  # large bf16 tiles
+    ("bf16", 128, 96, 100, (1, 0)),     # bf16 32x32 tiles, k split over 4 waves
+    ("bf16", 4096, 64, 64, (2, 0)),     # bf16 split contraction
+])
+def test_bias_gradient_with_the_weight_gradient(dtype, B, K, N, pout):
+    """dbias of an ungated layer comes from the row sums of the weight-gradient
+    product's first operand on every tile configuration without a k split,
+    and from its own kernel otherwise; both against the oracle."""
+    X, W, b, dY = make_inputs(dtype, B, K, N, seed=B + N)
+    run_layer(dtype, X, W, b, dY, (1, 0), pout, "none", 1.5, api.ARD_DROPPED_ZERO, use_null_plans=False)
+    run_layer(dtype, X, W, b, dY, (1, 0), pout, "none", 1.0, api.ARD_DROPPED_SKIP, use_null_plans=False,
+              sentinel=-2.0)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_pregated_gradient_and_input_gate(dtype):
     """Yt = NULL takes dYt as already gated; Xgate gates dXt with [Xgate > 0]."""
