@@ -329,15 +329,24 @@ struct StepFrags {
   }
 
   // Adds the A values of this k step to per-lane row sums: with a
-  // k-contiguous A, lane l holds k values of row rb + l % 32 only.
+  // k-contiguous A, lane l holds k values of row rb + l % 32 only. bf16 pairs
+  // go through v_dot2 against (1, 1), which needs no unpacked temporaries
+  // (the 256x256 tile has no registers to spare).
   __device__ __forceinline__ void rowsum(float (&rs)[Cfg::FM]) const {
     static_assert(!AMC, "row sums need a k-contiguous A");
 #pragma unroll
     for (int i = 0; i < Cfg::FM; ++i) {
-      float v = 0.0f;
+      if constexpr (Cfg::ES == 2) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 one = {static_cast<bf16>(1.0f), static_cast<bf16>(1.0f)};
 #pragma unroll
-      for (int e = 0; e < (Cfg::ES == 2 ? 8 : 4); ++e) v += static_cast<float>(a[i][e]);
-      rs[i] += v;
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 pr = {a[i][2 * e], a[i][2 * e + 1]};
+          rs[i] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, rs[i], false);
+        }
+      } else {
+        rs[i] += (a[i][0] + a[i][1]) + (a[i][2] + a[i][3]);
+      }
     }
   }
 
@@ -883,7 +892,9 @@ inline hipError_t launch_planned(const GemmArgs& g, int kind, int batch, hipStre
   using C = FastCfgs<T>;
   switch (kind) {
     case FAST_HUGE:
-      return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+      // the bf16 256x256 tile has no registers left for row sums (it spills)
+      if constexpr (RSUM && sizeof(T) == 2) return hipErrorNotSupported;
+      else return launch_fast<typename C::Huge, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
     case FAST_WIDE:
       return launch_fast<typename C::Wide, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
     case FAST_TALL:
@@ -896,8 +907,9 @@ inline hipError_t launch_planned(const GemmArgs& g, int kind, int batch, hipStre
 }
 
 // Runs a GEMM on the fast kernel; the caller has checked fast_ok(). With
-// RSUM, g.rsum receives the row sums of A when the plan has no k split, and
-// *rsum_done says whether it did (else the caller computes them itself).
+// RSUM, g.rsum receives the row sums of A when the plan has no k split and is
+// not the bf16 256x256 tile, and *rsum_done says whether it did (else the
+// caller computes them itself).
 template <typename T, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
 inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float* partial,
                                 bool* rsum_done = nullptr) {
@@ -907,7 +919,7 @@ inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float
   if (!partial) p.splits = 1;
   g.splits = p.splits;
   g.partial = partial;
-  if (RSUM && g.rsum && p.splits == 1) {
+  if (RSUM && g.rsum && p.splits == 1 && !(sizeof(T) == 2 && p.kind == FAST_HUGE)) {
     if (rsum_done) *rsum_done = true;
     return launch_planned<T, AMC, BMC, OutT, EPI, RSUM>(g, p.kind, batch, stream);
   }

@@ -324,3 +324,64 @@ def test_wide_layer_full_size_sampled(dtype, B, K, N, pats):
             np.abs(G[:, Sout]).T @ (np.abs(Xf[:, Sin]) @ np.abs(u[Sin])), tol(dtype), "dW projection")
     dropped_rows = np.setdiff1d(np.arange(N), Sout)[:64]
     assert not Yg[dropped_rows].any() and not dWg[dropped_rows].any()
+
+
+@pytest.mark.parametrize("B,K,N,pin,pout", [
+    (128, 784, 2048, (2, 1), (2, 0)),     # 32x32 tiles (fwd and bwd_data), K tail
+    (512, 1000, 2600, (3, 1), (2, 1)),    # 64x64 tiles (fwd), ragged
+    (1024, 5120, 2600, (2, 1), (2, 0)),   # 64x64 (fwd) and 128x128 tiles (bwd_data)
+    (1024, 1536, 5200, (5, 3), (2, 1)),   # 128x128 tiles (fwd)
+], ids=["t32", "t64", "t128-bwd", "t128-fwd"])
+def test_fp32_full_weights_with_input_gather(B, K, N, pin, pout):
+    """fp32 layers given the full W with a gathered input side (the compact
+    copy built in the workspace): fwd and the pre-gated bwd_data with an input
+    gate on every fp32 tile configuration, against the oracle on sampled
+    neurons over the whole batch and on sampled batch entries over every
+    output tile. Dropped input columns of W hold NaN and are never read."""
+    g = synth.generator(K + N)
+    X = torch.relu(synth.normal(g, (B, K)))
+    W = synth.normal(g, (N, K), 0.05)
+    b = synth.normal(g, (N,), 0.1)
+    dY = synth.normal(g, (B, N))
+    (pi, oi), (po, oo) = pin, pout
+    m_in, m_out = opat.row_mask(K, pi, oi), opat.row_mask(N, po, oo)
+    in_plan, out_plan = row_plan(K, pi, oi), row_plan(N, po, oo)
+    args = (api.ARD_F32, B, K, N, in_plan, out_plan, 1.0, api.ARD_ACT_RELU, api.ARD_DROPPED_ZERO)
+    desc = api.fc_desc(*args)
+    ws = workspace(api.ard_fc_workspace_bytes(desc))
+    Xt, Wd, dYt, bd = to_dev(X.T), to_dev(W), to_dev(dY.T), to_dev(b)
+    Wd[:, torch.from_numpy(m_in == 0).to(device())] = float("nan")  # dropped columns are never read
+    Yt = torch.full((N, B), 5.0, device=device())
+    dXt = torch.full((K, B), 5.0, device=device())
+    api.ard_fc_fwd(desc, Xt, Wd, bd, Yt, ws)
+    api.ard_fc_bwd_data(desc, dYt, None, Wd, dXt, ws, Xgate=Xt)
+    torch.cuda.synchronize()
+    Xf, Wf, bf, dYf = f64(X), f64(W), f64(b), f64(dY)
+    Sin, Sout = np.array(opat.row_kept_list(K, pi, oi)), np.array(opat.row_kept_list(N, po, oo))
+    rng = np.random.default_rng(5)
+    rows = np.sort(rng.choice(Sout, min(48, len(Sout)), replace=False))
+    cols = np.sort(rng.choice(Sin, min(48, len(Sin)), replace=False))
+    bs = np.sort(rng.choice(B, 16, replace=False))
+    Yg, dXg = f64(Yt).T, f64(dXt).T
+    Xa, Wa = np.abs(Xf * m_in[None, :]), np.abs(Wf)
+
+    def dx_oracle(xs, ws_cols, dys, mi):
+        # the oracle's bwd_data of the pre-gated gradient, then the ReLU gate of the layer below
+        dX = ofc.fc_backward(xs, ws_cols, None, dys, mi, m_out, 1.0, "none")[0]
+        return ofc.fc_output_grad(xs, dX, np.ones(dX.shape[1]), 1.0, "relu")
+
+    # sampled neurons over the whole batch
+    compare(Yg[:, rows], ofc.fc_forward(Xf, Wf[rows], bf[rows], m_in, m_out[rows], 1.0, "relu"),
+            Xa @ Wa[rows].T + np.abs(bf[rows])[None, :], tol("f32"), "Y rows")
+    Wo = Wa * m_out[:, None]
+    compare(dXg[:, cols], dx_oracle(Xf[:, cols], Wf[:, cols], dYf, m_in[cols]),
+            np.abs(dYf) @ Wo[:, cols], tol("f32"), "dX cols")
+    # sampled batch entries over every output tile
+    keep_out, keep_in = m_out > 0, m_in > 0
+    compare(Yg[bs][:, keep_out], ofc.fc_forward(Xf[bs], Wf, bf, m_in, m_out, 1.0, "relu")[:, keep_out],
+            (Xa[bs] @ Wa.T + np.abs(bf)[None, :])[:, keep_out], tol("f32"), "Y batch rows")
+    compare(dXg[bs][:, keep_in], dx_oracle(Xf[bs], Wf, dYf[bs], m_in)[:, keep_in],
+            (np.abs(dYf[bs]) @ Wo)[:, keep_in], tol("f32"), "dX batch rows")
+    Yg, dXg = Yg.T, dXg.T
+    assert not Yg[np.setdiff1d(np.arange(N), Sout)].any() and not dXg[np.setdiff1d(np.arange(K), Sin)].any()
+

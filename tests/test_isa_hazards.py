@@ -90,3 +90,34 @@ def test_checker_flags_a_short_gap():
     assert len(hazards(short)[1]) == 1
     assert hazards(ok)[1] == []
     assert len(hazards(nomo)[1]) == 1
+
+
+def _kernel_notes(obj, tmp_path):
+    fat, code = tmp_path / "fatbin", tmp_path / "code"
+    subprocess.run([TOOLS[0], f"--dump-section=.hip_fatbin={fat}", obj, str(tmp_path / "host.o")], check=True)
+    subprocess.run([TOOLS[1], "--type=o", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", f"--input={fat}",
+                    f"--output={code}", "--unbundle"], check=True)
+    readobj = os.path.join(LLVM, "llvm-readobj")
+    return subprocess.run([readobj, "--notes", str(code)], check=True, capture_output=True, text=True).stdout
+
+
+@pytest.mark.skipif(not all(os.path.exists(t) for t in TOOLS + [os.path.join(LLVM, "llvm-readobj")]),
+                    reason="ROCm LLVM tools not found")
+@pytest.mark.parametrize("src", ["ard_fc.hip", "ard_tile.hip", "ard_lstm.hip"])
+def test_no_kernel_spills_registers(tmp_path, src):
+    """A VGPR spill goes to scratch memory, and inside a GEMM main loop it
+    costs more than the kernel's arithmetic: every kernel of the library must
+    fit its vector registers (SGPR spills land in VGPR lanes and are cheap)."""
+    obj = os.path.join(BUILD, src + ".o")
+    if not os.path.exists(obj):
+        pytest.skip("library objects not built")
+    notes = _kernel_notes(obj, tmp_path)
+    kernels = re.findall(r"\.name:\s+(\S+)(.*?)(?=\n  - |\Z)", notes, re.S)
+    assert kernels, "no kernel metadata found"
+    bad = []
+    for name, body in kernels:
+        m = re.search(r"\.vgpr_spill_count:\s+(\d+)", body)
+        if m and int(m.group(1)) > 0:
+            bad.append(f"{name}: vgpr_spill_count {m.group(1)}")
+    assert not bad, "\n".join(bad)
+
