@@ -606,9 +606,13 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   int32_t ks = static_cast<int32_t>(((L.G4 + L.S - 1) / L.S + 63) / 64 * 64);  // whole slabs per split
   int32_t splits = static_cast<int32_t>((L.G4 + ks - 1) / ks);
   float* part = reinterpret_cast<float*>(w + L.part);
-  int32_t fs = 0;  // exact split count for the direct-load GEMM, 0 = none
+  // exact split count for the direct-load GEMM (0 = none): its 32 x 32 tiles
+  // run one workgroup per compute unit, so the splits stop at one round of
+  // 256 workgroups (a second, partial round costs more than longer splits)
+  const int64_t rtiles = ((ns + 31) / 32) * ((L.B + 31) / 32);
+  int32_t fs = 0;
   for (int32_t d = static_cast<int32_t>(L.S); d >= 1; --d)
-    if (L.G4 % d == 0 && L.G4 / d >= 256) {
+    if (L.G4 % d == 0 && L.G4 / d >= 256 && (d == 1 || rtiles * d <= 256)) {
       fs = d;
       break;
     }
