@@ -445,6 +445,47 @@ __global__ void __launch_bounds__(Cfg::NT) gemm_kernel(GemmArgs g) {
   store_tile<OutT, Cfg, EPI>(g, acc, m0, n0, wm, wn, bz, split);
 }
 
+// The same for 4 consecutive elements of one output row per thread (N a
+// multiple of 4, output columns contiguous, output, gate and partial rows 4-
+// element aligned): 16-byte partial loads, 32-bit index arithmetic (M N <
+// 2^31), one vector store.
+template <typename OutT, int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce4_kernel(GemmArgs g) {
+  const int32_t mn = g.M * g.N;
+  const int32_t e = (static_cast<int32_t>(blockIdx.x) * 256 + static_cast<int32_t>(threadIdx.x)) * 4;
+  if (e >= mn) return;
+  const int64_t bz = blockIdx.y;
+  const float* part = g.partial + bz * g.splits * static_cast<int64_t>(mn) + e;
+  f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s = 0; s < g.splits; ++s) v += *reinterpret_cast<const f32x4*>(part + static_cast<int64_t>(s) * mn);
+  const int32_t m = e / g.N, n = e - m * g.N;
+  const float bias = (EPI == EPI_FWD && g.c.bias) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
+  const int64_t o = bz * g.c.bstride + static_cast<int64_t>(m) * g.c.ld + n;
+  OutT w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float x = epilogue<EPI>(g.c, v[i], bias);
+    if (EPI == EPI_FWD && g.c.gate && !(to_f32(static_cast<const OutT*>(g.c.gate)[o + i]) > 0.0f)) x = 0.0f;
+    w[i] = from_f32<OutT>(x);
+  }
+  OutT* out = static_cast<OutT*>(g.c.p) + o;
+  if constexpr (sizeof(OutT) == 2)
+    *reinterpret_cast<uint2*>(out) = *reinterpret_cast<const uint2*>(w);
+  else
+    *reinterpret_cast<f32x4*>(out) = *reinterpret_cast<const f32x4*>(w);
+}
+
+// Whether splitk_reduce4_kernel can finish a problem.
+template <typename OutT>
+inline bool reduce4_ok(const GemmArgs& g) {
+  const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+  return mn < (int64_t{1} << 31) && g.N % 4 == 0 && g.c.ridx == nullptr && g.c.cidx == nullptr &&
+         g.c.col_stride <= 1 && g.c.ld % 4 == 0 && g.c.bstride % 4 == 0 &&
+         (reinterpret_cast<uintptr_t>(g.c.p) % (4 * sizeof(OutT))) == 0 &&
+         (reinterpret_cast<uintptr_t>(g.c.gate) % (4 * sizeof(OutT))) == 0 &&
+         (reinterpret_cast<uintptr_t>(g.partial) % 16) == 0;
+}
+
 // Sums the split partials of every compact element in fixed split order and
 // applies the epilogue.
 template <typename OutT, int EPI>

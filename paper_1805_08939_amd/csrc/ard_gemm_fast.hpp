@@ -882,8 +882,13 @@ inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const int64_t mn = static_cast<int64_t>(g.M) * g.N;
-  hipLaunchKernelGGL((splitk_reduce_kernel<OutT, EPI>), dim3(static_cast<unsigned>((mn + 255) / 256), batch),
-                     dim3(256), 0, stream, g);
+  if (reduce4_ok<OutT>(g)) {
+    hipLaunchKernelGGL((splitk_reduce4_kernel<OutT, EPI>), dim3(static_cast<unsigned>((mn / 4 + 255) / 256), batch),
+                       dim3(256), 0, stream, g);
+  } else {
+    hipLaunchKernelGGL((splitk_reduce_kernel<OutT, EPI>), dim3(static_cast<unsigned>((mn + 255) / 256), batch),
+                       dim3(256), 0, stream, g);
+  }
   return hipGetLastError();
 }
 
