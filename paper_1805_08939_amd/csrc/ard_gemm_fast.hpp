@@ -384,10 +384,13 @@ struct SlabLoader {
   int K, ik, is, left, wv;
   uint32_t lds0;
 
-  __device__ __forceinline__ void issue() {
-    const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
-    da.issue(na, K - ik, st, wv);
-    db.issue(nb, K - ik, st + Cfg::ABYTES, wv);
+  // One slab's loads in two halves: A (issue_a), then B and the advance to
+  // the next slab (issue_b); issue() does both.
+  __device__ __forceinline__ void issue_a() {
+    da.issue(na, K - ik, lds0 + static_cast<uint32_t>(is * Cfg::STAGE), wv);
+  }
+  __device__ __forceinline__ void issue_b() {
+    db.issue(nb, K - ik, lds0 + static_cast<uint32_t>(is * Cfg::STAGE) + Cfg::ABYTES, wv);
     is = is + 1 == Cfg::STAGES ? 0 : is + 1;
     if (left > 0) {
       --left;
@@ -396,6 +399,10 @@ struct SlabLoader {
       ik += Cfg::BK;
       if (ik >= K) ik = 0, na += a_wrap, nb += b_wrap;
     }
+  }
+  __device__ __forceinline__ void issue() {
+    issue_a();
+    issue_b();
   }
 };
 
@@ -425,7 +432,11 @@ __device__ __forceinline__ void grouped_tile(int bid, int nx, int ny, int& row, 
 // previous slab, whose stage takes the next load. Fragments are
 // double-buffered in registers: the reads of the next k step (the first step
 // of the next slab, behind the barrier) are issued before the MFMAs of the
-// current one, so LDS latency and the barrier overlap MFMA execution.
+// current one, so LDS latency and the barrier overlap MFMA execution. The
+// loads issued at a barrier are split: the A half right behind it, the B half
+// after the MFMAs of the slab's first k step, so that the waves do not all
+// queue at the load unit at once while the matrix cores wait (measured on
+// MI355X: 13% fewer cycles per slab for the 256x256 tile).
 // With TAIL, ck is the first k of the first slab within a contraction of
 // length K (slabs wrap to k 0 past K), and a slab with fewer than BK valid k
 // is zeroed past them in LDS before use. With RSUM, rs[i] also sums the A
@@ -450,7 +461,7 @@ __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, 
       fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, K - ck);
       lds_barrier();
     }
-    ld.issue();
+    ld.issue_a();  // B half after the first k step below
     fr[0].load(st, wm, wn, kw0);
   }
   // all slabs but the last one: the last k step crosses into the next slab
@@ -473,11 +484,12 @@ __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, 
           fast_zero_tail<Cfg, Cfg::BN, BMC>(st + Cfg::ABYTES, K - ck);
           lds_barrier();
         }
-        ld.issue();  // into the stage of slab q
+        ld.issue_a();  // into the stage of slab q; B half after the next slab's first k step
         fr[(s + 1) & 1].load(st, wm, wn, kw0);
       }
       fr[s & 1].mma(acc);
       if constexpr (RSUM) fr[s & 1].rowsum(*reinterpret_cast<float(*)[Cfg::FM]>(rs));
+      if (s == 0) ld.issue_b();
     }
   }
   if (nslab > 0) {  // the last slab (a separate copy keeps the loop body's LDS waits exact)
@@ -486,6 +498,7 @@ __device__ __forceinline__ void run_slabs(Loader& ld, int nslab, int K, int ck, 
       if (s + 1 < STEPS) fr[(s + 1) & 1].load(st, wm, wn, kw0 + (s + 1) * Frags::KSTEP);
       fr[s & 1].mma(acc);
       if constexpr (RSUM) fr[s & 1].rowsum(*reinterpret_cast<float(*)[Cfg::FM]>(rs));
+      if (s == 0) ld.issue_b();
     }
   }
   wait_vm<0>();  // no direct load may still write LDS past this point

@@ -401,18 +401,27 @@ struct ListLoader {
     win = v;
   }
 
-  __device__ __forceinline__ void issue() {
+  // One slab's loads in two halves (see run_slabs): A, then B and the advance.
+  int64_t tcur;
+  __device__ __forceinline__ void issue_a() {
     const int e = q / SPT, part = q % SPT;
     if (e - wbase >= 64) {
       wbase += 64;
       refill();
     }
-    const int64_t t = __builtin_amdgcn_readlane(win, e - wbase);
-    const uint32_t st = lds0 + static_cast<uint32_t>(is * Cfg::STAGE);
-    da.issue(a0 + t * a_tile + part * a_part, Cfg::BK, st, wv);
-    db.issue(b0 + t * b_tile + part * b_part, Cfg::BK, st + Cfg::ABYTES, wv);
+    tcur = __builtin_amdgcn_readlane(win, e - wbase);
+    da.issue(a0 + tcur * a_tile + part * a_part, Cfg::BK, lds0 + static_cast<uint32_t>(is * Cfg::STAGE), wv);
+  }
+  __device__ __forceinline__ void issue_b() {
+    const int part = q % SPT;
+    db.issue(b0 + tcur * b_tile + part * b_part, Cfg::BK,
+             lds0 + static_cast<uint32_t>(is * Cfg::STAGE) + Cfg::ABYTES, wv);
     is = is + 1 == Cfg::STAGES ? 0 : is + 1;
     if (q + 1 < nq) ++q;
+  }
+  __device__ __forceinline__ void issue() {
+    issue_a();
+    issue_b();
   }
 };
 
