@@ -58,9 +58,40 @@ __device__ int32_t block_prefix(int32_t v, int32_t* wsum, int32_t& total) {
 
 // Exclusive scan of cnt[0..n) (LDS, n >= 1), each thread summing a contiguous
 // run of entries: writes the n + 1 prefix sums to out (if not NULL), leaves
-// the exclusive prefix in cnt and returns the total.
+// the exclusive prefix in cnt and returns the total. Up to 1024 entries the
+// first wave scans alone (16 entries per lane at most, shuffles, one barrier):
+// the block-wide version costs four barriers of all 16 waves.
 __device__ int32_t block_exclusive_scan(int32_t* cnt, int n, int32_t* out, int32_t* wsum) {
   const int tid = threadIdx.x;
+  if (n <= 1024) {
+    if (tid < 64) {
+      const int per = (n + 63) / 64;
+      const int lo = min(n, tid * per), hi = min(n, lo + per);
+      int32_t v = 0;
+      for (int i = lo; i < hi; ++i) v += cnt[i];
+      int32_t inc = v;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int32_t t = __shfl_up(inc, d, 64);
+        if (tid >= d) inc += t;
+      }
+      int32_t run = inc - v;
+      for (int i = lo; i < hi; ++i) {
+        const int32_t c = cnt[i];
+        if (out) out[i] = run;
+        cnt[i] = run;
+        run += c;
+      }
+      if (tid == 63) {
+        wsum[0] = inc;
+        if (out) out[n] = inc;
+      }
+    }
+    __syncthreads();
+    const int32_t total = wsum[0];
+    __syncthreads();  // wsum may be reused right away
+    return total;
+  }
   const int per = (n + kScanThreads - 1) / kScanThreads;
   const int lo = min(n, tid * per), hi = min(n, lo + per);
   int32_t s = 0;
