@@ -618,8 +618,8 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int n0 = tile_col * Cfg::BN;
   const int m0 = tile_row * Cfg::BM;
   const int splits = g.splits > 1 ? g.splits : 1;
-  const int64_t bz = blockIdx.z / splits;
-  const int split = blockIdx.z % splits;
+  const int64_t bz = splits > 1 ? blockIdx.z / splits : blockIdx.z;
+  const int split = splits > 1 ? blockIdx.z % splits : 0;
   const int wave = threadIdx.x >> 6;
   const int ks = wave / (Cfg::WGM * Cfg::WGN);
   const int wmn = wave % (Cfg::WGM * Cfg::WGN);
@@ -639,8 +639,12 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   const int nks = (g.K + Cfg::BK - 1) / Cfg::BK;
   const int kbatch = g.kbatch > 0 ? g.kbatch : 1;
   const int nslab = kbatch * nks;
-  const int q0 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * split) / splits));
-  const int q1 = __builtin_amdgcn_readfirstlane(static_cast<int>((static_cast<int64_t>(nslab) * (split + 1)) / splits));
+  // slabs of this split (32-bit divisions: nslab * splits < 2^31; none without a split)
+  int q0 = 0, q1 = nslab;
+  if (splits > 1) {
+    q0 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(nslab * split) / splits));
+    q1 = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(nslab * (split + 1)) / splits));
+  }
 
   // slabs q0 .. q1 - 1 of this split
   SlabLoader<Cfg, AMC, BMC> ld;
@@ -657,7 +661,7 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   ld.b_step = (BMC ? g.b.ld : 1) * Cfg::BK * ES;
   ld.a_wrap = g.a.kbstride * ES - nks * ld.a_step;
   ld.b_wrap = g.b.kbstride * ES - nks * ld.b_step;
-  const int ib = q0 / (nks > 0 ? nks : 1);
+  const int ib = q0 == 0 ? 0 : q0 / (nks > 0 ? nks : 1);
   ld.ik = (q0 - ib * nks) * Cfg::BK;
   ld.is = 0;
   ld.left = q1 - q0 - 1;
@@ -934,7 +938,9 @@ inline hipError_t run_fast_gemm(GemmArgs g, int batch, hipStream_t stream, float
   if (rsum_done) *rsum_done = false;
   if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
   FastPlan p = plan_fast<T>(g.M, g.N, g.K, g.kbatch, batch);
-  if (!partial) p.splits = 1;
+  // the kernel splits the slabs with 32-bit arithmetic
+  const int64_t kb = g.kbatch > 0 ? g.kbatch : 1;
+  if (!partial || kb * (g.K / 32 + 1) * p.splits >= int64_t{1} << 31) p.splits = 1;
   g.splits = p.splits;
   g.partial = partial;
   if (RSUM && g.rsum && p.splits == 1 && !(sizeof(T) == 2 && p.kind == FAST_HUGE)) {
