@@ -148,10 +148,15 @@ int32_t ard_bitmap_popcount(const uint32_t* bits, int32_t total);
 /* ------------------------------------------------------------------------ */
 /*
  * The compact index list of a row pattern (Sec. III-A: the compact matrices are
- * built from the kept rows only). Fills d_idx[0..kept) with the kept neuron
- * indices in ascending order and the plan struct (host) with n, the pattern and
- * the host-known kept count, so that later launches need no device readback.
- * d_idx: device, capacity >= ard_row_kept(n, period, offset), caller-owned.
+ * built from the kept rows only). Fills the plan struct (host) with n, the
+ * pattern and the host-known kept count, so that later launches need no device
+ * readback, and d_idx[0..kept) with the kept neuron indices in ascending order.
+ * d_idx: device, capacity >= ard_row_kept(n, period, offset), caller-owned; or
+ * NULL for a list-free plan (nothing is launched). The kept set of a row pattern
+ * is the arithmetic progression offset + period * i, so the FC calls fold it
+ * into strided operand and output views and never read the list: they accept
+ * list-free plans. The LSTM calls read the list and reject a list-free plan
+ * that drops units (ARD_ERR_INVALID_ARG).
  */
 typedef struct {
   int32_t n;

@@ -11,7 +11,7 @@ import numpy as np
 
 from . import _ffi
 from ._ffi import (ARD_ACT_NONE, ARD_ACT_RELU, ARD_BF16, ARD_DROPPED_SKIP, ARD_DROPPED_ZERO,  # noqa: F401
-                   ARD_ERR_NOT_CONVERGED, ARD_F32, ARD_SEARCH_MIRROR, ARD_SEARCH_PLAIN,
+                   ARD_ERR_INVALID_ARG, ARD_ERR_NOT_CONVERGED, ARD_F32, ARD_SEARCH_MIRROR, ARD_SEARCH_PLAIN,
                    ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_FULL,
                    ard_fc_desc, ard_lstm_desc, ard_row_plan, ard_search_info, ard_search_opts,
                    ard_tile_desc, ard_tile_plan)
@@ -130,8 +130,9 @@ def ard_bitmap_popcount(bits, total):
 # --------------------------------------------------------------------------- compaction
 
 def ard_plan_rows(n, period, offset, d_idx, stream=None, plan=None):
-    """Fills the int32 device tensor d_idx with the kept list; returns the plan
-    (``plan`` if given, refilled in place). The plan keeps a reference to d_idx."""
+    """Fills the int32 device tensor d_idx with the kept list (d_idx None: a
+    list-free plan, nothing launched); returns the plan (``plan`` if given,
+    refilled in place). The plan keeps a reference to d_idx."""
     plan = ard_row_plan() if plan is None else plan
     _check(_ffi.lib().ard_plan_rows(n, period, offset, _ptr(d_idx), ctypes.byref(plan), _stream(stream)))
     plan._keep = d_idx

@@ -124,8 +124,6 @@ __global__ void __launch_bounds__(256) compact_weights_kernel(const T* __restric
 struct FcShape {
   int32_t B, K, N;
   int32_t kin, kout;                 // kept counts
-  const int32_t* in_idx;             // NULL when every input is kept
-  const int32_t* out_idx;            // NULL when every output is kept
   int32_t in_period, in_offset, out_period, out_offset;
   size_t esize;
   int64_t ldc;                       // compact weight row length
@@ -148,9 +146,9 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
     return fail(ARD_ERR_INVALID_ARG, "unknown weight layout %d", d->weight_layout);
   if (!(d->scale == d->scale) || d->scale == __builtin_inff() || d->scale == -__builtin_inff())
     return fail(ARD_ERR_INVALID_ARG, "scale must be finite");
-  int st = check_row_plan(d->in_plan, d->in_features, "in_plan");
+  int st = check_row_plan(d->in_plan, d->in_features, "in_plan", false);
   if (st != ARD_OK) return st;
-  st = check_row_plan(d->out_plan, d->out_features, "out_plan");
+  st = check_row_plan(d->out_plan, d->out_features, "out_plan", false);
   if (st != ARD_OK) return st;
   s->B = d->batch;
   s->K = d->in_features;
@@ -159,8 +157,6 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   const bool out_all = !d->out_plan || d->out_plan->period == 1;
   s->kin = in_all ? s->K : d->in_plan->kept;
   s->kout = out_all ? s->N : d->out_plan->kept;
-  s->in_idx = in_all ? nullptr : d->in_plan->d_idx;
-  s->out_idx = out_all ? nullptr : d->out_plan->d_idx;
   s->in_period = in_all ? 1 : d->in_plan->period;
   s->in_offset = in_all ? 0 : d->in_plan->offset;
   s->out_period = out_all ? 1 : d->out_plan->period;
@@ -168,7 +164,7 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   s->esize = d->dtype == ARD_BF16 ? 2 : 4;
   s->ldc = (static_cast<int64_t>(s->kin) + 7) / 8 * 8;
   s->compact_given = d->weight_layout == ARD_WEIGHTS_COMPACT;
-  s->needs_compact = !s->compact_given && s->in_idx != nullptr;
+  s->needs_compact = !s->compact_given && s->in_period > 1;
   return ARD_OK;
 }
 
@@ -297,12 +293,11 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   g.K = s.kin;
   g.a = wv.op;
   g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
-  g.c = {Yt, s.B, s.out_idx, nullptr, 0, bias, d->act == ARD_ACT_RELU, d->scale};
+  g.c = strided_out(Yt, s.B, sizeof(T), s.out_period, s.out_offset, 1, 0, bias, d->act == ARD_ACT_RELU, d->scale,
+                    nullptr);
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   if (fast_ok(g, sizeof(T))) {
-    g.c = strided_out(Yt, s.B, sizeof(T), s.out_period, s.out_offset, 1, 0, bias, d->act == ARD_ACT_RELU,
-                      d->scale, nullptr);
     ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -335,11 +330,10 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   // [Xgate > 0] of the layer below.
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   g.b = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
-  g.c = {dXt, s.B, s.in_idx, nullptr, 0, nullptr, 0, d->scale, Xgate};
+  g.c = strided_out(dXt, s.B, sizeof(T), s.in_period, s.in_offset, 1, 0, nullptr, 0, d->scale, Xgate);
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
   if (fast_ok(g, sizeof(T))) {
-    g.c = strided_out(dXt, s.B, sizeof(T), s.in_period, s.in_offset, 1, 0, nullptr, 0, d->scale, Xgate);
     ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
@@ -367,15 +361,14 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   g.a = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
   g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
-  g.c = {dW, s.K, s.out_idx, s.in_idx, 0, nullptr, 0, d->scale};
+  g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
+                    d->scale, nullptr);
   const bool v = vec_rows(s.B, sizeof(T));
   float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
   bool dbias_done = false;
   if (fast_ok(g, sizeof(T))) {
-    g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
-                      d->scale, nullptr);
     // dbias = scale * G 1: the row sums of A, taken by the same kernel
     if (dbias) {
       g.rsum = dbias + s.out_offset;
@@ -425,13 +418,12 @@ int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard
   if (period < 1 || offset < 0 || offset >= period)
     return fail(ARD_ERR_INVALID_ARG, "invalid pattern (period %d, offset %d)", period, offset);
   const int32_t kept = kept_count(n, period, offset);
-  if (kept > 0 && !d_idx) return fail(ARD_ERR_INVALID_ARG, "d_idx is NULL");
   plan->n = n;
   plan->period = period;
   plan->offset = offset;
   plan->kept = kept;
   plan->d_idx = d_idx;
-  if (kept > 0) {
+  if (kept > 0 && d_idx) {
     hipLaunchKernelGGL(plan_rows_kernel, dim3((kept + 255) / 256), dim3(256), 0,
                        static_cast<hipStream_t>(stream), d_idx, kept, period, offset);
     ARD_LAUNCH_CHECK();

@@ -822,10 +822,28 @@ inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
     bk = C::Small::BK;
     tiles = tiles_of(C::Small::BM, C::Small::BN);
   }
-  // split-K pays for its partial-sum round trip and reduction launch only on
-  // long contractions (measured on MI355X: never below K = 2048)
   const int64_t kb = kbatch > 0 ? kbatch : 1;
-  p.splits = kb * K >= 8192 ? fast_splits(tiles, kb * ((K + bk - 1) / bk)) : 1;
+  const int64_t slabs = kb * ((K + bk - 1) / bk);
+  if (p.kind == FAST_SMALL) {
+    // A 32x32 workgroup takes about 0.9 us per 128-deep slab however many run
+    // beside it (measured on MI355X), so a long contraction over few tiles is
+    // a serial chain: split it over more workgroups (up to one round of the
+    // chip) when that saves more than the partial-sum round trip and the
+    // reduction launch cost (about 3 us).
+    double best_t = 0.9 * static_cast<double>(slabs);
+    p.splits = 1;
+    for (int s = 2; s <= kMaxSplits && tiles * s <= kTargetBlocks && slabs >= s; s *= 2) {
+      const double t = 0.9 * static_cast<double>((slabs + s - 1) / s) + 3.0;
+      if (t < best_t) {
+        best_t = t;
+        p.splits = s;
+      }
+    }
+    return p;
+  }
+  // larger tiles: split-K pays for its partial-sum round trip and reduction
+  // launch only on long contractions (measured on MI355X: never below K = 2048)
+  p.splits = kb * K >= 8192 ? fast_splits(tiles, slabs) : 1;
   return p;
 }
 

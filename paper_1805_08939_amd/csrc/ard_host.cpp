@@ -29,7 +29,7 @@ int fail(int status, const char* fmt, ...) {
 
 void clear_error() { g_last_error.clear(); }
 
-int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what) {
+int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what, bool needs_list) {
   if (plan == nullptr) return ARD_OK;
   if (plan->n != n)
     return fail(ARD_ERR_INVALID_ARG, "%s: plan covers %d neurons, layer has %d", what, plan->n, n);
@@ -38,8 +38,8 @@ int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what) {
                 plan->period, plan->offset);
   if (plan->kept != kept_count(n, plan->period, plan->offset))
     return fail(ARD_ERR_INVALID_ARG, "%s: kept %d does not match the pattern", what, plan->kept);
-  if (plan->kept > 0 && plan->d_idx == nullptr)
-    return fail(ARD_ERR_INVALID_ARG, "%s: d_idx is NULL", what);
+  if (needs_list && plan->period > 1 && plan->kept > 0 && plan->d_idx == nullptr)
+    return fail(ARD_ERR_INVALID_ARG, "%s: d_idx is NULL (this call reads the kept-index list)", what);
   return ARD_OK;
 }
 

@@ -18,8 +18,10 @@ void clear_error();
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Validates a row plan against the neuron count it is applied to. A NULL plan
-// is "everything kept". Returns ARD_OK or an error with a message.
-int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what);
+// is "everything kept". needs_list: the caller reads the device kept-index
+// list, so a plan that drops neurons must carry one. Returns ARD_OK or an
+// error with a message.
+int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what, bool needs_list);
 
 // Kept count of a row pattern (see ard_row_kept).
 inline int32_t kept_count(int32_t n, int32_t period, int32_t offset) {

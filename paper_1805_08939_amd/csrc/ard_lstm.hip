@@ -414,7 +414,7 @@ int check_lstm(const ard_lstm_desc* d, int32_t* ns, int32_t* period, int32_t* of
   if (d->dtype != ARD_F32) return fail(ARD_ERR_UNSUPPORTED, "LSTM supports ARD_F32 only");
   if (d->seq_len < 1 || d->batch < 1 || d->input_size < 1 || d->hidden_size < 1)
     return fail(ARD_ERR_INVALID_ARG, "sizes must be >= 1");
-  int st = check_row_plan(d->hidden_plan, d->hidden_size, "hidden_plan");
+  int st = check_row_plan(d->hidden_plan, d->hidden_size, "hidden_plan", true);
   if (st != ARD_OK) return st;
   const bool all = !d->hidden_plan || d->hidden_plan->period == 1;
   *ns = all ? d->hidden_size : d->hidden_plan->kept;

@@ -22,9 +22,14 @@ def ard_dtype(dtype_name):
     return api.ARD_F32 if dtype_name == "f32" else api.ARD_BF16
 
 
-def row_plan(n, period, offset, check=True):
-    """Builds a row plan on the device; checks its list against the oracle."""
+def row_plan(n, period, offset, check=True, with_list=True):
+    """Builds a row plan on the device; checks its list against the oracle.
+    with_list=False: a list-free plan (no device list, nothing launched)."""
     kept = opat.row_kept_count(n, period, offset)
+    if not with_list:
+        plan = api.ard_plan_rows(n, period, offset, None)
+        assert plan.kept == kept and not plan.d_idx
+        return plan
     idx = torch.full((max(kept, 1),), -1, dtype=torch.int32, device=device())
     plan = api.ard_plan_rows(n, period, offset, idx)
     if check:

@@ -78,6 +78,17 @@ def test_bitmaps_bit_exact_against_oracle():
                 opat.bitmap_popcount(want, tn * tk)
 
 
+def test_list_free_row_plan_launches_nothing():
+    """ard_plan_rows without a device list fills the host plan only, so it runs
+    without a GPU."""
+    for n, per, off in [(2048, 3, 1), (10, 16, 12), (7, 1, 0)]:
+        plan = api.ard_plan_rows(n, per, off, None, stream=0)
+        assert (plan.n, plan.period, plan.offset, plan.kept) == (n, per, off, opat.row_kept_count(n, per, off))
+        assert not plan.d_idx
+    with pytest.raises(api.ArdError):
+        api.ard_plan_rows(10, 3, 3, None, stream=0)
+
+
 def test_row_kept_matches_oracle():
     for n in range(0, 50):
         for per in range(1, 19):

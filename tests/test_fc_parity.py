@@ -27,9 +27,10 @@ def make_inputs(dtype, B, K, N, seed, w_std=0.05, bias=True):
 
 
 def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans=True,
-              sentinel=None, poison=False):
+              sentinel=None, poison=False, lists=True):
     """Runs fwd, bwd_data and bwd_weight on the GPU and checks each against the
-    oracle. Returns the GPU outputs."""
+    oracle. Returns the GPU outputs. lists=False: list-free row plans (the FC
+    calls read patterns as strided views)."""
     B, K = X.shape
     N = W.shape[0]
     m_in, m_out = opat.row_mask(K, *pin), opat.row_mask(N, *pout)
@@ -39,8 +40,8 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
     Ys = synth.to_storage(torch.from_numpy(Y64).float(), dtype)
     dX64, dW64, db64 = ofc.fc_backward(f64(X), f64(W), f64(Ys), f64(dY), m_in, m_out, scale, act)
 
-    in_plan = None if (use_null_plans and pin == (1, 0)) else row_plan(K, *pin)
-    out_plan = None if (use_null_plans and pout == (1, 0)) else row_plan(N, *pout)
+    in_plan = None if (use_null_plans and pin == (1, 0)) else row_plan(K, *pin, with_list=lists)
+    out_plan = None if (use_null_plans and pout == (1, 0)) else row_plan(N, *pout, with_list=lists)
     desc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped)
 
     Xt, Wd, dYt, Yst = to_dev(X.T), to_dev(W), to_dev(dY.T), to_dev(Ys.T)
@@ -105,9 +106,9 @@ PATTERNS = [(1, 0), (2, 0), (2, 1), (3, 2), (5, 1), (16, 9), (40, 39)]
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_tiny_all_pattern_pairs(dtype):
     X, W, b, dY = make_inputs(dtype, 5, 13, 11, seed=1805)
-    for pin, pout in itertools.product(PATTERNS, repeat=2):
+    for i, (pin, pout) in enumerate(itertools.product(PATTERNS, repeat=2)):
         for act in ("none", "relu"):
-            run_layer(dtype, X, W, b, dY, pin, pout, act, 1.0 / 0.7, api.ARD_DROPPED_ZERO)
+            run_layer(dtype, X, W, b, dY, pin, pout, act, 1.0 / 0.7, api.ARD_DROPPED_ZERO, lists=i % 2 == 0)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -115,10 +116,10 @@ def test_tiny_all_pattern_pairs(dtype):
 def test_multi_tile_ragged(dtype, shape):
     B, K, N = shape
     X, W, b, dY = make_inputs(dtype, B, K, N, seed=sum(shape))
-    for pin, pout, act in [((3, 1), (2, 0), "relu"), ((1, 0), (5, 4), "none"),
-                           ((4, 2), (1, 0), "relu"), ((7, 0), (3, 1), "none")]:
+    for i, (pin, pout, act) in enumerate([((3, 1), (2, 0), "relu"), ((1, 0), (5, 4), "none"),
+                                          ((4, 2), (1, 0), "relu"), ((7, 0), (3, 1), "none")]):
         run_layer(dtype, X, W, b, dY, pin, pout, act, 1.25, api.ARD_DROPPED_ZERO,
-                  use_null_plans=False)
+                  use_null_plans=False, lists=i % 2 == 1)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -153,3 +153,10 @@ def test_invalid():
         api.ard_lstm_fwd(desc, torch.zeros(64, device=d), torch.zeros(512, device=d), None, None, None,
                          torch.zeros(64, device=d), None, None, small)
     assert e.value.status == 5
+    # the LSTM reads the kept-unit list: a list-free plan that drops units is rejected
+    plan = api.ard_plan_rows(8, 2, 1, None)
+    desc = api.lstm_desc(api.ARD_F32, 2, 4, 8, 8, plan)
+    with pytest.raises(api.ArdError) as e:
+        api.ard_lstm_fwd(desc, torch.zeros(64, device=d), torch.zeros(512, device=d), None, None, None,
+                         torch.zeros(64, device=d), None, None, torch.zeros(1 << 20, device=d))
+    assert e.value.status == api.ARD_ERR_INVALID_ARG and "d_idx" in e.value.message
