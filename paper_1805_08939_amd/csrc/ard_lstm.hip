@@ -383,9 +383,17 @@ __global__ void __launch_bounds__(256) lstm_bwd_rec_kernel(LstmStep s, float* __
 }
 
 // dh_rec of unit u, sample b: the splits' partial sums added in split order.
+// The loads of up to eight splits are issued together, then added in order.
 __device__ __forceinline__ float rec_sum(const float* __restrict__ part, int32_t splits, int64_t nsB, int64_t e) {
   float v = 0.0f;
-  for (int z = 0; z < splits; ++z) v += part[z * nsB + e];
+  for (int z0 = 0; z0 < splits; z0 += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = z0 + u < splits ? part[(z0 + u) * nsB + e] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (z0 + u < splits) v += t[u];
+  }
   return v;
 }
 
