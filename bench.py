@@ -6,7 +6,8 @@ with row-based dropout on both hidden layers. Each step samples a fresh
 pattern per hidden layer from the distribution K searched for p, plans it,
 gathers the compact weights of the layers whose inputs are dropped on the
 device, and runs fwd, bwd_data and bwd_weight of all three layers
-(bwd_data of the first layer is not needed). The headline value is TFLOP/s
+(bwd_data of the first layer is not needed; the two backward products of a
+layer are one call, one launch where both are small). The headline value is TFLOP/s
 counted on the work actually kept, at p = 0.5; the same steps at p = 0.3 and
 0.7 and at p = 0 (period 1: the same kernels with nothing dropped) give the
 speedups. Other workloads (--workload) are the single wide MLP layer set, the
@@ -102,24 +103,25 @@ class Mlp:
         def layer_calls(l, compact):
             desc = self.cdescs[l] if compact else self.descs[l]
             w = P["Wc"][l] if compact else P["W"][l]
-            calls = {("fwd", l): (api.ard_fc_fwd, (desc, acts[l], w, P["bias"][l], P["Y"][l], ws, st), {}),
-                     ("bwd_weight", l): (api.ard_fc_bwd_weight, (desc, acts[l], P["dY"][l], None, P["dW"][l],
-                                                                 P["db"][l], ws, st), {})}
-            # backward: each bwd_data also applies the ReLU derivative of the layer
-            # below (Xgate = that layer's output), so every dY[l] below the top is
-            # already gated and is passed with Yt = None
+            calls = {("fwd", l): (api.ard_fc_fwd, (desc, acts[l], w, P["bias"][l], P["Y"][l], ws, st), {})}
             if l > 0:
-                calls[("bwd_data", l)] = (api.ard_fc_bwd_data, (desc, P["dY"][l], None, w, P["dY"][l - 1], ws, st),
-                                          {"Xgate": acts[l]})
+                # the layer's backward in one call: bwd_data (which also applies the
+                # ReLU derivative of the layer below, Xgate = that layer's output, so
+                # every dY[l] below the top is already gated and is passed with
+                # Yt = None) and bwd_weight, one launch where both are small
+                calls[("bwd", l)] = (api.ard_fc_bwd, (desc, acts[l], P["dY"][l], None, w, P["dY"][l - 1],
+                                                      P["dW"][l], P["db"][l], ws, st), {"Xgate": acts[l]})
+            else:  # the network input needs no gradient
+                calls[("bwd_weight", l)] = (api.ard_fc_bwd_weight, (desc, acts[l], P["dY"][l], None, P["dW"][l],
+                                                                    P["db"][l], ws, st), {})
             return calls
 
         self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l > 0 else None}
                             for l in range(self.L)]
         self.order = [("fwd", l) for l in range(self.L)]
-        for l in reversed(range(self.L)):
-            self.order.append(("bwd_weight", l))
-            if l > 0:
-                self.order.append(("bwd_data", l))
+        self.order += [("bwd", l) for l in reversed(range(1, self.L))] + [("bwd_weight", 0)]
+        # calls of one GEMM each: the candidates for the roofline call
+        self.roofline_keys = [k for k in self.order if k[0] != "bwd"]
 
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
@@ -133,15 +135,17 @@ class Mlp:
         return n
 
     def kept_flops(self, pats):
-        """(total, per-call dict): 2*B*K_kept*N_kept per GEMM; no bwd_data for layer 0."""
+        """(total, per-call dict): 2*B*K_kept*N_kept per GEMM (fwd, bwd_data,
+        bwd_weight); no bwd_data for layer 0. A ("bwd", l) call holds two GEMMs."""
         n = self.kept(pats)
         per = {}
         for l in range(self.L):
             f = 2.0 * self.B * n[l] * n[l + 1]
             per[("fwd", l)] = f
-            per[("bwd_weight", l)] = f
             if l > 0:
-                per[("bwd_data", l)] = f
+                per[("bwd", l)] = 2.0 * f
+            else:
+                per[("bwd_weight", l)] = f
         return sum(per.values()), per
 
     @staticmethod
@@ -452,16 +456,17 @@ def time_steps(wl, steps, warmup, it0, timed_call=None):
 
 
 def roofline_call(wl, first_it, steps):
-    """The call with the most kept work over the timed steps (summed kept
+    """The one-GEMM call with the most kept work over the timed steps (summed kept
     FLOPs; ties go to the first call of a step). The patterns are seeded, so
     the choice is the same in every run of the same command."""
+    keys = getattr(wl, "roofline_keys", wl.order)
     totals = {}
     for i in range(steps):
         _, per = wl.kept_flops(wl.patterns(first_it + i))
-        for key in wl.order:
+        for key in keys:
             totals[key] = totals.get(key, 0.0) + per.get(key, 0.0)
     best = max(totals.values())
-    return next(k for k in wl.order if totals.get(k, 0.0) == best)
+    return next(k for k in keys if totals.get(k, 0.0) == best)
 
 
 def cpu_baseline(wl, p, budget_s):

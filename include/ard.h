@@ -295,6 +295,16 @@ int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, co
 /* dbias may be NULL. */
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
                       float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);
+/*
+ * The whole backward of one layer (Sec. III-A applied to both backward
+ * products): ard_fc_bwd_data followed by ard_fc_bwd_weight, with the same
+ * arguments, layouts, workspace and results, bit for bit. When both products
+ * are small enough to take the 32 x 32 output tiles without a split
+ * contraction they run as one kernel launch (the tiles of dXt, then those of
+ * dW), which saves one launch's fixed cost per layer. dbias may be NULL.
+ */
+int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt, const void* W,
+               void* dXt, const void* Xgate, float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Layer under a tile pattern (device).                                     */

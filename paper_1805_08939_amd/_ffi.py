@@ -92,6 +92,8 @@ SIGNATURES = {
                                        c_size, c_vp]),
     "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                          c_size, c_vp]),
+    "ard_fc_bwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                  c_vp, c_size, c_vp]),
     "ard_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
                                     c_vp, c_vp, c_vp, c_vp]),
     "ard_tile_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),

@@ -217,6 +217,13 @@ def ard_fc_bwd_weight(desc, Xt, dYt, Yt, dW, dbias, ws=None, stream=None):
                                         _ptr(dbias), p, n, _stream(stream)))
 
 
+def ard_fc_bwd(desc, Xt, dYt, Yt, W, dXt, dW, dbias, ws=None, stream=None, Xgate=None):
+    """bwd_data then bwd_weight of one layer (one launch where both are small)."""
+    p, n = _ws(ws)
+    _check(_ffi.lib().ard_fc_bwd(ctypes.byref(desc), _ptr(Xt), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt),
+                                 _ptr(Xgate), _ptr(dW), _ptr(dbias), p, n, _stream(stream)))
+
+
 # --------------------------------------------------------------------------- tile layer
 
 def tile_desc(dtype, batch, in_features, out_features, scale=1.0, dropped=ARD_DROPPED_ZERO):

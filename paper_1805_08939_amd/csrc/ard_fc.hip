@@ -312,18 +312,16 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   return ARD_OK;
 }
 
+// bwd_data as a GEMM: dXt[S_in] = W[S_out][S_in]^T G over the kept outputs.
 template <typename T>
-int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
-                     const void* W, void* dXt, const void* Xgate, void* ws, hipStream_t stream) {
-  WeightView wv;
-  int st = weight_view<T>(s, W, ws, stream, &wv);
-  if (st != ARD_OK) return st;
+GemmArgs bwd_data_args(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
+                       const GemmOperand& wop, void* dXt, const void* Xgate) {
   GemmArgs g = {};
   g.M = s.kin;
   g.N = s.B;
   g.K = s.kout;
   // A(m, t) = W[out(t)][in(m)]: the view's rows are the contraction index.
-  g.a = wv.op;
+  g.a = wop;
   // B(t, n) = dY[out(t)][n] * [Y > 0] (no gate when Yt is NULL: dY is already
   // the gated gradient); the 0/1 gate keeps bf16 operands exact, and scale is
   // applied to the fp32 accumulators in the epilogue, as is the optional gate
@@ -331,29 +329,13 @@ int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, co
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   g.b = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
   g.c = strided_out(dXt, s.B, sizeof(T), s.in_period, s.in_offset, 1, 0, nullptr, 0, d->scale, Xgate);
-  const bool a_vec = vec_rows(g.a.ld, sizeof(T));
-  const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok(g, sizeof(T))) {
-    ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
-  } else if (gated) {
-    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
-        g, 1, a_vec, b_vec, stream, wv.partial)));
-  } else {
-    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-        g, 1, a_vec, b_vec, stream, wv.partial)));
-  }
-  if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
-    hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
-                       static_cast<T*>(dXt), static_cast<int64_t>(s.B), s.B, s.in_period,
-                       s.in_offset);
-    ARD_LAUNCH_CHECK();
-  }
-  return ARD_OK;
+  return g;
 }
 
+// bwd_weight as a GEMM: dW[S_out][S_in] = G X^T over the batch.
 template <typename T>
-int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
-                       const void* Yt, float* dW, float* dbias, void* ws, hipStream_t stream) {
+GemmArgs bwd_weight_args(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
+                         const void* Yt, float* dW) {
   GemmArgs g = {};
   g.M = s.kout;
   g.N = s.kin;
@@ -363,25 +345,26 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
   g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
   g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
                     d->scale, nullptr);
-  const bool v = vec_rows(s.B, sizeof(T));
-  float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                                 (s.needs_compact ? al256(compact_bytes(s)) : 0))
-                      : nullptr;
-  bool dbias_done = false;
-  if (fast_ok(g, sizeof(T))) {
-    // dbias = scale * G 1: the row sums of A, taken by the same kernel
-    if (dbias) {
-      g.rsum = dbias + s.out_offset;
-      g.rsum_ld = s.out_period;
-    }
-    ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD, true>(g, 1, stream, partial, &dbias_done)));
-  } else if (gated) {
-    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
-        g, 1, v, v, stream, partial)));
-  } else {
-    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
-        g, 1, v, v, stream, partial)));
+  return g;
+}
+
+template <typename T>
+int zero_dropped_inputs(const ard_fc_desc* d, const FcShape& s, void* dXt, hipStream_t stream) {
+  if (d->dropped == ARD_DROPPED_ZERO && s.in_period > 1) {
+    hipLaunchKernelGGL(zero_dropped_rows_kernel<T>, dim3(s.K), dim3(256), 0, stream,
+                       static_cast<T*>(dXt), static_cast<int64_t>(s.B), s.B, s.in_period,
+                       s.in_offset);
+    ARD_LAUNCH_CHECK();
   }
+  return ARD_OK;
+}
+
+// The bias gradient where the weight-gradient GEMM did not take it, and the
+// ZERO-mode fills of dropped weight-gradient entries.
+template <typename T>
+int finish_bwd_weight(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt, float* dW,
+                      float* dbias, bool dbias_done, hipStream_t stream) {
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   if (dbias && s.kout > 0 && !dbias_done) {
     const int vec = aligned16(dYt) && (!gated || aligned16(Yt)) &&
                     (static_cast<int64_t>(s.B) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
@@ -401,6 +384,93 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
     }
   }
   return ARD_OK;
+}
+
+template <typename T>
+int run_bwd_data(const ard_fc_desc* d, const FcShape& s, const GemmArgs& g, const void* Yt, void* dXt,
+                 float* partial, hipStream_t stream) {
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
+  const bool a_vec = vec_rows(g.a.ld, sizeof(T));
+  const bool b_vec = vec_rows(s.B, sizeof(T));
+  if (fast_ok(g, sizeof(T))) {
+    ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, partial)));
+  } else if (gated) {
+    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
+        g, 1, a_vec, b_vec, stream, partial)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+        g, 1, a_vec, b_vec, stream, partial)));
+  }
+  return zero_dropped_inputs<T>(d, s, dXt, stream);
+}
+
+template <typename T>
+int fc_bwd_data_impl(const ard_fc_desc* d, const FcShape& s, const void* dYt, const void* Yt,
+                     const void* W, void* dXt, const void* Xgate, void* ws, hipStream_t stream) {
+  WeightView wv;
+  int st = weight_view<T>(s, W, ws, stream, &wv);
+  if (st != ARD_OK) return st;
+  return run_bwd_data<T>(d, s, bwd_data_args<T>(d, s, dYt, Yt, wv.op, dXt, Xgate), Yt, dXt, wv.partial, stream);
+}
+
+template <typename T>
+int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
+                       const void* Yt, float* dW, float* dbias, void* ws, hipStream_t stream) {
+  GemmArgs g = bwd_weight_args<T>(d, s, Xt, dYt, Yt, dW);
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
+  const bool v = vec_rows(s.B, sizeof(T));
+  float* partial = ws ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                 (s.needs_compact ? al256(compact_bytes(s)) : 0))
+                      : nullptr;
+  bool dbias_done = false;
+  if (fast_ok(g, sizeof(T))) {
+    // dbias = scale * G 1: the row sums of A, taken by the same kernel
+    if (dbias) {
+      g.rsum = dbias + s.out_offset;
+      g.rsum_ld = s.out_period;
+    }
+    ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD, true>(g, 1, stream, partial, &dbias_done)));
+  } else if (gated) {
+    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, true, false, EPI_FWD>(
+        g, 1, v, v, stream, partial)));
+  } else {
+    ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
+        g, 1, v, v, stream, partial)));
+  }
+  return finish_bwd_weight<T>(d, s, dYt, Yt, dW, dbias, dbias_done, stream);
+}
+
+// bwd_data and bwd_weight of one layer. When both GEMMs take the fast 32x32
+// configuration without a k split they run as one launch (the bias gradient
+// from the weight-gradient GEMM's row sums); otherwise the two calls one
+// after the other. The results are bitwise those of the separate calls: each
+// output tile is computed by the same code on the same operands.
+template <typename T>
+int fc_bwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt, const void* Yt,
+                const void* W, void* dXt, const void* Xgate, float* dW, float* dbias, void* ws,
+                hipStream_t stream) {
+  WeightView wv;
+  int st = weight_view<T>(s, W, ws, stream, &wv);
+  if (st != ARD_OK) return st;
+  const GemmArgs gd = bwd_data_args<T>(d, s, dYt, Yt, wv.op, dXt, Xgate);
+  GemmArgs gw = bwd_weight_args<T>(d, s, Xt, dYt, Yt, dW);
+  if (fast_ok(gd, sizeof(T)) && fast_ok(gw, sizeof(T)) && fast_pair_ok<T>(gd, gw)) {
+    if (dbias) {
+      gw.rsum = dbias + s.out_offset;
+      gw.rsum_ld = s.out_period;
+      ARD_HIP_CHECK((launch_fast_pair<T, true, true, T, EPI_FWD, false, false, false, float, EPI_FWD, true>(
+          gd, gw, stream)));
+    } else {
+      ARD_HIP_CHECK((launch_fast_pair<T, true, true, T, EPI_FWD, false, false, false, float, EPI_FWD, false>(
+          gd, gw, stream)));
+    }
+    if ((st = zero_dropped_inputs<T>(d, s, dXt, stream)) != ARD_OK) return st;
+    return finish_bwd_weight<T>(d, s, dYt, Yt, dW, dbias, dbias != nullptr, stream);
+  }
+  // the compact weights (if built into ws) are not needed past bwd_data,
+  // whose partial sums lie behind them: bwd_weight's own call layout
+  if ((st = run_bwd_data<T>(d, s, gd, Yt, dXt, wv.partial, stream)) != ARD_OK) return st;
+  return fc_bwd_weight_impl<T>(d, s, Xt, dYt, Yt, dW, dbias, ws, stream);
 }
 
 }  // namespace
@@ -493,6 +563,24 @@ int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, co
   hipStream_t sm = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) return fc_bwd_data_impl<bf16>(desc, s, dYt, Yt, W, dXt, Xgate, ws, sm);
   return fc_bwd_data_impl<float>(desc, s, dYt, Yt, W, dXt, Xgate, ws, sm);
+}
+
+int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt, const void* W,
+               void* dXt, const void* Xgate, float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(dYt, "dYt")) || (st = check_ptr(W, "W")) ||
+      (st = check_ptr(dXt, "dXt")) || (st = check_ptr(dW, "dW")))
+    return st;
+  if (Yt && !aligned16(Yt)) return fail(ARD_ERR_INVALID_ARG, "Yt is not 16-byte aligned");
+  if (Xgate && !aligned16(Xgate)) return fail(ARD_ERR_INVALID_ARG, "Xgate is not 16-byte aligned");
+  if (dbias && !aligned16(dbias)) return fail(ARD_ERR_INVALID_ARG, "dbias is not 16-byte aligned");
+  if ((st = check_ws(s, desc->dtype, ws, ws_bytes))) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) return fc_bwd_impl<bf16>(desc, s, Xt, dYt, Yt, W, dXt, Xgate, dW, dbias, ws, sm);
+  return fc_bwd_impl<float>(desc, s, Xt, dYt, Yt, W, dXt, Xgate, dW, dbias, ws, sm);
 }
 
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,

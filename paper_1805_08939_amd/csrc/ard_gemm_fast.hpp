@@ -608,18 +608,18 @@ __device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg:
 // Row sums of A (RSUM, see GemmArgs::rsum) for the tile row of a workgroup
 // in tile column 0: lanes l and l + 32 of a wave hold the two k halves of
 // row 32 i + l % 32, the waves of a k split are added in LDS in split order.
+// One workgroup's output tile: position bid of an nx x ny tile grid in the
+// grouped order, batch-and-split index bzs.
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
-__global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ void fast_gemm_tile(const GemmArgs& g, int bid, int nx, int ny, int bzs, char* smem) {
   using T = typename Cfg::T;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-
   int tile_row, tile_col;
-  grouped_tile(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x, gridDim.y, tile_row, tile_col);
+  grouped_tile(bid, nx, ny, tile_row, tile_col);
   const int n0 = tile_col * Cfg::BN;
   const int m0 = tile_row * Cfg::BM;
   const int splits = g.splits > 1 ? g.splits : 1;
-  const int64_t bz = splits > 1 ? blockIdx.z / splits : blockIdx.z;
-  const int split = splits > 1 ? blockIdx.z % splits : 0;
+  const int64_t bz = splits > 1 ? bzs / splits : bzs;
+  const int split = splits > 1 ? bzs % splits : 0;
   const int wave = threadIdx.x >> 6;
   const int ks = wave / (Cfg::WGM * Cfg::WGN);
   const int wmn = wave % (Cfg::WGM * Cfg::WGN);
@@ -745,6 +745,31 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
         v = 0.0f;
       (static_cast<OutT*>(g.c.p) + bz * g.c.bstride)[o] = from_f32<OutT>(v);
     }
+  }
+}
+
+template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
+__global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  fast_gemm_tile<Cfg, AMC, BMC, OutT, EPI, RSUM>(g, blockIdx.y * gridDim.x + blockIdx.x, gridDim.x, gridDim.y,
+                                                 blockIdx.z, smem);
+}
+
+// Two independent GEMMs of one configuration in one launch (no batch, no k
+// split): the first workgroups take the tiles of g1, the rest those of g2.
+// One launch instead of two saves a kernel's fixed start and drain time, and
+// two problems too small to fill the chip alone run side by side.
+template <class Cfg, bool AMC1, bool BMC1, typename OutT1, int EPI1, bool RSUM1, bool AMC2, bool BMC2,
+          typename OutT2, int EPI2, bool RSUM2>
+__global__ void __launch_bounds__(Cfg::NT) fast_gemm_pair_kernel(GemmArgs g1, GemmArgs g2) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int nx1 = (g1.N + Cfg::BN - 1) / Cfg::BN, ny1 = (g1.M + Cfg::BM - 1) / Cfg::BM;
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < nx1 * ny1) {
+    fast_gemm_tile<Cfg, AMC1, BMC1, OutT1, EPI1, RSUM1>(g1, b, nx1, ny1, 0, smem);
+  } else {
+    const int nx2 = (g2.N + Cfg::BN - 1) / Cfg::BN, ny2 = (g2.M + Cfg::BM - 1) / Cfg::BM;
+    fast_gemm_tile<Cfg, AMC2, BMC2, OutT2, EPI2, RSUM2>(g2, b - nx1 * ny1, nx2, ny2, 0, smem);
   }
 }
 
@@ -925,6 +950,35 @@ inline hipError_t launch_fast(const GemmArgs& g, int batch, hipStream_t stream) 
                        dim3(256), 0, stream, g);
   }
   return hipGetLastError();
+}
+
+// Launches g1 and g2 (both fast_ok, splits 1, no batch) as one grid of
+// fast_gemm_pair_kernel on the 32x32 configuration of T.
+template <typename T, bool AMC1, bool BMC1, typename OutT1, int EPI1, bool RSUM1, bool AMC2, bool BMC2,
+          typename OutT2, int EPI2, bool RSUM2>
+inline hipError_t launch_fast_pair(GemmArgs g1, GemmArgs g2, hipStream_t stream) {
+  using Cfg = typename FastCfgs<T>::Small;
+  auto kern = fast_gemm_pair_kernel<Cfg, AMC1, BMC1, OutT1, EPI1, RSUM1, AMC2, BMC2, OutT2, EPI2, RSUM2>;
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::LDS);
+  if (attr != hipSuccess) return attr;
+  g1.splits = g2.splits = 1;
+  if (!RSUM1) g1.rsum = nullptr;
+  if (!RSUM2) g2.rsum = nullptr;
+  const int64_t n1 = static_cast<int64_t>((g1.N + Cfg::BN - 1) / Cfg::BN) * ((g1.M + Cfg::BM - 1) / Cfg::BM);
+  const int64_t n2 = static_cast<int64_t>((g2.N + Cfg::BN - 1) / Cfg::BN) * ((g2.M + Cfg::BM - 1) / Cfg::BM);
+  if (n1 + n2 == 0) return hipSuccess;
+  hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(n1 + n2)), dim3(Cfg::NT), Cfg::LDS, stream, g1, g2);
+  return hipGetLastError();
+}
+
+// Whether two problems run as one fast_gemm_pair_kernel launch: both take the
+// 32x32 configuration without a k split on their own, and each has a tile.
+template <typename T>
+inline bool fast_pair_ok(const GemmArgs& g1, const GemmArgs& g2) {
+  if (g1.M <= 0 || g1.N <= 0 || g2.M <= 0 || g2.N <= 0) return false;
+  const FastPlan p1 = plan_fast<T>(g1.M, g1.N, g1.K, 1, 1), p2 = plan_fast<T>(g2.M, g2.N, g2.K, 1, 1);
+  return p1.kind == FAST_SMALL && p2.kind == FAST_SMALL && p1.splits == 1 && p2.splits == 1;
 }
 
 template <typename T, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM>

@@ -63,7 +63,12 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
     api.ard_fc_fwd(desc, Xt, Wd, bd, Yt, ws)
     api.ard_fc_bwd_data(desc, dYt, Yst, Wd, dXt, ws)
     api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dW, db, ws)
+    # the layer backward in one call (one launch where both products are
+    # small): bitwise the separate calls' results
+    dXt2, dW2, db2 = (torch.full_like(t, fill) for t in (dXt, dW, db))
+    api.ard_fc_bwd(desc, Xt, dYt, Yst, Wd, dXt2, dW2, db2, ws)
     torch.cuda.synchronize()
+    assert torch.equal(dXt2, dXt) and torch.equal(dW2, dW) and torch.equal(db2, db)
     if pin != (1, 0) and not poison:
         # the same layer with the caller compacting W once: bitwise identical
         cdesc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped,
