@@ -802,10 +802,10 @@ struct FastCfgs<bf16> {
 };
 template <>
 struct FastCfgs<float> {
-  using Huge = FastCfg<float, 128, 128, 32, 4, 2, 2, 1>;  // 128 KB
+  using Huge = FastCfg<float, 128, 128, 32, 4, 2, 4, 1>;  // 128 KB, 8 waves
   using Wide = Huge;
   using Tall = Huge;
-  using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 1>;     // 96 KB
+  using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 2>;     // 96 KB, 8 waves on 32-deep k shares
   using Small = FastCfg<float, 32, 32, 128, 4, 1, 1, 8>;  // 128 KB, 8 waves on 16-deep k shares
 };
 
