@@ -118,6 +118,14 @@ class Mlp:
 
         self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l > 0 else None}
                             for l in range(self.L)]
+        # one compaction launch per step for the layers whose inputs are
+        # dropped: the marshalled arguments of every subset, built once
+        import itertools
+        self.compact_batches = {}
+        for r in range(1, self.L):
+            for sub in itertools.combinations(range(1, self.L), r):
+                self.compact_batches[sub] = api.CompactBatch([self.cdescs[l] for l in sub],
+                                                             [P["W"][l] for l in sub], [P["Wc"][l] for l in sub])
         self.order = [("fwd", l) for l in range(self.L)]
         self.order += [("bwd", l) for l in reversed(range(1, self.L))] + [("bwd_weight", 0)]
         # calls of one GEMM each: the candidates for the roofline call
@@ -173,11 +181,11 @@ class Mlp:
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, None, st, plan=self.plans[l])
         calls = dict(self.layer_calls[0][False])
+        sub = tuple(l for l in range(1, self.L) if pats[l - 1][0] > 1)
+        if sub:
+            api.ard_fc_compact_weights_batch(self.compact_batches[sub], st)
         for l in range(1, self.L):
-            compact = pats[l - 1][0] > 1
-            if compact:
-                api.ard_fc_compact_weights(self.cdescs[l], P["W"][l], P["Wc"][l], st)
-            calls.update(self.layer_calls[l][compact])
+            calls.update(self.layer_calls[l][l in sub])
         return pats, calls
 
     def step(self, it, timed_call=None, events=None):

@@ -272,6 +272,12 @@ size_t ard_fc_compact_bytes(const ard_fc_desc* desc);
 /* Gathers W[S_out][S_in] (W full, [N][K]) into Wc (device, compact bytes,
  * caller-owned); padding columns are written 0. */
 int ard_fc_compact_weights(const ard_fc_desc* desc, const void* W, void* Wc, void* stream);
+/* The same for count (1..4) layers of one dtype in one kernel launch: layer q
+ * gathers W[q] (full) into Wc[q] under descs[q]. A network's compact weights
+ * for one step's patterns come from one launch instead of one per layer.
+ * descs, W and Wc are host arrays of count entries. */
+int ard_fc_compact_weights_batch(int32_t count, const ard_fc_desc* const* descs, const void* const* W,
+                                 void* const* Wc, void* stream);
 
 /* Workspace (bytes) that fwd, bwd_data and bwd_weight of this descriptor need:
  * split-contraction partial sums for small output grids and, for FULL weights

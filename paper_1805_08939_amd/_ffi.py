@@ -86,6 +86,8 @@ SIGNATURES = {
     "ard_fc_compact_ld": (c_i32, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_compact_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_compact_weights": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp]),
+    "ard_fc_compact_weights_batch": (ctypes.c_int, [c_i32, ctypes.POINTER(ctypes.POINTER(ard_fc_desc)),
+                                                    ctypes.POINTER(c_vp), ctypes.POINTER(c_vp), c_vp]),
     "ard_fc_workspace_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,

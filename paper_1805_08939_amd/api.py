@@ -195,6 +195,24 @@ def ard_fc_compact_weights(desc, W, Wc, stream=None):
     _check(_ffi.lib().ard_fc_compact_weights(ctypes.byref(desc), _ptr(W), _ptr(Wc), _stream(stream)))
 
 
+class CompactBatch:
+    """Marshalled arguments of ard_fc_compact_weights_batch, built once and
+    reused (the descriptors are read at each call, so their plans may change)."""
+
+    def __init__(self, descs, Ws, Wcs):
+        n = len(descs)
+        self.descs = list(descs)
+        self.count = n
+        self.d = (ctypes.POINTER(ard_fc_desc) * n)(*[ctypes.pointer(x) for x in descs])
+        self.w = (ctypes.c_void_p * n)(*[_ptr(x) for x in Ws])
+        self.wc = (ctypes.c_void_p * n)(*[_ptr(x) for x in Wcs])
+
+
+def ard_fc_compact_weights_batch(batch, stream=None):
+    """Gathers the compact weights of up to 4 layers in one launch (a CompactBatch)."""
+    _check(_ffi.lib().ard_fc_compact_weights_batch(batch.count, batch.d, batch.w, batch.wc, _stream(stream)))
+
+
 def ard_fc_workspace_bytes(desc):
     return _ffi.lib().ard_fc_workspace_bytes(ctypes.byref(desc))
 

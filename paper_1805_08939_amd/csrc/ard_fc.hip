@@ -88,23 +88,39 @@ namespace {
 // chunks; else element loads), then consecutive threads write consecutive
 // kept columns.
 template <typename T>
-__global__ void __launch_bounds__(256) compact_weights_kernel(const T* __restrict__ W, int64_t K, int32_t out_period,
-                                                              int32_t out_offset, int32_t in_period, int32_t in_offset,
-                                                              int32_t kin, int64_t ldc, int32_t vec,
-                                                              T* __restrict__ Wc) {
+struct CompactJob {
+  const T* W;
+  int64_t K;
+  int32_t out_period, out_offset, in_period, in_offset, kin;
+  int64_t ldc;
+  int32_t vec;
+  T* Wc;
+  int32_t rows;  // kept output rows: one block each
+};
+
+constexpr int kMaxCompactJobs = 4;
+
+template <typename T>
+struct CompactJobs {
+  CompactJob<T> job[kMaxCompactJobs];
+  int32_t count;
+};
+
+template <typename T>
+__device__ __forceinline__ void compact_row(const CompactJob<T>& jb, int64_t i, T* seg) {
   constexpr int SEG = 4096;  // source columns per segment
   constexpr int EPC = 16 / static_cast<int>(sizeof(T));
-  __shared__ __attribute__((aligned(16))) T seg[SEG];
-  const int64_t i = blockIdx.x;
-  const T* row = W + (out_offset + static_cast<int64_t>(out_period) * i) * K;
-  T* crow = Wc + i * ldc;
+  const int64_t K = jb.K;
+  const int32_t in_period = jb.in_period, kin = jb.kin;
+  const T* row = jb.W + (jb.out_offset + static_cast<int64_t>(jb.out_period) * i) * K;
+  T* crow = jb.Wc + i * jb.ldc;
   const int t = threadIdx.x;
   if (kin > 0) {
-    const int64_t first = in_offset, last = in_offset + static_cast<int64_t>(in_period) * (kin - 1);
+    const int64_t first = jb.in_offset, last = jb.in_offset + static_cast<int64_t>(in_period) * (kin - 1);
     for (int64_t s0 = first / SEG * SEG; s0 <= last; s0 += SEG) {
       const int64_t n = K - s0 < SEG ? K - s0 : SEG;  // columns of this segment
       __syncthreads();  // the previous segment is no longer read
-      if (vec) {
+      if (jb.vec) {
         for (int64_t c = t * EPC; c < n; c += 256 * EPC)
           *reinterpret_cast<u32x4*>(seg + c) = *reinterpret_cast<const u32x4*>(row + s0 + c);
       } else {
@@ -118,7 +134,27 @@ __global__ void __launch_bounds__(256) compact_weights_kernel(const T* __restric
       for (int64_t j = jlo + t; j < jhi; j += 256) crow[j] = seg[first + in_period * j - s0];
     }
   }
-  for (int64_t j = kin + t; j < ldc; j += 256) crow[j] = from_f32<T>(0.0f);
+  for (int64_t j = kin + t; j < jb.ldc; j += 256) crow[j] = from_f32<T>(0.0f);
+}
+
+// Gathers W[S_out][S_in] into Wc[kout][ldc] for up to kMaxCompactJobs layers
+// in one launch; padding columns are 0. Kept rows and columns are arithmetic
+// progressions (source row out_offset + out_period * i, source column
+// in_offset + in_period * j). One block per compact row (the blocks of job 0
+// first): the source row passes through LDS in segments read with coalesced
+// 16-byte loads (vec: rows start 16-byte aligned and hold whole chunks; else
+// element loads), then consecutive threads write consecutive kept columns.
+template <typename T>
+__global__ void __launch_bounds__(256) compact_weights_kernel(CompactJobs<T> jobs) {
+  __shared__ __attribute__((aligned(16))) T seg[4096];
+  int64_t i = blockIdx.x;
+  for (int q = 0; q < jobs.count; ++q) {
+    if (i < jobs.job[q].rows) {
+      compact_row(jobs.job[q], i, seg);
+      return;
+    }
+    i -= jobs.job[q].rows;
+  }
 }
 
 struct FcShape {
@@ -214,13 +250,37 @@ int check_ws(const FcShape& s, int dtype, void* ws, size_t ws_bytes) {
 inline bool vec_rows(int64_t ld, size_t esize) { return (ld * static_cast<int64_t>(esize)) % 16 == 0; }
 
 template <typename T>
-hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t stream) {
-  if (s.kout == 0) return hipSuccess;
-  const int vec = aligned16(W) && (static_cast<int64_t>(s.K) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
-  hipLaunchKernelGGL(compact_weights_kernel<T>, dim3(s.kout), dim3(256), 0, stream, static_cast<const T*>(W),
-                     static_cast<int64_t>(s.K), s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, s.ldc,
-                     vec, static_cast<T*>(Wc));
+CompactJob<T> compact_job(const FcShape& s, const void* W, void* Wc) {
+  CompactJob<T> j;
+  j.W = static_cast<const T*>(W);
+  j.K = s.K;
+  j.out_period = s.out_period;
+  j.out_offset = s.out_offset;
+  j.in_period = s.in_period;
+  j.in_offset = s.in_offset;
+  j.kin = s.kin;
+  j.ldc = s.ldc;
+  j.vec = aligned16(W) && (static_cast<int64_t>(s.K) * static_cast<int64_t>(sizeof(T))) % 16 == 0;
+  j.Wc = static_cast<T*>(Wc);
+  j.rows = s.kout;
+  return j;
+}
+
+template <typename T>
+hipError_t launch_compact_jobs(const CompactJobs<T>& jobs, hipStream_t stream) {
+  int64_t rows = 0;
+  for (int q = 0; q < jobs.count; ++q) rows += jobs.job[q].rows;
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(compact_weights_kernel<T>, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, jobs);
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t stream) {
+  CompactJobs<T> jobs = {};
+  jobs.job[0] = compact_job<T>(s, W, Wc);
+  jobs.count = 1;
+  return launch_compact_jobs<T>(jobs, stream);
 }
 
 // The kept rows offset + period * i of a row-major matrix (row stride ld): a
@@ -524,6 +584,34 @@ int ard_fc_compact_weights(const ard_fc_desc* desc, const void* W, void* Wc, voi
     ARD_HIP_CHECK(launch_compact<bf16>(s, W, Wc, sm));
   } else {
     ARD_HIP_CHECK(launch_compact<float>(s, W, Wc, sm));
+  }
+  return ARD_OK;
+}
+
+int ard_fc_compact_weights_batch(int32_t count, const ard_fc_desc* const* descs, const void* const* W,
+                                 void* const* Wc, void* stream) {
+  clear_error();
+  if (count < 1 || count > kMaxCompactJobs)
+    return fail(ARD_ERR_INVALID_ARG, "count %d outside 1..%d", count, kMaxCompactJobs);
+  if (!descs || !W || !Wc) return fail(ARD_ERR_INVALID_ARG, "descs, W or Wc is NULL");
+  CompactJobs<float> jf = {};
+  CompactJobs<bf16> jb = {};
+  const int dtype = descs[0] ? descs[0]->dtype : -1;
+  for (int q = 0; q < count; ++q) {
+    FcShape s;
+    int st = check_desc(descs[q], &s);
+    if (st != ARD_OK) return st;
+    if (descs[q]->dtype != dtype) return fail(ARD_ERR_INVALID_ARG, "descs[%d]: dtypes differ", q);
+    if ((st = check_ptr(W[q], "W")) || (st = check_ptr(Wc[q], "Wc"))) return st;
+    jf.job[q] = compact_job<float>(s, W[q], Wc[q]);
+    jb.job[q] = compact_job<bf16>(s, W[q], Wc[q]);
+  }
+  jf.count = jb.count = count;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (dtype == ARD_BF16) {
+    ARD_HIP_CHECK(launch_compact_jobs<bf16>(jb, sm));
+  } else {
+    ARD_HIP_CHECK(launch_compact_jobs<float>(jf, sm));
   }
   return ARD_OK;
 }

@@ -391,3 +391,41 @@ def test_fp32_full_weights_with_input_gather(B, K, N, pin, pout):
     Yg, dXg = Yg.T, dXg.T
     assert not Yg[np.setdiff1d(np.arange(N), Sout)].any() and not dXg[np.setdiff1d(np.arange(K), Sin)].any()
 
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_compact_weights_batch(dtype):
+    """One launch for several layers' compact weights: each equals the gather
+    W[S_out][S_in] (padding columns 0), bitwise the single-layer call."""
+    d = device()
+    sdt = synth.storage_dtype(dtype)
+    layers = [(130, 70, (3, 1), (2, 0)), (10, 2048, (5, 4), (1, 0)), (4104, 36, (1, 0), (7, 3))]
+    descs, Ws, Wcs, singles = [], [], [], []
+    for i, (K, N, pin, pout) in enumerate(layers):
+        g = synth.generator(40 + i)
+        W = synth.to_storage(synth.normal(g, (N, K)), dtype)
+        desc = api.fc_desc(ard_dtype(dtype), 8, K, N, row_plan(K, *pin, with_list=False),
+                           row_plan(N, *pout, with_list=False), 1.0, api.ARD_ACT_NONE, api.ARD_DROPPED_SKIP,
+                           api.ARD_WEIGHTS_COMPACT)
+        n = max(api.ard_fc_compact_bytes(desc) // (2 if dtype == "bf16" else 4), 1)
+        Wc = torch.full((n,), 5.0, dtype=sdt, device=d)
+        one = torch.full((n,), 5.0, dtype=sdt, device=d)
+        api.ard_fc_compact_weights(desc, to_dev(W), one)
+        descs.append(desc)
+        Ws.append(to_dev(W))
+        Wcs.append(Wc)
+        singles.append((one, W, K, N, pin, pout, api.ard_fc_compact_ld(desc)))
+    batch = api.CompactBatch(descs, Ws, Wcs)
+    api.ard_fc_compact_weights_batch(batch)
+    torch.cuda.synchronize()
+    for Wc, (one, W, K, N, pin, pout, ldc) in zip(Wcs, singles):
+        assert torch.equal(Wc, one)
+        Sin, Sout = opat.row_kept_list(K, *pin), opat.row_kept_list(N, *pout)
+        got = f64(Wc[:len(Sout) * ldc].view(len(Sout), ldc))
+        assert np.array_equal(got[:, :len(Sin)], f64(W)[np.ix_(Sout, Sin)])
+        assert not got[:, len(Sin):].any()
+    with pytest.raises(api.ArdError):
+        api.ard_fc_compact_weights_batch(api.CompactBatch(descs * 2, Ws * 2, Wcs * 2))  # 6 > 4 layers
+    other = api.fc_desc(api.ARD_BF16 if dtype == "f32" else api.ARD_F32, 8, 130, 70)
+    with pytest.raises(api.ArdError):
+        api.ard_fc_compact_weights_batch(api.CompactBatch([descs[0], other], Ws[:2], Wcs[:2]))
