@@ -134,6 +134,43 @@ class Mlp:
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
 
+    # ------------------------------------------------------- conventional dropout
+    def set_conventional(self, p):
+        """The same network under conventional dropout (Sec. II-C), the paper's
+        baseline: dense layer GEMMs (the p = 0 calls) and a Bernoulli(1 - p)
+        element mask, drawn per step on the device, on each hidden layer's
+        output (forward) and output derivative (backward)."""
+        import torch
+        api = self.api
+        self.conv_p = p
+        if not hasattr(self, "masks"):
+            self.masks = [torch.zeros((self.dims[l + 1] * self.B + 31) // 32, dtype=torch.int32, device="cuda")
+                          for l in range(self.L - 1)]
+            self.ptr["mask"] = [m.data_ptr() for m in self.masks]
+        self.dense = []
+        for l in range(self.L):
+            act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
+            self.dense.append(api.fc_desc(self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], None, None, 1.0, act,
+                                          api.ARD_DROPPED_SKIP))
+
+    def conventional_step(self, it):
+        api, P, st, L, B = self.api, self.ptr, self.stream, self.L, self.B
+        acts = [P["X0"]] + P["Y"]
+        ws = (self.ws.data_ptr(), self.ws.numel() * 4)
+        d, dt, p = self.dense, self.ard_dtype, self.conv_p
+        for l in range(L):
+            api.ard_fc_fwd(d[l], acts[l], P["W"][l], P["bias"][l], P["Y"][l], ws, st)
+            if l < L - 1:
+                api.ard_dropout_fwd(dt, self.dims[l + 1], B, p, 1.0, PATTERN_SEED, l + 1, it, P["Y"][l],
+                                    P["mask"][l], st)
+        for l in reversed(range(1, L)):
+            if l < L - 1:
+                api.ard_dropout_bwd(dt, self.dims[l + 1], B, 1.0, P["mask"][l], P["dY"][l], st)
+            api.ard_fc_bwd(d[l], acts[l], P["dY"][l], None, P["W"][l], P["dY"][l - 1], P["dW"][l], P["db"][l], ws, st,
+                           Xgate=acts[l])
+        api.ard_dropout_bwd(dt, self.dims[1], B, 1.0, P["mask"][0], P["dY"][0], st)
+        api.ard_fc_bwd_weight(d[0], acts[0], P["dY"][0], None, P["dW"][0], P["db"][0], ws, st)
+
     def kept(self, pats):
         api = self.api
         n = [self.dims[0]]
@@ -463,6 +500,22 @@ def time_steps(wl, steps, warmup, it0, timed_call=None):
             "call_shapes": shapes}
 
 
+def time_conventional(wl, steps, warmup, it0):
+    """GPU ms of `steps` conventional-dropout steps after `warmup` untimed ones
+    (the same timing as the approximate-dropout steps)."""
+    import torch
+    for i in range(warmup):
+        wl.conventional_step(it0 + i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        wl.conventional_step(it0 + warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end)
+
+
 def roofline_call(wl, first_it, steps):
     """The one-GEMM call with the most kept work over the timed steps (summed kept
     FLOPs; ties go to the first call of a step). The patterns are seeded, so
@@ -702,6 +755,23 @@ def main():
         print(f"# p={p}: {r['ms'] / args.steps:.4f} ms/step, kept {r['flops'] / args.steps / 1e9:.3f} GFLOP/step, "
               f"{r['flops'] / (r['ms'] * 1e-3) / 1e12:.3f} TFLOP/s", file=sys.stderr, flush=True)
 
+    # the paper's own baseline (Sec. II-C, Sec. IV): conventional dropout on the
+    # same network, dense GEMMs plus element masks, at the same rates
+    conventional = None
+    if hasattr(wl, "conventional_step"):
+        conventional = {"ms_per_step": {}, "speedup_vs_conventional": {}, "training_time_reduction": {}}
+        for i, p in enumerate(rates):
+            if p == 0.0:
+                continue
+            wl.set_conventional(p)
+            ms = time_conventional(wl, args.steps, args.warmup, 5_000_000 * (i + 1)) / args.steps
+            ard_ms = results[p]["ms"] / args.steps
+            conventional["ms_per_step"][f"{p}"] = ms
+            conventional["speedup_vs_conventional"][f"{p}"] = ms / ard_ms
+            conventional["training_time_reduction"][f"{p}"] = 1.0 - ard_ms / ms
+            print(f"# conventional dropout p={p}: {ms:.4f} ms/step ({ms / ard_ms:.3f}x the approximate step)",
+                  file=sys.stderr, flush=True)
+
     head = results[args.p]
     value = head["flops"] / (head["ms"] * 1e-3) / 1e12
     t0 = results[0.0]["ms"]
@@ -749,6 +819,11 @@ def main():
         "roofline": roofline,
         "k_search": k_search,
     }
+    if conventional is not None:
+        out["conventional_dropout"] = dict(
+            conventional, definition="dense layer GEMMs (the p = 0 kernels) plus a Bernoulli(1 - p) element mask "
+                                     "kernel on each hidden output and its derivative; speedup = its step time / "
+                                     "the approximate-dropout step time at the same p")
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.p, args.cpu_budget)
     print(json.dumps(out), flush=True)

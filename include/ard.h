@@ -313,6 +313,26 @@ int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const v
                void* dXt, const void* Xgate, float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Conventional dropout, the baseline the method replaces (device).         */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. II-C: conventional dropout keeps every GEMM dense and multiplies a
+ * layer's output by a random 0/1 mask, and the output derivative by the same
+ * mask in the backward pass. Element e = j * batch + b of the feature-major
+ * Yt[n][batch] (dtype ARD_F32 or ARD_BF16) is kept iff draw e of the
+ * counter-based sequence of (seed, stream_id, iter) -- the generator of the
+ * pattern sampler -- as a 53-bit uniform is >= p: an independent
+ * Bernoulli(1 - p) per element. fwd multiplies Yt in place by scale (kept) or
+ * 0 and writes the mask bits (bit e in word e / 32; ceil(n * batch / 32)
+ * words, device, caller-owned, 4-byte aligned); bwd multiplies dYt in place by
+ * scale * mask. p in [0, 1); stream_id < 2^24, iter < 2^40.
+ */
+int ard_dropout_fwd(int32_t dtype, int32_t n, int32_t batch, double p, float scale, uint64_t seed,
+                    uint32_t stream_id, uint64_t iter, void* Yt, uint32_t* mask, void* stream);
+int ard_dropout_bwd(int32_t dtype, int32_t n, int32_t batch, float scale, const uint32_t* mask, void* dYt,
+                    void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Layer under a tile pattern (device).                                     */
 /* ------------------------------------------------------------------------ */
 /*

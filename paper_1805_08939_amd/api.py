@@ -242,6 +242,18 @@ def ard_fc_bwd(desc, Xt, dYt, Yt, W, dXt, dW, dbias, ws=None, stream=None, Xgate
                                  _ptr(Xgate), _ptr(dW), _ptr(dbias), p, n, _stream(stream)))
 
 
+# --------------------------------------------------------------------------- conventional dropout
+
+def ard_dropout_fwd(dtype, n, batch, p, scale, seed, stream_id, iteration, Yt, mask, stream=None):
+    """Bernoulli dropout of Yt[n][batch] in place; mask receives the keep bits."""
+    _check(_ffi.lib().ard_dropout_fwd(dtype, n, batch, p, scale, seed, stream_id, iteration, _ptr(Yt), _ptr(mask),
+                                      _stream(stream)))
+
+
+def ard_dropout_bwd(dtype, n, batch, scale, mask, dYt, stream=None):
+    _check(_ffi.lib().ard_dropout_bwd(dtype, n, batch, scale, _ptr(mask), _ptr(dYt), _stream(stream)))
+
+
 # --------------------------------------------------------------------------- tile layer
 
 def tile_desc(dtype, batch, in_features, out_features, scale=1.0, dropped=ARD_DROPPED_ZERO):
