@@ -153,6 +153,21 @@ class Mlp:
             self.dense.append(api.fc_desc(self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], None, None, 1.0, act,
                                           api.ARD_DROPPED_SKIP))
 
+    def sgd_step(self, dense):
+        """Momentum SGD on every layer (lr 1e-6, momentum 0.9; the cost does not
+        depend on the values): on the approximate path restricted to the
+        step's kept weights, on the conventional one dense."""
+        import torch
+        api, P, st = self.api, self.ptr, self.stream
+        if not hasattr(self, "V"):
+            self.V = [torch.zeros_like(w) for w in self.dW]
+            self.Vb = [torch.zeros_like(b) for b in self.db]
+            P["V"], P["Vb"] = [v.data_ptr() for v in self.V], [v.data_ptr() for v in self.Vb]
+        descs = self.dense if dense else self.descs
+        for l in range(self.L):
+            api.ard_fc_sgd_momentum(descs[l], P["W"][l], P["V"][l], P["dW"][l], P["bias"][l], P["Vb"][l], P["db"][l],
+                                    1e-6, 0.9, st)
+
     def conventional_step(self, it):
         api, P, st, L, B = self.api, self.ptr, self.stream, self.L, self.B
         acts = [P["X0"]] + P["Y"]
@@ -516,6 +531,29 @@ def time_conventional(wl, steps, warmup, it0):
     return start.elapsed_time(end)
 
 
+def time_training(wl, steps, warmup, it0, conventional):
+    """GPU ms of `steps` training steps (a step of the path, or of the
+    conventional network, followed by the momentum-SGD update of every layer)."""
+    import torch
+
+    def one(it):
+        if conventional:
+            wl.conventional_step(it)
+        else:
+            wl.step(it)
+        wl.sgd_step(conventional)
+    for i in range(warmup):
+        one(it0 + i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        one(it0 + warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end)
+
+
 def roofline_call(wl, first_it, steps):
     """The one-GEMM call with the most kept work over the timed steps (summed kept
     FLOPs; ties go to the first call of a step). The patterns are seeded, so
@@ -772,6 +810,28 @@ def main():
             print(f"# conventional dropout p={p}: {ms:.4f} ms/step ({ms / ard_ms:.3f}x the approximate step)",
                   file=sys.stderr, flush=True)
 
+    # whole training steps: the same comparison with the optimizer update of
+    # every layer after each step (the weights are restored afterwards)
+    training = None
+    if hasattr(wl, "sgd_step"):
+        saved = [w.clone() for w in wl.W]
+        training = {"approximate_ms": {}, "conventional_ms": {}, "training_time_reduction": {}}
+        for i, p in enumerate(rates):
+            if p == 0.0:
+                continue
+            wl.set_rate(p)
+            a_ms = time_training(wl, args.steps, args.warmup, 7_000_000 * (i + 1), False) / args.steps
+            wl.set_conventional(p)
+            c_ms = time_training(wl, args.steps, args.warmup, 8_000_000 * (i + 1), True) / args.steps
+            training["approximate_ms"][f"{p}"] = a_ms
+            training["conventional_ms"][f"{p}"] = c_ms
+            training["training_time_reduction"][f"{p}"] = 1.0 - a_ms / c_ms
+            print(f"# training step p={p}: approximate {a_ms:.4f} ms, conventional {c_ms:.4f} ms",
+                  file=sys.stderr, flush=True)
+        for w, s0 in zip(wl.W, saved):
+            w.copy_(s0)
+        del saved
+
     head = results[args.p]
     value = head["flops"] / (head["ms"] * 1e-3) / 1e12
     t0 = results[0.0]["ms"]
@@ -819,6 +879,10 @@ def main():
         "roofline": roofline,
         "k_search": k_search,
     }
+    if training is not None:
+        out["training_step"] = dict(training, definition="a step as above followed by momentum SGD (lr 1e-6, "
+                                    "momentum 0.9) on every layer: restricted to the step's kept weights on the "
+                                    "approximate path, dense under conventional dropout")
     if conventional is not None:
         out["conventional_dropout"] = dict(
             conventional, definition="dense layer GEMMs (the p = 0 kernels) plus a Bernoulli(1 - p) element mask "

@@ -312,6 +312,21 @@ int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, 
 int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt, const void* W,
                void* dXt, const void* Xgate, float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * SGD with momentum restricted to the kept weights of the layer's patterns
+ * (the update of a training step around the path; Sec. IV trains with
+ * momentum SGD): for every kept output row n and kept input column k,
+ *   V[n][k] = momentum * V[n][k] + dW[n][k],  W[n][k] -= lr * V[n][k],
+ * and for the kept rows' bias entries the same with Vb, dbias. W is the full
+ * [N][K] matrix of the descriptor's dtype (its weight_layout is ignored), V,
+ * dW [N][K] fp32, bias, Vb, dbias [N] fp32 (all three given or all NULL).
+ * Dropped weights, their momentum and their bias entries are left untouched:
+ * they are frozen for the step (the reading of an update restricted to the
+ * kept rows). All device, caller-owned.
+ */
+int ard_fc_sgd_momentum(const ard_fc_desc* desc, void* W, float* V, const float* dW, float* bias, float* Vb,
+                        const float* dbias, float lr, float momentum, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Conventional dropout, the baseline the method replaces (device).         */
 /* ------------------------------------------------------------------------ */

@@ -59,3 +59,30 @@ def fc_backward(X, W, Y, dY, m_in, m_out, scale=1.0, act="none"):
     dW = (G.T @ X) * np.outer(m_out, m_in)
     db = G.sum(axis=0)
     return dX, dW, db
+
+
+def sgd_momentum(W, V, dW, m_out, m_in, lr, mu, b=None, Vb=None, db=None):
+    """Momentum SGD restricted to the kept weights (the update of a training
+    step around the method; Sec. IV trains with momentum SGD).
+
+    Reading: a weight is updated in a step iff its output row and input column
+    are both kept; dropped weights and their momentum stay as they are, and a
+    bias entry is updated iff its row is kept. For the kept entries:
+        V <- mu * V + dW,   W <- W - lr * V.
+    Returns (W, V) or (W, V, b, Vb) as new fp64 arrays.
+    """
+    W = np.array(W, dtype=np.float64)
+    V = np.array(V, dtype=np.float64)
+    keep = np.outer(m_out, m_in) > 0
+    Vn = mu * V + np.asarray(dW, dtype=np.float64)
+    V = np.where(keep, Vn, V)
+    W = np.where(keep, W - lr * V, W)
+    if b is None:
+        return W, V
+    b = np.array(b, dtype=np.float64)
+    Vb = np.array(Vb, dtype=np.float64)
+    rows = np.asarray(m_out) > 0
+    Vbn = mu * Vb + np.asarray(db, dtype=np.float64)
+    Vb = np.where(rows, Vbn, Vb)
+    b = np.where(rows, b - lr * Vb, b)
+    return W, V, b, Vb

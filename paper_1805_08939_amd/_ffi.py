@@ -94,6 +94,8 @@ SIGNATURES = {
                                        c_size, c_vp]),
     "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                          c_size, c_vp]),
+    "ard_fc_sgd_momentum": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_f32,
+                                           c_f32, c_vp]),
     "ard_dropout_fwd": (ctypes.c_int, [c_i32, c_i32, c_i32, c_f64, c_f32, c_u64, c_u32, c_u64, c_vp, c_vp, c_vp]),
     "ard_dropout_bwd": (ctypes.c_int, [c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp]),
     "ard_fc_bwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,

@@ -242,6 +242,12 @@ def ard_fc_bwd(desc, Xt, dYt, Yt, W, dXt, dW, dbias, ws=None, stream=None, Xgate
                                  _ptr(Xgate), _ptr(dW), _ptr(dbias), p, n, _stream(stream)))
 
 
+def ard_fc_sgd_momentum(desc, W, V, dW, bias, Vb, dbias, lr, momentum, stream=None):
+    """Momentum SGD on the kept weights (and kept bias entries) of the descriptor's patterns."""
+    _check(_ffi.lib().ard_fc_sgd_momentum(ctypes.byref(desc), _ptr(W), _ptr(V), _ptr(dW), _ptr(bias), _ptr(Vb),
+                                          _ptr(dbias), lr, momentum, _stream(stream)))
+
+
 # --------------------------------------------------------------------------- conventional dropout
 
 def ard_dropout_fwd(dtype, n, batch, p, scale, seed, stream_id, iteration, Yt, mask, stream=None):

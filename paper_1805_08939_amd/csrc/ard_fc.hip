@@ -43,6 +43,35 @@ __global__ void zero_dropped_weights_kernel(float* __restrict__ dW, int32_t K, i
     if (!row_kept || (c % in_period) != in_offset) row[c] = 0.0f;
 }
 
+// SGD with momentum restricted to the kept weights of a row pattern: for kept
+// rows n = out_offset + out_period i and kept columns k = in_offset +
+// in_period j, V = mu V + dW and W -= lr V; the same for the bias entries of
+// kept rows. Dropped weights, their momentum and their bias entries keep their
+// values (frozen for the step). One block per kept row.
+template <typename T>
+__global__ void __launch_bounds__(256) sgd_momentum_kernel(T* __restrict__ W, float* __restrict__ V,
+                                                           const float* __restrict__ dW, int32_t K,
+                                                           int32_t out_period, int32_t out_offset, int32_t in_period,
+                                                           int32_t in_offset, int32_t kin, float* __restrict__ bias,
+                                                           float* __restrict__ Vb, const float* __restrict__ db,
+                                                           float lr, float mu) {
+  const int64_t n = out_offset + static_cast<int64_t>(out_period) * blockIdx.x;
+  T* w = W + n * K;
+  float* v = V + n * K;
+  const float* g = dW + n * K;
+  for (int64_t j = threadIdx.x; j < kin; j += 256) {
+    const int64_t k = in_offset + static_cast<int64_t>(in_period) * j;
+    const float vn = mu * v[k] + g[k];
+    v[k] = vn;
+    w[k] = from_f32<T>(to_f32(w[k]) - lr * vn);
+  }
+  if (threadIdx.x == 0 && bias) {
+    const float vb = mu * Vb[n] + db[n];
+    Vb[n] = vb;
+    bias[n] -= lr * vb;
+  }
+}
+
 // dbias[r] = scale * sum_b G[r][b] for the kept rows r = offset + period * i,
 // with G = dY * [Y > 0] when Y is given, else dY. One wave per kept row: each
 // lane sums its 16-byte chunks of the row in order, then the lanes are summed
@@ -613,6 +642,32 @@ int ard_fc_compact_weights_batch(int32_t count, const ard_fc_desc* const* descs,
   } else {
     ARD_HIP_CHECK(launch_compact_jobs<float>(jf, sm));
   }
+  return ARD_OK;
+}
+
+int ard_fc_sgd_momentum(const ard_fc_desc* desc, void* W, float* V, const float* dW, float* bias, float* Vb,
+                        const float* dbias, float lr, float momentum, void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if (!W || !V || !dW) return fail(ARD_ERR_INVALID_ARG, "W, V or dW is NULL");
+  if ((bias == nullptr) != (Vb == nullptr) || (bias == nullptr) != (dbias == nullptr))
+    return fail(ARD_ERR_INVALID_ARG, "bias, Vb and dbias must be all given or all NULL");
+  if (reinterpret_cast<uintptr_t>(W) % s.esize || reinterpret_cast<uintptr_t>(V) % 4 ||
+      reinterpret_cast<uintptr_t>(dW) % 4)
+    return fail(ARD_ERR_INVALID_ARG, "W, V or dW is not aligned to its element size");
+  if (!(lr == lr) || !(momentum == momentum)) return fail(ARD_ERR_INVALID_ARG, "lr and momentum must be numbers");
+  if (s.kout == 0) return ARD_OK;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16)
+    hipLaunchKernelGGL(sgd_momentum_kernel<bf16>, dim3(s.kout), dim3(256), 0, sm, static_cast<bf16*>(W), V, dW, s.K,
+                       s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr, momentum);
+  else
+    hipLaunchKernelGGL(sgd_momentum_kernel<float>, dim3(s.kout), dim3(256), 0, sm, static_cast<float*>(W), V, dW,
+                       s.K, s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr,
+                       momentum);
+  ARD_LAUNCH_CHECK();
   return ARD_OK;
 }
 

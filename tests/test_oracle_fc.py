@@ -134,3 +134,36 @@ def test_rate_zero_is_the_plain_layer():
     Y = fc.fc_forward(X, W, None, ones_in, ones_out)
     want = [[sum(X[s][k] * W[n][k] for k in range(3)) for n in range(4)] for s in range(2)]
     assert np.allclose(Y, want, rtol=1e-14, atol=0)
+
+
+def test_sgd_momentum_pinned_to_torch_sgd():
+    """The restricted update equals torch.optim.SGD(momentum, no dampening) on
+    the kept entries over several steps (a library routine), leaves dropped
+    entries and their momentum as they were, and with nothing dropped is
+    torch's update of the whole matrix."""
+    import torch
+    rng = np.random.default_rng(5)
+    N, K, lr, mu = 7, 9, 0.01, 0.9
+    for (po, oo), (pi, oi) in [((1, 0), (1, 0)), ((2, 1), (3, 0)), ((4, 3), (1, 0))]:
+        m_out, m_in = patterns.row_mask(N, po, oo), patterns.row_mask(K, pi, oi)
+        W0 = rng.standard_normal((N, K))
+        b0 = rng.standard_normal(N)
+        rows = np.flatnonzero(m_out)
+        cols = np.flatnonzero(m_in)
+        Wt = torch.tensor(W0[np.ix_(rows, cols)], requires_grad=True)
+        bt = torch.tensor(b0[rows], requires_grad=True)
+        opt = torch.optim.SGD([Wt, bt], lr=lr, momentum=mu)
+        W, V, b, Vb = W0.copy(), np.zeros((N, K)), b0.copy(), np.zeros(N)
+        for _ in range(3):
+            dW = rng.standard_normal((N, K))
+            db = rng.standard_normal(N)
+            opt.zero_grad()
+            Wt.grad = torch.tensor(dW[np.ix_(rows, cols)])
+            bt.grad = torch.tensor(db[rows])
+            opt.step()
+            W, V, b, Vb = fc.sgd_momentum(W, V, dW, m_out, m_in, lr, mu, b, Vb, db)
+        np.testing.assert_allclose(W[np.ix_(rows, cols)], Wt.detach().numpy(), rtol=1e-14, atol=1e-15)
+        np.testing.assert_allclose(b[rows], bt.detach().numpy(), rtol=1e-14, atol=1e-15)
+        dropped = np.outer(m_out, m_in) == 0
+        assert np.array_equal(W[dropped], W0[dropped]) and not V[dropped].any()
+        assert np.array_equal(b[m_out == 0], b0[m_out == 0]) and not Vb[m_out == 0].any()
