@@ -384,6 +384,45 @@ class TileLayer:
         self._host = tuple(synth.as_f64(t).numpy() for t in self._host_src)
 
 
+class TileLayerTdp(TileLayer):
+    """The same layer under the paper's tile-based pattern (Sec. III-B): each
+    step draws (dp, offset) from K(p) and keeps the tiles t = tn * tiles_k + tk
+    with t mod dp == offset. The bitmaps of every (dp, offset) are built once on
+    the device; a step plans the drawn one there."""
+
+    def __init__(self, **kw):
+        super().__init__(**kw)
+        self.config["patterns"] = "tile-based (dp, offset) per step from K(p), n_max 16"
+        self.tdp_bits = {}
+
+    def set_rate(self, p):
+        api, torch = self.api, self.torch
+        self.p = p
+        self.Kdist, _ = api.ard_search_distribution(p)
+        for per in range(1, len(self.Kdist) + 1):
+            for off in range(per):
+                if (per, off) not in self.tdp_bits:
+                    bits = api.ard_tile_bitmap_tdp(self.tn, self.tk, per, off)
+                    dev = torch.from_numpy(bits.view("int32").copy()).to("cuda")
+                    self.tdp_bits[(per, off)] = (dev, api.ard_bitmap_popcount(bits, self.tn * self.tk), bits)
+
+    def patterns(self, it):
+        per, off = self.api.ard_sample_row_pattern(self.Kdist, PATTERN_SEED, 0, it)
+        _, nnz, bits = self.tdp_bits[(per, off)]
+        return bits, nnz, (per, off)
+
+    def prepare(self, it):
+        api = self.api
+        _, nnz, _ = pats = self.patterns(it)
+        dbits = self.tdp_bits[pats[2]][0]
+        plan = api.ard_plan_tiles(self.N, self.K, self.tile, dbits, nnz, self.plan_ws, self.stream)
+        d, st = self.desc, self.stream
+        calls = {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
+                 ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
+                 ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
+        return it, calls
+
+
 class Lstm:
     """One LSTM layer whose hidden units take a row-based pattern sampled per
     sequence from K(p): the gate GEMMs run on the kept hidden set (forward, then
@@ -475,6 +514,8 @@ WORKLOADS = {
                    dtype="f32", init="xavier", seed=1805 + 1),
     "tile4096": dict(cls="TileLayer", name="tile-4096x4096-bf16-b512-t64", n=4096, k=4096, batch=512, tile=64,
                      dtype="bf16", seed=1805 + 2, w_std=0.02),
+    "tile4096tdp": dict(cls="TileLayerTdp", name="tile-4096x4096-bf16-b512-t64-tdp", n=4096, k=4096, batch=512,
+                        tile=64, dtype="bf16", seed=1805 + 2, w_std=0.02),
     "lstm1024": dict(cls="Lstm", name="lstm-t35-b64-i1024-h1024-fp32", T=35, batch=64, inputs=1024, hidden=1024,
                      dtype="f32", seed=1805 + 3),
     "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
@@ -764,7 +805,7 @@ def main():
     from paper_1805_08939_amd import _ffi
     _ffi.lib()
     spec = dict(WORKLOADS[args.workload])
-    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "Lstm": Lstm}[spec.pop("cls")]
+    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm}[spec.pop("cls")]
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:
