@@ -16,6 +16,11 @@ Gate order i, f, g, o; W = [W_ih | W_hh] stored as W[4H][I + H]:
     c_t = m * (f * c_{t-1} + i * g)
     h_t = m * (o * tanh(c_t))
 
+An optional input mask m_in (the hidden-unit pattern of the layer below, when
+layers are stacked) removes dropped inputs the same way: the layer sees
+x_t * m_in, so the input columns of dropped inputs take no part in any
+product, and their entries of dX are 0.
+
 Logical layout: X [T][B][I], h0 and c0 [B][H], outputs Hs [T][B][H].
 Back-propagation through time takes dHs [T][B][H] (the derivative of the loss
 with respect to every h_t) and optional extra derivatives dhT, dcT of the final
@@ -29,9 +34,11 @@ def _sigmoid(z):
     return 1.0 / (1.0 + np.exp(-z))
 
 
-def lstm_forward(X, W, b, m, h0=None, c0=None):
+def lstm_forward(X, W, b, m, h0=None, c0=None, m_in=None):
     """Returns (Hs, hT, cT, cache)."""
     X = np.asarray(X, np.float64)
+    if m_in is not None:
+        X = X * np.asarray(m_in, np.float64)[None, None, :]
     W = np.asarray(W, np.float64)
     T, B, I = X.shape
     H = W.shape[0] // 4
@@ -57,12 +64,14 @@ def lstm_forward(X, W, b, m, h0=None, c0=None):
     return Hs, h, c, cache
 
 
-def lstm_backward(X, W, m, cache, dHs, dhT=None, dcT=None):
+def lstm_backward(X, W, m, cache, dHs, dhT=None, dcT=None, m_in=None):
     """Manual back-propagation through time of ``lstm_forward``.
 
     Returns (dX, dW, db, dh0, dc0).
     """
     X = np.asarray(X, np.float64)
+    if m_in is not None:
+        X = X * np.asarray(m_in, np.float64)[None, None, :]
     W = np.asarray(W, np.float64)
     dHs = np.asarray(dHs, np.float64)
     T, B, I = X.shape
@@ -93,4 +102,6 @@ def lstm_backward(X, W, m, cache, dHs, dhT=None, dcT=None):
         db += dz.sum(axis=0)
         dh_next = m * (dz @ Wh)              # the input was m * h_{t-1}
         dc_next = dc * f
+    if m_in is not None:                     # the input was x_t * m_in
+        dX = dX * np.asarray(m_in, np.float64)[None, None, :]
     return dX, dW, db, dh_next, dc_next

@@ -86,6 +86,33 @@ def test_masked_equals_compact_torch_lstm(period, offset):
     assert np.allclose(dc0[:, S], r[7], rtol=1e-12, atol=1e-13) and not dc0[:, dropped].any()
 
 
+@pytest.mark.parametrize("pin,ph", [((3, 1), (2, 0)), ((2, 0), (1, 0)), ((4, 3), (3, 2))])
+def test_input_mask_equals_compact_torch_lstm(pin, ph):
+    """An input pattern (the hidden pattern of the layer below): kept units
+    equal a torch.nn.LSTM of input size |S_in| and hidden size |S| on the
+    kept inputs, dX is torch's gradient at kept inputs and 0 at dropped ones,
+    and the input columns of dropped inputs get no weight gradient."""
+    T, B, I, H = 4, 2, 9, 6
+    X, W, b, h0, c0, dHs, dhT, dcT = make(T, B, I, H, 31 + pin[0])
+    Sin, S = patterns.row_kept_list(I, *pin), patterns.row_kept_list(H, *ph)
+    m_in, m = patterns.row_mask(I, *pin), patterns.row_mask(H, *ph)
+    Hs, hT, cT, cache = lstm.lstm_forward(X, W, b, m, h0, c0, m_in=m_in)
+    dX, dW, db, dh0, dc0 = lstm.lstm_backward(X, W, m, cache, dHs, dhT, dcT, m_in=m_in)
+    rows = [g * H + j for g in range(4) for j in S]
+    cols = list(Sin) + [I + j for j in S]
+    r = torch_lstm(X[:, :, Sin], W[np.ix_(rows, cols)], b[rows], h0[:, S], c0[:, S], dHs[:, :, S], dhT[:, S],
+                   dcT[:, S], len(Sin), len(S))
+    assert np.allclose(Hs[:, :, S], r[0], rtol=1e-12, atol=1e-13)
+    assert np.allclose(dX[:, :, Sin], r[3], rtol=1e-12, atol=1e-13)
+    dropped_in = [k for k in range(I) if k not in Sin]
+    assert not dX[:, :, dropped_in].any()
+    dWfull = np.zeros_like(W)
+    dWfull[np.ix_(rows, cols)] = r[4]
+    assert np.allclose(dW, dWfull, rtol=1e-12, atol=1e-13)
+    assert np.allclose(db[rows], r[5], rtol=1e-12, atol=1e-13)
+    assert np.allclose(dh0[:, S], r[6], rtol=1e-12, atol=1e-13)
+
+
 def test_backward_is_the_derivative_of_forward():
     T, B, I, H = 3, 2, 2, 4
     X, W, b, h0, c0, dHs, dhT, dcT = make(T, B, I, H, 42)
