@@ -509,6 +509,122 @@ class Lstm:
         self._host = tuple(synth.as_f64(t).numpy() for t in self._host_src)
 
 
+class LstmStack:
+    """Stacked LSTM layers (Sec. IV-C's language model shape), each with a
+    hidden-unit pattern sampled per sequence from K(p); a layer's input rows
+    are the layer below's hidden units, so its input plan is that layer's
+    pattern and its input products shrink with it (K-side compaction).
+    Forward through the stack, then BPTT backward from the top, the top
+    layer's dX being the layer below's dHs."""
+
+    def __init__(self, name, T, batch, inputs, hidden, layers, dtype, seed):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.T, self.B, self.I, self.H, self.NL, self.dtype = name, T, batch, inputs, hidden, layers, dtype
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        X = synth.uniform(g, (T, batch, inputs), 0.1)
+        self.X = X.permute(0, 2, 1).contiguous().to(dev)
+        self.Ws, self.bs, self.Hs, self.dX, self.dW, self.db, self.ws, self.idx = [], [], [], [], [], [], [], []
+        self.plans = [api.ard_row_plan() for _ in range(layers)]
+        for l in range(layers):
+            i = inputs if l == 0 else hidden
+            self.Ws.append(synth.uniform(g, (4 * hidden, i + hidden), 0.1).to(dev))
+            self.bs.append(synth.uniform(g, (4 * hidden,), 0.1).to(dev))
+            self.Hs.append(torch.empty(T, hidden, batch, device=dev))
+            self.dX.append(torch.empty(T, i, batch, device=dev))
+            self.dW.append(torch.empty(4 * hidden, i + hidden, device=dev))
+            self.db.append(torch.empty(4 * hidden, device=dev))
+            self.idx.append(torch.empty(hidden, dtype=torch.int32, device=dev))
+            full = api.ard_plan_rows(hidden, 1, 0, self.idx[l])  # the largest kept set bounds the workspace
+            nbytes = api.ard_lstm_workspace_bytes(api.lstm_desc(api.ARD_F32, T, batch, i, hidden, full))
+            self.ws.append(torch.empty(max(nbytes, 16) // 4 + 1, device=dev))
+        self.dHs = synth.normal(g, (T, batch, hidden)).permute(0, 2, 1).contiguous().to(dev)
+        self.descs = [api.lstm_desc(api.ARD_F32, T, batch, inputs if l == 0 else hidden, hidden, self.plans[l],
+                                    self.plans[l - 1] if l > 0 else None) for l in range(layers)]
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.order = [("fwd", 0), ("bwd", 0)]
+        self.config = {"workload": name, "global_batch": batch, "seq_len": T, "input": inputs, "hidden": hidden,
+                       "layers": layers,
+                       "patterns": "row-based on each layer's hidden units, sampled per sequence from K(p), n_max 16; "
+                                   "each layer's input plan is the pattern of the layer below"}
+
+    def set_rate(self, p):
+        self.p = p
+        self.K, _ = self.api.ard_search_distribution(p)
+
+    def patterns(self, it):
+        return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.NL)]
+
+    def kept(self, pats):
+        return [self.api.ard_row_kept(self.H, *pt) for pt in pats]
+
+    def kept_flops(self, pats):
+        S = self.kept(pats)
+        f = 0.0
+        for l in range(self.NL):
+            ic = self.I if l == 0 else S[l - 1]
+            f += 2.0 * self.T * self.B * (ic + S[l]) * 4 * S[l]
+        per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
+        return 3.0 * f, per
+
+    def gemm_shape(self, pats, kind, l):
+        return tuple([self.T, self.B, self.I] + self.kept(pats))
+
+    def shape_label(self, shape):
+        return "T, B, I = %d, %d, %d, kept hidden units per layer %s" % (shape[0], shape[1], shape[2],
+                                                                          list(shape[3:]))
+
+    def prepare(self, it):
+        api, st = self.api, self.stream
+        pats = self.patterns(it)
+        for l, pt in enumerate(pats):
+            api.ard_plan_rows(self.H, *pt, self.idx[l], st, plan=self.plans[l])
+
+        def fwd():
+            for l in range(self.NL):
+                x = self.X if l == 0 else self.Hs[l - 1]
+                api.ard_lstm_fwd(self.descs[l], x, self.Ws[l], self.bs[l], None, None, self.Hs[l], None, None,
+                                 self.ws[l], st)
+
+        def bwd():
+            for l in reversed(range(self.NL)):
+                x = self.X if l == 0 else self.Hs[l - 1]
+                dh = self.dHs if l == self.NL - 1 else self.dX[l + 1]
+                api.ard_lstm_bwd(self.descs[l], x, dh, None, None, self.ws[l], self.dX[l] if l > 0 else None,
+                                 self.dW[l], self.db[l], None, None, st)
+        return pats, {("fwd", 0): (fwd, (), {}), ("bwd", 0): (bwd, (), {})}
+
+    step = Mlp.step
+    replay = Mlp.replay
+
+    def host_copies(self):
+        self._host = {"X": self.X.double().cpu().numpy().transpose(0, 2, 1),
+                      "W": [w.double().cpu().numpy() for w in self.Ws],
+                      "b": [b.double().cpu().numpy() for b in self.bs],
+                      "dHs": self.dHs.double().cpu().numpy().transpose(0, 2, 1)}
+
+    def oracle_step(self, pats):
+        """The stack through the fp64 oracle (one sequence)."""
+        from oracle import lstm as olstm
+        from oracle import patterns as opat
+        X = self._host["X"]
+        masks = [opat.row_mask(self.H, *pt) for pt in pats]
+        caches = []
+        for l in range(self.NL):
+            W, b = self._host["W"][l], self._host["b"][l]
+            m_in = masks[l - 1] if l > 0 else None
+            Hs, _, _, cache = olstm.lstm_forward(X, W, b, masks[l], m_in=m_in)
+            caches.append((X, W, cache, m_in))
+            X = Hs
+        dH = self._host["dHs"]
+        for l in reversed(range(self.NL)):
+            Xl, W, cache, m_in = caches[l]
+            dH = olstm.lstm_backward(Xl, W, masks[l], cache, dH, m_in=m_in)[0]
+        return dH
+
+
 WORKLOADS = {
     "mlp784": dict(cls="Mlp", name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
                    dtype="f32", init="xavier", seed=1805 + 1),
@@ -518,6 +634,10 @@ WORKLOADS = {
                         tile=64, dtype="bf16", seed=1805 + 2, w_std=0.02),
     "lstm1024": dict(cls="Lstm", name="lstm-t35-b64-i1024-h1024-fp32", T=35, batch=64, inputs=1024, hidden=1024,
                      dtype="f32", seed=1805 + 3),
+    "lstm2x1500": dict(cls="LstmStack", name="lstm-2x1500-t35-b20-fp32", T=35, batch=20, inputs=1500, hidden=1500,
+                       layers=2, dtype="f32", seed=1805 + 5),
+    "lstm2x1500b40": dict(cls="LstmStack", name="lstm-2x1500-t35-b40-fp32", T=35, batch=40, inputs=1500,
+                          hidden=1500, layers=2, dtype="f32", seed=1805 + 5),
     "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
                     dtype="bf16", init="he", seed=1805 + 4),
 }
@@ -805,7 +925,8 @@ def main():
     from paper_1805_08939_amd import _ffi
     _ffi.lib()
     spec = dict(WORKLOADS[args.workload])
-    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm}[spec.pop("cls")]
+    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm,
+           "LstmStack": LstmStack}[spec.pop("cls")]
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:

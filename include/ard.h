@@ -397,6 +397,12 @@ int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, co
  * (extra derivatives of the final state, NULL = 0) -> dX[T][I][B], dW[4H][I+H]
  * fp32, dbias[4H] fp32, dh0 and dc0 [H][B] (each output may be NULL). Entries
  * of dropped units are written 0. Only ARD_F32 is supported.
+ * input_plan (stacked layers): the hidden pattern of the layer below, whose
+ * dropped units are this layer's dropped inputs. The layer then reads only the
+ * kept rows of X (a strided view, no list needed) and compacts the matching
+ * input columns of W, so the input products shrink by the kept fraction too;
+ * the result is the layer applied to X with dropped input rows taken as 0,
+ * and the dX rows and dW input columns of dropped inputs are written 0.
  */
 typedef struct {
   int32_t dtype;
@@ -406,6 +412,7 @@ typedef struct {
   int32_t hidden_size; /* H >= 1 */
   int32_t reserved;
   const ard_row_plan* hidden_plan;  /* n == H, or NULL = no dropout */
+  const ard_row_plan* input_plan;   /* n == I, or NULL = every input kept */
 } ard_lstm_desc;
 
 size_t ard_lstm_workspace_bytes(const ard_lstm_desc* desc);

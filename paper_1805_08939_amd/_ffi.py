@@ -58,7 +58,7 @@ class ard_tile_desc(ctypes.Structure):
 class ard_lstm_desc(ctypes.Structure):
     _fields_ = [("dtype", c_i32), ("seq_len", c_i32), ("batch", c_i32), ("input_size", c_i32),
                 ("hidden_size", c_i32), ("reserved", c_i32),
-                ("hidden_plan", ctypes.POINTER(ard_row_plan))]
+                ("hidden_plan", ctypes.POINTER(ard_row_plan)), ("input_plan", ctypes.POINTER(ard_row_plan))]
 
 
 # name -> (restype, argtypes); every symbol the header declares.

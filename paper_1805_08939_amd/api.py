@@ -283,9 +283,10 @@ def ard_tile_bwd_weight(desc, plan, Xt, dYt, dW, stream=None):
 
 # --------------------------------------------------------------------------- LSTM layer
 
-def lstm_desc(dtype, seq_len, batch, input_size, hidden_size, hidden_plan=None):
-    d = ard_lstm_desc(dtype, seq_len, batch, input_size, hidden_size, 0, _plan_ptr(hidden_plan))
-    d._keep = hidden_plan
+def lstm_desc(dtype, seq_len, batch, input_size, hidden_size, hidden_plan=None, input_plan=None):
+    d = ard_lstm_desc(dtype, seq_len, batch, input_size, hidden_size, 0, _plan_ptr(hidden_plan),
+                      _plan_ptr(input_plan))
+    d._keep = (hidden_plan, input_plan)
     return d
 
 

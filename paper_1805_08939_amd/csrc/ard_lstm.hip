@@ -36,6 +36,7 @@ namespace {
 
 struct Layout {
   int64_t T, B, I, H, ns, G4, KW, S;
+  int64_t Ic, ip, io;  // kept inputs (compact input width) and their pattern
   size_t wc, bc, rowmap, z, cc, hc, da, dc, part, total;
 };
 
@@ -60,7 +61,11 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
   L.H = d->hidden_size;
   L.ns = ns;
   L.G4 = 4 * static_cast<int64_t>(ns);
-  L.KW = (L.I + ns + 3) / 4 * 4;  // compact rows padded to 16 bytes (zeros past I + |S|)
+  const bool in_all = !d->input_plan || d->input_plan->period == 1;
+  L.Ic = in_all ? L.I : d->input_plan->kept;
+  L.ip = in_all ? 1 : d->input_plan->period;
+  L.io = in_all ? 0 : d->input_plan->offset;
+  L.KW = (L.Ic + ns + 3) / 4 * 4;  // compact rows padded to 16 bytes (zeros past Ic + |S|)
   L.S = bwd_splits(ns, L.B);
   size_t off = 0;
   L.wc = off;     off += al256(4 * L.G4 * L.KW);
@@ -84,16 +89,16 @@ __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x))
 // Compact weights (rows of KW >= I + |S| entries, zero past I + |S|), bias
 // and row map; one block per compact row 4u + g.
 __global__ void lstm_prepare_kernel(const float* __restrict__ W, const float* __restrict__ bias,
-                                    const int32_t* __restrict__ idx, int32_t I, int32_t H, int32_t ns,
-                                    int32_t KW, float* __restrict__ Wc, float* __restrict__ bc,
-                                    int32_t* __restrict__ rowmap) {
+                                    const int32_t* __restrict__ idx, int32_t I, int32_t Ic, int32_t ip,
+                                    int32_t io, int32_t H, int32_t ns, int32_t KW, float* __restrict__ Wc,
+                                    float* __restrict__ bc, int32_t* __restrict__ rowmap) {
   const int r = blockIdx.x;
   const int u = r >> 2, g = r & 3;
   const int64_t src = static_cast<int64_t>(g) * H + unit_row(idx, u);
   const float* wrow = W + src * (I + H);
   float* crow = Wc + static_cast<int64_t>(r) * KW;
   for (int c = threadIdx.x; c < KW; c += blockDim.x)
-    crow[c] = c < I ? wrow[c] : c < I + ns ? wrow[I + unit_row(idx, c - I)] : 0.0f;
+    crow[c] = c < Ic ? wrow[io + static_cast<int64_t>(ip) * c] : c < Ic + ns ? wrow[I + unit_row(idx, c - Ic)] : 0.0f;
   if (threadIdx.x == 0) {
     bc[r] = bias ? bias[src] : 0.0f;
     rowmap[r] = static_cast<int32_t>(src);
@@ -126,15 +131,16 @@ __global__ void lstm_zero_dropped_rows_kernel(float* __restrict__ out, int64_t r
   for (int c = threadIdx.x; c < cols; c += blockDim.x) out[r * cols + c] = 0.0f;
 }
 
-// dW[4H][I+H]: zero the rows of dropped units and the recurrent columns of
-// dropped units; dbias entries of dropped units.
+// dW[4H][I+H]: zero the rows of dropped units, the recurrent columns of
+// dropped units and the input columns of dropped inputs (pattern ip, io);
+// dbias entries of dropped units.
 __global__ void lstm_zero_dropped_dw_kernel(float* __restrict__ dW, float* __restrict__ dbias, int32_t I,
-                                            int32_t H, int32_t period, int32_t offset) {
+                                            int32_t H, int32_t period, int32_t offset, int32_t ip, int32_t io) {
   const int r = blockIdx.x;
   const bool row_kept = ((r % H) % period) == offset;
   float* row = dW + static_cast<int64_t>(r) * (I + H);
   for (int c = threadIdx.x; c < I + H; c += blockDim.x)
-    if (!row_kept || (c >= I && ((c - I) % period) != offset)) row[c] = 0.0f;
+    if (!row_kept || (c >= I ? ((c - I) % period) != offset : (c % ip) != io)) row[c] = 0.0f;
   if (threadIdx.x == 0 && dbias && !row_kept) dbias[r] = 0.0f;
 }
 
@@ -424,6 +430,8 @@ int check_lstm(const ard_lstm_desc* d, int32_t* ns, int32_t* period, int32_t* of
     return fail(ARD_ERR_INVALID_ARG, "sizes must be >= 1");
   int st = check_row_plan(d->hidden_plan, d->hidden_size, "hidden_plan", true);
   if (st != ARD_OK) return st;
+  if ((st = check_row_plan(d->input_plan, d->input_size, "input_plan", false)) != ARD_OK) return st;
+  if (d->input_plan && d->input_plan->kept == 0) return fail(ARD_ERR_INVALID_ARG, "input_plan keeps no input");
   const bool all = !d->hidden_plan || d->hidden_plan->period == 1;
   *ns = all ? d->hidden_size : d->hidden_plan->kept;
   *period = all ? 1 : d->hidden_plan->period;
@@ -456,7 +464,7 @@ LstmStep step_args(const Layout& L, char* w, const int32_t* idx) {
   s.dA = reinterpret_cast<float*>(w + L.da);
   s.dc = reinterpret_cast<float*>(w + L.dc);
   s.B = static_cast<int32_t>(L.B);
-  s.I = static_cast<int32_t>(L.I);
+  s.I = static_cast<int32_t>(L.Ic);  // compact input width: the recurrent columns of Wc start here
   s.H = static_cast<int32_t>(L.H);
   s.ns = static_cast<int32_t>(L.ns);
   s.G4 = static_cast<int32_t>(L.G4);
@@ -508,7 +516,8 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   }
 
   hipLaunchKernelGGL(lstm_prepare_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm,
-                     static_cast<const float*>(W), bias, idx, s.I, s.H, ns, s.KW, const_cast<float*>(s.Wc),
+                     static_cast<const float*>(W), bias, idx, static_cast<int32_t>(L.I), s.I,
+                     static_cast<int32_t>(L.ip), static_cast<int32_t>(L.io), s.H, ns, s.KW, const_cast<float*>(s.Wc),
                      reinterpret_cast<float*>(w + L.bc), reinterpret_cast<int32_t*>(w + L.rowmap));
   ARD_LAUNCH_CHECK();
   const int64_t nsB = static_cast<int64_t>(ns) * L.B;
@@ -524,7 +533,8 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   g.N = s.B;
   g.K = s.I;
   g.a = {s.Wc, nullptr, L.KW, nullptr, nullptr, 0, 0, 1.0f, 0};
-  g.b = {X, nullptr, L.B, nullptr, nullptr, L.I * L.B, 0, 1.0f, 0};
+  // the kept input rows io + ip * k of X[t]: a strided view
+  g.b = {static_cast<const float*>(X) + L.io * L.B, nullptr, L.ip * L.B, nullptr, nullptr, L.I * L.B, 0, 1.0f, 0};
   g.c = {s.Z, L.B, nullptr, nullptr, L.G4 * L.B, reinterpret_cast<const float*>(w + L.bc), 0, 1.0f};
   const bool kw_vec = L.KW % 4 == 0;
   const bool b_vec = L.B % 4 == 0 && L.I % 4 == 0;
@@ -536,7 +546,7 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   }
 
   const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((L.G4 + 31) / 32));
-  const bool avec = kw_vec && L.I % 4 == 0, bvec = L.B % 4 == 0;
+  const bool avec = kw_vec && L.Ic % 4 == 0, bvec = L.B % 4 == 0;
   // direct loads: aligned rows, and every chunk offset of a slab below 2^31 bytes
   const bool step_fast = avec && bvec && aligned16(s.Wc) &&
                          (L.G4 + 1) * L.KW * 4 < (int64_t{1} << 31) && (L.ns + 64) * L.B * 4 < (int64_t{1} << 31);
@@ -630,7 +640,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     gr.M = ns;
     gr.N = s.B;
     gr.K = static_cast<int32_t>(L.G4 / fs);
-    gr.a = {s.Wc + L.I, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
+    gr.a = {s.Wc + L.Ic, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
     gr.b = {s.dA, nullptr, L.B, nullptr, nullptr, gr.K * L.B, 0, 1.0f, 0};
     gr.c = {part, L.B, nullptr, nullptr, nsB, nullptr, 0, 1.0f};
     rec_fast = fast_ok(gr, sizeof(float));
@@ -641,7 +651,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   }
   const dim3 rgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32),
                    static_cast<unsigned>(splits));
-  const bool vec = L.KW % 4 == 0 && L.I % 4 == 0 && L.B % 4 == 0;
+  const bool vec = L.KW % 4 == 0 && L.Ic % 4 == 0 && L.B % 4 == 0;
   for (int t = static_cast<int>(L.T) - 1; t >= 0; --t) {
     if (t == 0 && !dh0) break;
     s.t = t;
@@ -695,9 +705,10 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     g.K = s.B;
     g.kbatch = static_cast<int32_t>(L.T);
     g.a = {s.dA, nullptr, 4 * L.B, nullptr, nullptr, L.B, 0, 1.0f, L.G4 * L.B};
-    g.b = {X, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
-    g.c = {dW + static_cast<int64_t>(offset) * colsW, period * colsW, nullptr, nullptr, L.H * colsW, nullptr, 0,
-           1.0f};
+    g.b = {static_cast<const float*>(X) + L.io * L.B, nullptr, L.ip * L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
+    g.c = {dW + static_cast<int64_t>(offset) * colsW + L.io, period * colsW, nullptr, nullptr, L.H * colsW, nullptr,
+           0, 1.0f};
+    g.c.col_stride = L.ip;
     GemmArgs gr = g;  // recurrent columns
     gr.N = ns;
     gr.b = {s.Hc, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, nsB};
@@ -725,8 +736,9 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     g.K = s.B;
     g.kbatch = static_cast<int32_t>(L.T);
     g.a = {s.dA, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.G4 * L.B};
-    g.b = {X, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
-    g.c = {dW, colsW, rowmap, nullptr, 0, nullptr, 0, 1.0f};
+    g.b = {static_cast<const float*>(X) + L.io * L.B, nullptr, L.ip * L.B, nullptr, nullptr, 0, 0, 1.0f, L.I * L.B};
+    g.c = {dW + L.io, colsW, rowmap, nullptr, 0, nullptr, 0, 1.0f};
+    g.c.col_stride = L.ip;
     ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
         g, 1, bv, bv && L.I % 4 == 0, sm)));
     g.N = ns;
@@ -741,10 +753,11 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
                        static_cast<int32_t>(L.T), static_cast<int32_t>(L.G4), s.B, dbias);
     ARD_LAUNCH_CHECK();
   }
-  if (period > 1 && (dW || dbias)) {
+  if ((period > 1 && (dW || dbias)) || (L.ip > 1 && dW)) {
     if (dW) {
       hipLaunchKernelGGL(lstm_zero_dropped_dw_kernel, dim3(static_cast<unsigned>(rowsW)), dim3(256), 0, sm, dW,
-                         dbias, s.I, s.H, period, offset);
+                         dbias, static_cast<int32_t>(L.I), s.H, period, offset, static_cast<int32_t>(L.ip),
+                         static_cast<int32_t>(L.io));
     } else {
       hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(rowsW)), dim3(64), 0, sm,
                          dbias, rowsW, 1, s.H, period, offset);
@@ -759,12 +772,19 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     g.K = static_cast<int32_t>(L.G4);
     g.a = {s.Wc, nullptr, L.KW, nullptr, nullptr, 0, 0, 1.0f, 0};
     g.b = {s.dA, nullptr, L.B, nullptr, nullptr, L.G4 * L.B, 0, 1.0f, 0};
-    g.c = {dX, L.B, nullptr, nullptr, L.I * L.B, nullptr, 0, 1.0f};
+    // rows io + ip * k of dX[t]; the rows of dropped inputs are written 0
+    g.c = {static_cast<float*>(dX) + L.io * L.B, L.ip * L.B, nullptr, nullptr, L.I * L.B, nullptr, 0, 1.0f};
     if (fast_ok(g, sizeof(float))) {
       ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(g, static_cast<int>(L.T), sm, nullptr)));
     } else {
       ARD_HIP_CHECK((run_gemm<float, float, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
-          g, static_cast<int>(L.T), L.KW % 4 == 0 && L.I % 4 == 0, bv, sm)));
+          g, static_cast<int>(L.T), L.KW % 4 == 0 && L.Ic % 4 == 0, bv, sm)));
+    }
+    if (L.ip > 1) {
+      hipLaunchKernelGGL(lstm_zero_dropped_rows_kernel, dim3(static_cast<unsigned>(L.T * L.I)), dim3(256), 0, sm,
+                         static_cast<float*>(dX), L.T * L.I, s.B, static_cast<int32_t>(L.I),
+                         static_cast<int32_t>(L.ip), static_cast<int32_t>(L.io));
+      ARD_LAUNCH_CHECK();
     }
   }
   return ARD_OK;

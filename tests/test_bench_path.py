@@ -84,3 +84,43 @@ def test_mlp784_step_against_oracle(mlp, p):
                 keep_in = m_in > 0
                 ndX = (np.abs(G) @ np.abs(W[l])) * m_in[None, :] * gate
                 compare(got_dX[:, keep_in], (dX * gate)[:, keep_in], ndX[:, keep_in], F32_TOL, f"dX{l} it{it}")
+
+
+def test_lstm_stack_step_against_oracle():
+    """Two stacked LSTM layers as the benchmark's stacked workload runs them
+    (each layer's hidden pattern from K(p), the upper layer's input plan the
+    lower layer's pattern, BPTT from the top): every layer's outputs and
+    gradients against the oracle's stack, normwise per tensor."""
+    import bench
+    from oracle import lstm as olstm
+    st = bench.LstmStack("stack", T=4, batch=8, inputs=48, hidden=40, layers=2, dtype="f32", seed=3)
+    st.set_rate(0.5)
+    it = next(i for i in range(200) if all(pt[0] > 1 for pt in st.patterns(i)))
+    for i in (it, 0):
+        pats = st.step(i)
+        torch.cuda.synchronize()
+        st.host_copies()
+        masks = [opat.row_mask(st.H, *pt) for pt in pats]
+        X = st._host["X"]
+        caches = []
+        for l in range(st.NL):
+            m_in = masks[l - 1] if l > 0 else None
+            Hs, _, _, cache = olstm.lstm_forward(X, st._host["W"][l], st._host["b"][l], masks[l], m_in=m_in)
+            got = st.Hs[l].double().cpu().numpy().transpose(0, 2, 1)
+            err = np.abs(got - Hs).max() / np.abs(Hs).max()
+            assert err <= F32_TOL, f"Hs{l}: {err:.3e}"
+            caches.append((X, cache, m_in))
+            X = Hs
+        dH = st._host["dHs"]
+        for l in reversed(range(st.NL)):
+            Xl, cache, m_in = caches[l]
+            dX, dW, db, _, _ = olstm.lstm_backward(Xl, st._host["W"][l], masks[l], cache, dH, m_in=m_in)
+            for name, got, want in (("dW", st.dW[l], dW), ("db", st.db[l], db)):
+                g = got.double().cpu().numpy()
+                err = np.abs(g - want).max() / np.abs(want).max()
+                assert err <= F32_TOL, f"{name}{l}: {err:.3e}"
+            if l > 0:
+                g = st.dX[l].double().cpu().numpy().transpose(0, 2, 1)
+                err = np.abs(g - dX).max() / np.abs(dX).max()
+                assert err <= F32_TOL, f"dX{l}: {err:.3e}"
+            dH = dX

@@ -24,7 +24,7 @@ def check(got, want, what, tol=TOL):
     return err
 
 
-def run_lstm(T, B, I, H, pattern, seed, with_state=True, with_final_grads=True, a=0.1):
+def run_lstm(T, B, I, H, pattern, seed, with_state=True, with_final_grads=True, a=0.1, in_pattern=(1, 0)):
     g = synth.generator(seed)
     X = synth.uniform(g, (T, B, I), a)
     W = synth.uniform(g, (4 * H, I + H), a)
@@ -35,15 +35,21 @@ def run_lstm(T, B, I, H, pattern, seed, with_state=True, with_final_grads=True, 
     dhT = synth.normal(g, (B, H)) if with_final_grads else None
     dcT = synth.normal(g, (B, H)) if with_final_grads else None
     m = opat.row_mask(H, *pattern)
+    m_in = opat.row_mask(I, *in_pattern)
     Hs64, hT64, cT64, cache = olstm.lstm_forward(f64(X), f64(W), f64(b), m,
-                                                 None if h0 is None else f64(h0), None if c0 is None else f64(c0))
+                                                 None if h0 is None else f64(h0), None if c0 is None else f64(c0),
+                                                 m_in=m_in)
     dX64, dW64, db64, dh064, dc064 = olstm.lstm_backward(
-        f64(X), f64(W), m, cache, f64(dHs), None if dhT is None else f64(dhT), None if dcT is None else f64(dcT))
+        f64(X), f64(W), m, cache, f64(dHs), None if dhT is None else f64(dhT), None if dcT is None else f64(dcT),
+        m_in=m_in)
 
     plan = None if pattern == (1, 0) else row_plan(H, *pattern)
-    desc = api.lstm_desc(api.ARD_F32, T, B, I, H, plan)
+    in_plan = None if in_pattern == (1, 0) else row_plan(I, *in_pattern, with_list=False)
+    desc = api.lstm_desc(api.ARD_F32, T, B, I, H, plan, in_plan)
     ws = torch.empty(api.ard_lstm_workspace_bytes(desc) // 4 + 1, dtype=torch.float32, device=device())
     Xd = to_dev(X.permute(0, 2, 1))      # [T][I][B]
+    if in_plan is not None:  # dropped inputs must never be read
+        Xd[:, torch.from_numpy(m_in == 0).to(device())] = float("nan")
     Wd, bd = to_dev(W), to_dev(b)
     h0d = to_dev(h0.T) if h0 is not None else None
     c0d = to_dev(c0.T) if c0 is not None else None
@@ -72,6 +78,19 @@ def run_lstm(T, B, I, H, pattern, seed, with_state=True, with_final_grads=True, 
     dropped = m == 0
     assert not f64(Hs)[:, dropped].any() and not f64(dW)[np.tile(dropped, 4)].any()
     return Hs
+
+
+@pytest.mark.parametrize("shape,pattern,in_pattern", [
+    ((3, 5, 6, 10), (2, 1), (3, 1)),         # unaligned: the register-staged paths
+    ((2, 8, 12, 10), (3, 0), (2, 1)),
+    ((2, 8, 12, 10), (1, 0), (4, 3)),
+    ((4, 64, 96, 200), (2, 1), (3, 2)),      # aligned: the direct-load GEMMs and step kernels
+    ((8, 64, 512, 384), (2, 0), (2, 1)),
+])
+def test_input_pattern(shape, pattern, in_pattern):
+    """Stacked layers: the input rows dropped by the layer below are skipped
+    (the input products and the input columns of W shrink with them)."""
+    run_lstm(*shape, pattern, seed=sum(shape), in_pattern=in_pattern)
 
 
 @pytest.mark.parametrize("pattern", [(1, 0), (2, 1), (3, 0), (7, 6), (16, 12)])
