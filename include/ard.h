@@ -423,6 +423,41 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
                  const void* dcT, void* ws, size_t ws_bytes, void* dX, float* dW, float* dbias,
                  void* dh0, void* dc0, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* LSTM layer with a tile pattern on its weights (device).                  */
+/* ------------------------------------------------------------------------ */
+/*
+ * The tile-based pattern (Sec. III-B) applied to an LSTM's matrix products
+ * (Sec. IV-C): with M the kept-tile mask of W = [W_ih | W_hh] (4H x (I + H),
+ * tiles of weight_plan, built by ard_plan_tiles / ard_plan_tiles_bernoulli
+ * over n = 4H, k = I + H), every gate product uses W * M:
+ *   z_t = (W * M) [x_t; h_{t-1}] + bias,  i, f, o = sigmoid, g = tanh,
+ *   c_t = f * c_{t-1} + i * g,  h_t = o * tanh(c_t)   (every unit kept).
+ * Only kept tiles of W are read, and dW = M * dL/d(W * M) is computed on kept
+ * tiles only (0 elsewhere). Layouts as for ard_lstm_fwd (fp32 only); 4H and
+ * I + H must be multiples of the plan's tile. The workspace
+ * (ard_lstm_tile_workspace_bytes) holds the stacked inputs and saved gates
+ * from fwd to bwd: bwd must get the fwd call's workspace, unmodified. bwd
+ * outputs may be NULL.
+ */
+typedef struct {
+  int32_t dtype;
+  int32_t seq_len;
+  int32_t batch;
+  int32_t input_size;
+  int32_t hidden_size;
+  int32_t reserved;
+  const ard_tile_plan* weight_plan;
+} ard_lstm_tile_desc;
+
+size_t ard_lstm_tile_workspace_bytes(const ard_lstm_tile_desc* desc);
+int ard_lstm_tile_fwd(const ard_lstm_tile_desc* desc, const void* X, const void* W, const float* bias,
+                      const void* h0, const void* c0, void* Hs, void* hT, void* cT, void* ws, size_t ws_bytes,
+                      void* stream);
+int ard_lstm_tile_bwd(const ard_lstm_tile_desc* desc, const void* W, const void* dHs, const void* dhT,
+                      const void* dcT, void* ws, size_t ws_bytes, void* dX, float* dW, float* dbias, void* dh0,
+                      void* dc0, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

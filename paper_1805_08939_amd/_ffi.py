@@ -61,6 +61,11 @@ class ard_lstm_desc(ctypes.Structure):
                 ("hidden_plan", ctypes.POINTER(ard_row_plan)), ("input_plan", ctypes.POINTER(ard_row_plan))]
 
 
+class ard_lstm_tile_desc(ctypes.Structure):
+    _fields_ = [("dtype", c_i32), ("seq_len", c_i32), ("batch", c_i32), ("input_size", c_i32),
+                ("hidden_size", c_i32), ("reserved", c_i32), ("weight_plan", ctypes.POINTER(ard_tile_plan))]
+
+
 # name -> (restype, argtypes); every symbol the header declares.
 SIGNATURES = {
     "ard_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -107,6 +112,11 @@ SIGNATURES = {
     "ard_tile_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
                                            c_vp, c_vp, c_vp, c_vp]),
     "ard_lstm_workspace_bytes": (c_size, [ctypes.POINTER(ard_lstm_desc)]),
+    "ard_lstm_tile_workspace_bytes": (c_size, [ctypes.POINTER(ard_lstm_tile_desc)]),
+    "ard_lstm_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_tile_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                         c_vp, c_vp, c_size, c_vp]),
+    "ard_lstm_tile_bwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_tile_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size,
+                                         c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "ard_lstm_fwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_desc), c_vp, c_vp, c_vp, c_vp, c_vp,
                                     c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "ard_lstm_bwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_desc), c_vp, c_vp, c_vp, c_vp, c_vp,

@@ -13,7 +13,7 @@ from . import _ffi
 from ._ffi import (ARD_ACT_NONE, ARD_ACT_RELU, ARD_BF16, ARD_DROPPED_SKIP, ARD_DROPPED_ZERO,  # noqa: F401
                    ARD_ERR_INVALID_ARG, ARD_ERR_NOT_CONVERGED, ARD_F32, ARD_SEARCH_MIRROR, ARD_SEARCH_PLAIN,
                    ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_FULL,
-                   ard_fc_desc, ard_lstm_desc, ard_row_plan, ard_search_info, ard_search_opts,
+                   ard_fc_desc, ard_lstm_desc, ard_lstm_tile_desc, ard_row_plan, ard_search_info, ard_search_opts,
                    ard_tile_desc, ard_tile_plan)
 
 
@@ -305,3 +305,28 @@ def ard_lstm_bwd(desc, X, dHs, dhT, dcT, ws, dX, dW, dbias, dh0, dc0, stream=Non
     _check(_ffi.lib().ard_lstm_bwd(ctypes.byref(desc), _ptr(X), _ptr(dHs), _ptr(dhT), _ptr(dcT),
                                    _ptr(ws), nbytes, _ptr(dX), _ptr(dW), _ptr(dbias), _ptr(dh0),
                                    _ptr(dc0), _stream(stream)))
+
+
+# --------------------------------------------------------------------------- LSTM under a tile pattern
+
+def lstm_tile_desc(dtype, seq_len, batch, input_size, hidden_size, weight_plan):
+    d = ard_lstm_tile_desc(dtype, seq_len, batch, input_size, hidden_size, 0, ctypes.pointer(weight_plan))
+    d._keep = weight_plan
+    return d
+
+
+def ard_lstm_tile_workspace_bytes(desc):
+    return _ffi.lib().ard_lstm_tile_workspace_bytes(ctypes.byref(desc))
+
+
+def ard_lstm_tile_fwd(desc, X, W, bias, h0, c0, Hs, hT, cT, ws, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(_ffi.lib().ard_lstm_tile_fwd(ctypes.byref(desc), _ptr(X), _ptr(W), _ptr(bias), _ptr(h0), _ptr(c0),
+                                        _ptr(Hs), _ptr(hT), _ptr(cT), _ptr(ws), nbytes, _stream(stream)))
+
+
+def ard_lstm_tile_bwd(desc, W, dHs, dhT, dcT, ws, dX, dW, dbias, dh0, dc0, stream=None):
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(_ffi.lib().ard_lstm_tile_bwd(ctypes.byref(desc), _ptr(W), _ptr(dHs), _ptr(dhT), _ptr(dcT), _ptr(ws),
+                                        nbytes, _ptr(dX), _ptr(dW), _ptr(dbias), _ptr(dh0), _ptr(dc0),
+                                        _stream(stream)))
