@@ -625,6 +625,98 @@ class LstmStack:
         return dH
 
 
+class LstmTile:
+    """One LSTM layer whose weight matrix W[4H][I+H] takes the paper's tile
+    pattern, (dp, offset) drawn from K(p) per sequence over its 64 x 64 tiles:
+    the gate products read only kept tiles, the weight gradient is computed on
+    kept tiles only; every hidden unit is kept."""
+
+    def __init__(self, name, T, batch, inputs, hidden, tile, dtype, seed):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.T, self.B, self.I, self.H, self.tile, self.dtype = name, T, batch, inputs, hidden, tile, dtype
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        self.X = synth.uniform(g, (T, batch, inputs), 0.1).permute(0, 2, 1).contiguous().to(dev)
+        self.W = synth.uniform(g, (4 * hidden, inputs + hidden), 0.1).to(dev)
+        self.b = synth.uniform(g, (4 * hidden,), 0.1).to(dev)
+        self.dHs = synth.normal(g, (T, batch, hidden)).permute(0, 2, 1).contiguous().to(dev)
+        self.Hs = torch.empty(T, hidden, batch, device=dev)
+        self.dX = torch.empty(T, inputs, batch, device=dev)
+        self.dW = torch.empty(4 * hidden, inputs + hidden, device=dev)
+        self.db = torch.empty(4 * hidden, device=dev)
+        self.tn, self.tk = 4 * hidden // tile, (inputs + hidden) // tile
+        self.plan_ws = torch.empty(max(api.ard_tile_plan_workspace_bytes(self.tn, self.tk), 16) // 4,
+                                   dtype=torch.int32, device=dev)
+        self.tdp_bits = {}
+        self.ws = None
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.order = [("fwd", 0), ("bwd", 0)]
+        self.config = {"workload": name, "global_batch": batch, "seq_len": T, "input": inputs, "hidden": hidden,
+                       "tile": tile, "patterns": "tile-based (dp, offset) on W per sequence from K(p), n_max 16"}
+
+    def set_rate(self, p):
+        api, torch = self.api, self.torch
+        self.p = p
+        self.Kdist, _ = api.ard_search_distribution(p)
+        for per in range(1, len(self.Kdist) + 1):
+            for off in range(per):
+                if (per, off) not in self.tdp_bits:
+                    bits = api.ard_tile_bitmap_tdp(self.tn, self.tk, per, off)
+                    dev = torch.from_numpy(bits.view("int32").copy()).to("cuda")
+                    self.tdp_bits[(per, off)] = (dev, api.ard_bitmap_popcount(bits, self.tn * self.tk))
+
+    def patterns(self, it):
+        return [self.api.ard_sample_row_pattern(self.Kdist, PATTERN_SEED, 1, it)]
+
+    def kept_flops(self, pats):
+        nnz = self.tdp_bits[tuple(pats[0])][1]
+        f = 2.0 * self.T * self.B * nnz * self.tile * self.tile
+        per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
+        return 3.0 * f, per
+
+    def gemm_shape(self, pats, kind, l):
+        return (self.T, self.B, self.I, self.H, self.tdp_bits[tuple(pats[0])][1])
+
+    @staticmethod
+    def shape_label(shape):
+        return "T, B, I, H = %d, %d, %d, %d, %d kept 64 x 64 tiles of W" % tuple(shape)
+
+    def prepare(self, it):
+        api, st = self.api, self.stream
+        pats = self.patterns(it)
+        dbits, nnz = self.tdp_bits[tuple(pats[0])]
+        plan = api.ard_plan_tiles(4 * self.H, self.I + self.H, self.tile, dbits, nnz, self.plan_ws, st)
+        d = api.lstm_tile_desc(api.ARD_F32, self.T, self.B, self.I, self.H, plan)
+        if self.ws is None:
+            self.ws = self.torch.empty(api.ard_lstm_tile_workspace_bytes(d) // 4 + 1, device="cuda")
+        calls = {("fwd", 0): (api.ard_lstm_tile_fwd, (d, self.X, self.W, self.b, None, None, self.Hs, None, None,
+                                                       self.ws, st), {}),
+                 ("bwd", 0): (api.ard_lstm_tile_bwd, (d, self.W, self.dHs, None, None, self.ws, self.dX, self.dW,
+                                                       self.db, None, None, st), {})}
+        return pats, calls
+
+    step = Mlp.step
+    replay = Mlp.replay
+
+    def host_copies(self):
+        self._host = (self.X.double().cpu().numpy().transpose(0, 2, 1), self.W.double().cpu().numpy(),
+                      self.b.double().cpu().numpy(), self.dHs.double().cpu().numpy().transpose(0, 2, 1))
+
+    def oracle_step(self, pats):
+        import numpy as np
+        from oracle import lstm as olstm
+        from oracle import patterns as opat
+        from oracle import prng as oprng
+        X, W, b, dHs = self._host
+        words = oprng.tile_bitmap_tdp(self.tn, self.tk, *pats[0])
+        Wm = W * opat.tile_mask(words, self.tn, self.tk, self.tile)
+        ones = np.ones(self.H)
+        _, _, _, cache = olstm.lstm_forward(X, Wm, b, ones)
+        return olstm.lstm_backward(X, Wm, ones, cache, dHs)
+
+
 WORKLOADS = {
     "mlp784": dict(cls="Mlp", name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
                    dtype="f32", init="xavier", seed=1805 + 1),
@@ -638,6 +730,8 @@ WORKLOADS = {
                        layers=2, dtype="f32", seed=1805 + 5),
     "lstm2x1500b40": dict(cls="LstmStack", name="lstm-2x1500-t35-b40-fp32", T=35, batch=40, inputs=1500,
                           hidden=1500, layers=2, dtype="f32", seed=1805 + 5),
+    "lstm1024tile": dict(cls="LstmTile", name="lstm-t35-b64-i1024-h1024-fp32-tile64", T=35, batch=64, inputs=1024,
+                         hidden=1024, tile=64, dtype="f32", seed=1805 + 3),
     "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
                     dtype="bf16", init="he", seed=1805 + 4),
 }
@@ -926,7 +1020,7 @@ def main():
     _ffi.lib()
     spec = dict(WORKLOADS[args.workload])
     cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm,
-           "LstmStack": LstmStack}[spec.pop("cls")]
+           "LstmStack": LstmStack, "LstmTile": LstmTile}[spec.pop("cls")]
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:
