@@ -23,6 +23,12 @@ inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 // error with a message.
 int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what, bool needs_list);
 
+// The fp32 tile layer's forward (fwd) or transposed product with the kept-tile
+// lists split over several workgroups for small grids, partial sums in the
+// caller's buffer (ard_tile.hip). Falls back to ard_tile_fwd / ard_tile_bwd_data.
+int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan* p, const void* act, const void* W,
+                          void* out, float* partial, size_t partial_floats, void* stream);
+
 // Kept count of a row pattern (see ard_row_kept).
 inline int32_t kept_count(int32_t n, int32_t period, int32_t offset) {
   if (offset >= n) return 0;

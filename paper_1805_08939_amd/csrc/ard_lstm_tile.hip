@@ -38,12 +38,14 @@ struct TileLstm {
   float* dZ;            // [4H][T B]
   float* dxh;           // [(I + H)][B] step input derivative
   float* dc;            // [H][B] cell derivative carry
+  float* part;          // split partial sums of the step products
+  size_t part_floats;
 };
 
 size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct TileLayout {
-  size_t xh, XH, z, G, C, dz, dZ, dxh, dc, total;
+  size_t xh, XH, z, G, C, dz, dZ, dxh, dc, part, part_floats, total;
 };
 
 TileLayout tile_layout(int64_t T, int64_t B, int64_t I, int64_t H) {
@@ -59,6 +61,10 @@ TileLayout tile_layout(int64_t T, int64_t B, int64_t I, int64_t H) {
   L.dZ = off;  off += al256(4 * 4 * H * T * B);
   L.dxh = off; off += al256(4 * K * B);
   L.dc = off;  off += al256(4 * H * B);
+  // up to 8 splits of the larger step product (4H or I + H rows, rounded to whole 64-row tiles)
+  const int64_t rows = ((4 * H > K ? 4 * H : K) + 63) / 64 * 64;
+  L.part_floats = static_cast<size_t>(8 * rows * B);
+  L.part = off; off += al256(4 * L.part_floats);
   L.total = off;
   return L;
 }
@@ -79,6 +85,8 @@ TileLstm tile_args(const TileLayout& L, char* w, int32_t T, int32_t B, int32_t I
   s.dZ = reinterpret_cast<float*>(w + L.dZ);
   s.dxh = reinterpret_cast<float*>(w + L.dxh);
   s.dc = reinterpret_cast<float*>(w + L.dc);
+  s.part = reinterpret_cast<float*>(w + L.part);
+  s.part_floats = L.part_floats;
   return s;
 }
 
@@ -267,7 +275,9 @@ int ard_lstm_tile_fwd(const ard_lstm_tile_desc* desc, const void* X, const void*
   ARD_LAUNCH_CHECK();
   const ard_tile_desc td = step_desc(desc, s.B);
   for (int32_t t = 0; t < s.T; ++t) {
-    if ((st = ard_tile_fwd(&td, desc->weight_plan, s.xh, W, s.z, stream)) != ARD_OK) return st;
+    if ((st = tdp_product_f32_split(true, &td, desc->weight_plan, s.xh, W, s.z, s.part, s.part_floats, stream)) !=
+        ARD_OK)
+      return st;
     hipLaunchKernelGGL(tile_lstm_point_fwd_kernel, grid_of(IB > HB ? IB : HB), dim3(256), 0, sm, s, t, bias,
                        static_cast<const float*>(X), static_cast<float*>(Hs));
     ARD_LAUNCH_CHECK();
@@ -299,7 +309,9 @@ int ard_lstm_tile_bwd(const ard_lstm_tile_desc* desc, const void* W, const void*
                        static_cast<const float*>(dHs), static_cast<const float*>(dhT),
                        static_cast<const float*>(dcT), static_cast<float*>(dX));
     ARD_LAUNCH_CHECK();
-    if ((st = ard_tile_bwd_data(&td, desc->weight_plan, s.dz, W, s.dxh, stream)) != ARD_OK) return st;
+    if ((st = tdp_product_f32_split(false, &td, desc->weight_plan, s.dz, W, s.dxh, s.part, s.part_floats,
+                                    stream)) != ARD_OK)
+      return st;
   }
   hipLaunchKernelGGL(tile_lstm_bwd_final_kernel, grid_of(IB > HB ? IB : HB), dim3(256), 0, sm, s,
                      static_cast<float*>(dX), static_cast<float*>(dh0), static_cast<float*>(dc0));

@@ -467,6 +467,10 @@ struct TdpFastArgs {
   const int32_t* list;  // row_cols (fwd, bwd_weight) or col_rows (bwd_data)
   const int32_t* chunks;
   float scale;
+  // split lists (fp32 output only): workgroup (tile, split) sums its share of
+  // the row's (column's) kept tiles into partial[split][rows][B]
+  int32_t splits, rows;
+  float* partial;
 };
 
 constexpr int kFastTile = 64;
@@ -486,8 +490,12 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
   int own, col;
   grouped_tile(blockIdx.x, a.nx, a.ny, own, col);
   const int n0 = col * Cfg::BN;
-  const int p0 = __builtin_amdgcn_readfirstlane(a.ptr[own]);
-  const int p1 = __builtin_amdgcn_readfirstlane(a.ptr[own + 1]);
+  const int splits = a.splits > 1 ? a.splits : 1;
+  const int sp = splits > 1 ? static_cast<int>(blockIdx.y) : 0;
+  const int pa = __builtin_amdgcn_readfirstlane(a.ptr[own]);
+  const int nall = __builtin_amdgcn_readfirstlane(a.ptr[own + 1]) - pa;
+  const int p0 = pa + nall * sp / splits;  // this split's share of the list
+  const int p1 = pa + nall * (sp + 1) / splits;
 
   f32x16 acc[Cfg::FM][Cfg::FN];
 #pragma unroll
@@ -563,7 +571,31 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
   g.c.p = static_cast<OutT*>(a.out) + static_cast<int64_t>(own) * TT * B;
   g.c.ld = B;
   g.c.scale = a.scale;
+  if constexpr (sizeof(OutT) == 4) {
+    if (splits > 1) {  // unscaled partial sums; the reduction applies the scale
+      g.c.p = a.partial + (static_cast<int64_t>(sp) * a.rows + static_cast<int64_t>(own) * TT) * B;
+      g.c.scale = 1.0f;
+    }
+  }
   fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, n0, wm, wn, 0, 0, smem);
+}
+
+// out[e] = scale * sum over the splits of partial[split][e], in split order
+// (the loads of up to eight splits issued together).
+__global__ void __launch_bounds__(256) tdp_split_reduce_kernel(const float* __restrict__ partial, int32_t splits,
+                                                               int64_t n, float scale, float* __restrict__ out) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= n) return;
+  float v = 0.0f;
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = s0 + u < splits ? partial[(s0 + u) * n + e] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < splits) v += t[u];
+  }
+  out[e] = scale * v;
 }
 
 // bwd_weight: dW(tn, tk) = scale * dYt[tn block] Xt[tk block]^T (contraction
@@ -829,6 +861,50 @@ int plan_tiles(int32_t n, int32_t k, int32_t tile, uint32_t* d_bits, int32_t nnz
 }
 
 }  // namespace
+
+// The fp32 tile layer's forward (fwd) or transposed product with each tile
+// row's (column's) kept-tile list split over up to 8 workgroups when the tile
+// rows (columns) alone would leave most of the chip idle, as for a recurrent
+// step at a small batch: partial sums in `partial` (partial_floats floats),
+// then a fixed-order reduction that applies the scale. Runs the single-pass
+// call when no split applies (another dtype, the register-staged path, too
+// many workgroups already, or too small a partial buffer).
+int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan* p, const void* act, const void* W,
+                          void* out, float* partial, size_t partial_floats, void* stream) {
+  int st = check_tile_call(d, p);
+  if (st != ARD_OK) return st;
+  auto single = [&]() {
+    return fwd ? ard_tile_fwd(d, p, act, W, out, stream) : ard_tile_bwd_data(d, p, act, W, out, stream);
+  };
+  if (d->dtype != ARD_F32 || !partial || !aligned16(partial)) return single();
+  if ((st = check_dev_ptr(act, "act")) || (st = check_dev_ptr(W, "W")) || (st = check_dev_ptr(out, "out")))
+    return st;
+  TdpArgs a = {act, nullptr, W, out, d->batch, p->n, p->k, p->tile, p->tiles_k,
+               fwd ? p->d_row_ptr : p->d_col_ptr, fwd ? p->d_row_cols : p->d_col_rows, d->scale,
+               p->d_row_ptr + p->tiles_n};
+  if (!tdp_fast_ok<float>(a)) return single();
+  using C = TdpFastCfgs<float>;
+  const int owners = fwd ? p->tiles_n : p->tiles_k;
+  const int nx = (a.B + C::Rows::BN - 1) / C::Rows::BN;
+  int splits = 1;
+  while (splits < 8 && static_cast<int64_t>(nx) * owners * splits * 2 <= kTargetBlocks) splits *= 2;
+  const int64_t rows = static_cast<int64_t>(owners) * kFastTile;
+  if (splits == 1 || static_cast<size_t>(splits) * rows * a.B > partial_floats) return single();
+  TdpFastArgs f = {a.act, nullptr, a.W, a.out, a.B, a.K, nx, owners, a.ptr, a.list, p->d_chunks, a.scale,
+                   splits, static_cast<int32_t>(rows), partial};
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  const dim3 grid(static_cast<unsigned>(nx * owners), static_cast<unsigned>(splits));
+  if (fwd)
+    ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_FWD, float>>(grid, f, sm)));
+  else
+    ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_BWD_DATA, float>>(grid, f, sm)));
+  const int64_t n = rows * a.B;
+  hipLaunchKernelGGL(tdp_split_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, sm,
+                     partial, splits, n, a.scale, static_cast<float*>(out));
+  ARD_LAUNCH_CHECK();
+  return ARD_OK;
+}
+
 }  // namespace ard
 
 using namespace ard;
