@@ -37,7 +37,7 @@ class Mlp:
     """An MLP whose hidden layers take row-based dropout patterns sampled per
     step from K(p). Layers are FC: Xt[K][B] -> Yt[N][B]."""
 
-    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False):
+    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False, dropped="skip"):
         import torch
         from paper_1805_08939_amd import api, synth
         self.api, self.torch = api, torch
@@ -68,7 +68,8 @@ class Mlp:
         self.ws = torch.empty(2 * 256 * 256 * 256, dtype=torch.float32, device=dev)
         self.K = None
         self.config = {"workload": name, "global_batch": batch, "layers": dims,
-                       "patterns": "row-based, sampled per step from K(p), n_max 16", "dropped": "skip"}
+                       "patterns": "row-based, sampled per step from K(p), n_max 16", "dropped": dropped}
+        self.dropped = api.ARD_DROPPED_ZERO if dropped == "zero" else api.ARD_DROPPED_SKIP
         # raw device addresses and the stream handle, resolved once: the step
         # then costs one C call per launch with no per-call tensor lookups
         self.stream = torch.cuda.current_stream().cuda_stream
@@ -89,7 +90,7 @@ class Mlp:
             out_plan = self.plans[l] if l < self.L - 1 else None
             act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
             args = (self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], in_plan, out_plan, 1.0, act,
-                    api.ARD_DROPPED_SKIP)
+                    self.dropped)
             self.descs.append(api.fc_desc(*args))
             self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT) if l > 0 else self.descs[-1])
         # the calls of one step, in order, with their arguments resolved once.
@@ -981,6 +982,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mlp784", choices=sorted(WORKLOADS))
     ap.add_argument("--p", type=float, default=0.5, help="dropout rate of the headline value")
+    ap.add_argument("--dropped", default="skip", choices=["skip", "zero"],
+                    help="MLP workloads: dropped outputs and gradients left untouched (skip) or written 0 (zero)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--summarize-trace", metavar="CSV", help="print a per-kernel table of a rocprofv3 kernel trace")
@@ -1021,6 +1024,10 @@ def main():
     spec = dict(WORKLOADS[args.workload])
     cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm,
            "LstmStack": LstmStack, "LstmTile": LstmTile}[spec.pop("cls")]
+    if args.dropped != "skip":
+        if cls is not Mlp:
+            sys.exit("--dropped zero applies to the MLP workloads")
+        spec["dropped"] = args.dropped
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:
