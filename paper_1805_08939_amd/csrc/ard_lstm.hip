@@ -34,6 +34,10 @@ namespace ard {
 
 namespace {
 
+// 32 x 64 output tiles on eight waves (two columns of 32, four k shares of a
+// 128-deep slab), three stages: the backward recurrence at a batch of 64.
+using RecWideCfg = FastCfg<float, 32, 64, 128, 3, 1, 2, 4>;
+
 struct Layout {
   int64_t T, B, I, H, ns, G4, KW, S;
   int64_t Ic, ip, io;  // kept inputs (compact input width) and their pattern
@@ -634,6 +638,19 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
       fs = d;
       break;
     }
+  // A batch of 64 is one column of 32 x 64 tiles: each block of the recurrent
+  // weights is then read by one workgroup per step instead of two. Taken when
+  // those tiles alone fill one round of 256 workgroups.
+  const int64_t wtiles = ((ns + 31) / 32) * ((L.B + 63) / 64);
+  bool rec_wide = false;
+  if (L.B > 32 && L.B <= 64) {
+    for (int32_t d = static_cast<int32_t>(L.S); d >= 1; --d)
+      if (L.G4 % d == 0 && L.G4 / d >= 256 && wtiles * d == 256) {
+        fs = d;
+        rec_wide = true;
+        break;
+      }
+  }
   GemmArgs gr = {};
   bool rec_fast = false;
   if (fs > 0) {
@@ -657,7 +674,10 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     s.t = t;
     if (rec_fast) {
       gr.b.p = s.dA + static_cast<int64_t>(t) * L.G4 * L.B;
-      ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(gr, splits, sm, nullptr)));
+      if (rec_wide)
+        ARD_HIP_CHECK((launch_fast<RecWideCfg, true, true, float, EPI_FWD>(gr, splits, sm)));
+      else
+        ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(gr, splits, sm, nullptr)));
     } else if (vec) {
       hipLaunchKernelGGL((lstm_bwd_rec_kernel<true, true>), rgrid, dim3(256), 0, sm, s, part, ks);
     } else {

@@ -108,6 +108,13 @@ def test_multi_tile_and_unaligned(shape, pattern):
     run_lstm(T, B, I, H, pattern, seed=B)
 
 
+@pytest.mark.parametrize("shape", [(3, 64, 256, 1024), (2, 48, 128, 2048)])
+def test_all_units_kept_wide_recurrence_tiles(shape):
+    """1024 and 2048 kept units at batch 64 and 48: the backward recurrence on
+    32 x 64 tiles (one tile column holds the batch)."""
+    run_lstm(*shape, (1, 0), seed=sum(shape), with_state=True)
+
+
 def test_full_config_lstm_1024():
     """Single LSTM layer fp32, input 1024, hidden 1024, 35 steps, batch 64, hidden
     units dropped with period 2 (seeded offset), inputs ~ U(-0.1, 0.1)."""
