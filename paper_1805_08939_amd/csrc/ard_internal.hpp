@@ -27,7 +27,8 @@ int check_row_plan(const ard_row_plan* plan, int32_t n, const char* what, bool n
 // lists split over several workgroups for small grids, partial sums in the
 // caller's buffer (ard_tile.hip). Falls back to ard_tile_fwd / ard_tile_bwd_data.
 int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan* p, const void* act, const void* W,
-                          void* out, float* partial, size_t partial_floats, void* stream);
+                          void* out, float* partial, size_t partial_floats, void* stream,
+                          int* splits_left = nullptr);
 
 // Kept count of a row pattern (see ard_row_kept).
 inline int32_t kept_count(int32_t n, int32_t period, int32_t offset) {

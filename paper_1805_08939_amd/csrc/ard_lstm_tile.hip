@@ -40,6 +40,8 @@ struct TileLstm {
   float* dc;            // [H][B] cell derivative carry
   float* part;          // split partial sums of the step products
   size_t part_floats;
+  int32_t zsplits;      // partial sums of z (1: z itself holds the product)
+  int32_t dsplits;      // partial sums of dxh (1: dxh itself holds the product)
 };
 
 size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -87,7 +89,25 @@ TileLstm tile_args(const TileLayout& L, char* w, int32_t T, int32_t B, int32_t I
   s.dc = reinterpret_cast<float*>(w + L.dc);
   s.part = reinterpret_cast<float*>(w + L.part);
   s.part_floats = L.part_floats;
+  s.zsplits = s.dsplits = 1;
   return s;
+}
+
+// Element e of a step product: the product buffer itself, or the sum of its
+// split partial sums (n elements each) in split order, the loads of up to
+// eight splits issued together.
+__device__ __forceinline__ float step_val(const float* direct, const float* part, int splits, int64_t n, int64_t e) {
+  if (splits <= 1) return direct[e];
+  float v = 0.0f;
+  for (int q0 = 0; q0 < splits; q0 += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = q0 + u < splits ? part[(q0 + u) * n + e] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (q0 + u < splits) v += t[u];
+  }
+  return v;
 }
 
 // Before the first step: x_t into the input rows of XH for every t, h0 (or 0)
@@ -123,7 +143,8 @@ __global__ void tile_lstm_point_fwd_kernel(TileLstm s, int32_t t, const float* _
     const int64_t j = e / s.B, b = e % s.B;
     float zv[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) zv[q] = s.z[(q * s.H + j) * s.B + b] + (bias ? bias[q * s.H + j] : 0.0f);
+    for (int q = 0; q < 4; ++q)
+      zv[q] = step_val(s.z, s.part, s.zsplits, 4 * HB, (q * s.H + j) * s.B + b) + (bias ? bias[q * s.H + j] : 0.0f);
     const float ig = sgm(zv[0]), fg = sgm(zv[1]), gg = tanhf(zv[2]), og = sgm(zv[3]);
     const float cp = s.C[static_cast<int64_t>(t) * HB + e];
     const float c = fg * cp + ig * gg;
@@ -154,7 +175,8 @@ __global__ void tile_lstm_point_bwd_kernel(TileLstm s, int32_t t, const float* _
   const int64_t HB = static_cast<int64_t>(s.H) * s.B;
   const bool last = t == s.T - 1;
   const int64_t IB = static_cast<int64_t>(s.I) * s.B;
-  if (!last && dX && e < IB) dX[static_cast<int64_t>(t + 1) * IB + e] = s.dxh[e];
+  const int64_t KB = static_cast<int64_t>(s.I + s.H) * s.B;
+  if (!last && dX && e < IB) dX[static_cast<int64_t>(t + 1) * IB + e] = step_val(s.dxh, s.part, s.dsplits, KB, e);
   if (e >= HB) return;
   const int64_t j = e / s.B, b = e % s.B;
   float dh = dHs[static_cast<int64_t>(t) * HB + e];
@@ -163,7 +185,7 @@ __global__ void tile_lstm_point_bwd_kernel(TileLstm s, int32_t t, const float* _
     if (dhT) dh += dhT[e];
     dcin = dcT ? dcT[e] : 0.0f;
   } else {
-    dh += s.dxh[(s.I + j) * s.B + b];
+    dh += step_val(s.dxh, s.part, s.dsplits, KB, (s.I + j) * s.B + b);
     dcin = s.dc[e];
   }
   const float* Gt = s.G + static_cast<int64_t>(t) * 4 * HB;
@@ -189,10 +211,11 @@ __global__ void tile_lstm_bwd_final_kernel(TileLstm s, float* __restrict__ dX, f
                                            float* __restrict__ dc0) {
   const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t IB = static_cast<int64_t>(s.I) * s.B, HB = static_cast<int64_t>(s.H) * s.B;
-  if (dX && e < IB) dX[e] = s.dxh[e];
+  const int64_t KB = static_cast<int64_t>(s.I + s.H) * s.B;
+  if (dX && e < IB) dX[e] = step_val(s.dxh, s.part, s.dsplits, KB, e);
   if (e < HB) {
     const int64_t j = e / s.B, b = e % s.B;
-    if (dh0) dh0[e] = s.dxh[(s.I + j) * s.B + b];
+    if (dh0) dh0[e] = step_val(s.dxh, s.part, s.dsplits, KB, (s.I + j) * s.B + b);
     if (dc0) dc0[e] = s.dc[e];
   }
 }
@@ -275,8 +298,8 @@ int ard_lstm_tile_fwd(const ard_lstm_tile_desc* desc, const void* X, const void*
   ARD_LAUNCH_CHECK();
   const ard_tile_desc td = step_desc(desc, s.B);
   for (int32_t t = 0; t < s.T; ++t) {
-    if ((st = tdp_product_f32_split(true, &td, desc->weight_plan, s.xh, W, s.z, s.part, s.part_floats, stream)) !=
-        ARD_OK)
+    if ((st = tdp_product_f32_split(true, &td, desc->weight_plan, s.xh, W, s.z, s.part, s.part_floats, stream,
+                                    &s.zsplits)) != ARD_OK)
       return st;
     hipLaunchKernelGGL(tile_lstm_point_fwd_kernel, grid_of(IB > HB ? IB : HB), dim3(256), 0, sm, s, t, bias,
                        static_cast<const float*>(X), static_cast<float*>(Hs));
@@ -310,7 +333,7 @@ int ard_lstm_tile_bwd(const ard_lstm_tile_desc* desc, const void* W, const void*
                        static_cast<const float*>(dcT), static_cast<float*>(dX));
     ARD_LAUNCH_CHECK();
     if ((st = tdp_product_f32_split(false, &td, desc->weight_plan, s.dz, W, s.dxh, s.part, s.part_floats,
-                                    stream)) != ARD_OK)
+                                    stream, &s.dsplits)) != ARD_OK)
       return st;
   }
   hipLaunchKernelGGL(tile_lstm_bwd_final_kernel, grid_of(IB > HB ? IB : HB), dim3(256), 0, sm, s,

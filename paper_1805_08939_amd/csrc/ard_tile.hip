@@ -870,7 +870,8 @@ int plan_tiles(int32_t n, int32_t k, int32_t tile, uint32_t* d_bits, int32_t nnz
 // call when no split applies (another dtype, the register-staged path, too
 // many workgroups already, or too small a partial buffer).
 int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan* p, const void* act, const void* W,
-                          void* out, float* partial, size_t partial_floats, void* stream) {
+                          void* out, float* partial, size_t partial_floats, void* stream, int* splits_left) {
+  if (splits_left) *splits_left = 1;
   int st = check_tile_call(d, p);
   if (st != ARD_OK) return st;
   auto single = [&]() {
@@ -898,6 +899,10 @@ int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan*
     ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_FWD, float>>(grid, f, sm)));
   else
     ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_BWD_DATA, float>>(grid, f, sm)));
+  if (splits_left) {  // the caller adds the partial sums itself (scale 1 only)
+    *splits_left = splits;
+    return ARD_OK;
+  }
   const int64_t n = rows * a.B;
   hipLaunchKernelGGL(tdp_split_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, sm,
                      partial, splits, n, a.scale, static_cast<float*>(out));
