@@ -137,7 +137,7 @@ struct CompactJobs {
 
 template <typename T>
 __device__ __forceinline__ void compact_row(const CompactJob<T>& jb, int64_t i, T* seg) {
-  constexpr int SEG = 4096;  // source columns per segment
+  constexpr int SEG = 16384 / static_cast<int>(sizeof(T));  // source columns per segment: 16 KB of LDS
   constexpr int EPC = 16 / static_cast<int>(sizeof(T));
   const int64_t K = jb.K;
   const int32_t in_period = jb.in_period, kin = jb.kin;
@@ -175,7 +175,7 @@ __device__ __forceinline__ void compact_row(const CompactJob<T>& jb, int64_t i, 
 // element loads), then consecutive threads write consecutive kept columns.
 template <typename T>
 __global__ void __launch_bounds__(256) compact_weights_kernel(CompactJobs<T> jobs) {
-  __shared__ __attribute__((aligned(16))) T seg[4096];
+  __shared__ __attribute__((aligned(16))) T seg[16384 / sizeof(T)];
   int64_t i = blockIdx.x;
   for (int q = 0; q < jobs.count; ++q) {
     if (i < jobs.job[q].rows) {
