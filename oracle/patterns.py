@@ -59,8 +59,6 @@ def tile_lists(words, tiles_n, tiles_k):
       row_ptr[tiles_n + 1], row_cols[nnz]  - kept tile columns of each tile row
       col_ptr[tiles_k + 1], col_rows[nnz]  - kept tile rows of each tile column
       flat[nnz]                            - kept linear tile indices t
-      chunks                               - records of the groups of up to 4
-                                             kept tiles of a row (row_groups)
     Every list is ascending within its segment.
     """
     grid = bitmap_to_grid(words, tiles_n, tiles_k)
@@ -78,24 +76,7 @@ def tile_lists(words, tiles_n, tiles_k):
         col_ptr.append(len(col_rows))
     flat = [t for t in range(tiles_n * tiles_k) if grid[t // tiles_k, t % tiles_k]]
     return {"row_ptr": row_ptr, "row_cols": row_cols,
-            "col_ptr": col_ptr, "col_rows": col_rows, "flat": flat,
-            "chunks": row_groups(row_ptr, row_cols, 4)}
-
-
-def row_groups(row_ptr, row_cols, group):
-    """Work groups of the weight-gradient pass: the kept tiles of each tile row
-    taken ``group`` at a time in row order (the last group of a row may be
-    shorter). Returned flattened as a 4-int header [count, 0, 0, 0] followed by
-    one record of 4 + group ints per group: tile row, first position in
-    row_cols, tile count n, 0, then the n tile columns and the last of them
-    repeated up to ``group`` entries."""
-    recs = []
-    for tn in range(len(row_ptr) - 1):
-        for first in range(row_ptr[tn], row_ptr[tn + 1], group):
-            n = min(group, row_ptr[tn + 1] - first)
-            cols = row_cols[first:first + n]
-            recs.append([tn, first, n, 0] + cols + [cols[-1]] * (group - n))
-    return [len(recs), 0, 0, 0] + [v for r in recs for v in r]
+            "col_ptr": col_ptr, "col_rows": col_rows, "flat": flat}
 
 
 def bitmap_popcount(words, total):

@@ -91,38 +91,6 @@ def test_tile_lists_reconstruct_the_grid(seed):
     assert (g1 == grid).all() and (g2 == grid).all() and (g3 == grid).all()
     assert L["flat"] == sorted(L["flat"])
     assert patterns.bitmap_popcount(words, tn * tk) == int(grid.sum()) == len(L["flat"])
-    # the weight-gradient groups cover every kept tile once, each within one
-    # tile row, at most 4 tiles, in row order, only the last of a row short
-    ch = L["chunks"]
-    assert ch[1:4] == [0, 0, 0] and len(ch) == 4 + 8 * ch[0]
-    g4 = np.zeros_like(grid)
-    seen = []
-    for i in range(ch[0]):
-        r, first, n, zero, *cols = ch[4 + 8 * i: 12 + 8 * i]
-        end = first + n
-        assert zero == 0 and 1 <= n <= 4 and L["row_ptr"][r] <= first and end <= L["row_ptr"][r + 1]
-        if n < 4:
-            assert end == L["row_ptr"][r + 1]
-        for j in range(4):
-            assert cols[j] == cols[min(j, n - 1)]
-        for j in range(n):
-            assert not g4[r, cols[j]] and grid[r, cols[j]]
-            g4[r, cols[j]] = True
-        seen.append((r, first))
-    assert seen == sorted(seen) and (g4 == grid).all()
-
-
-def test_row_groups_by_hand():
-    # rows with 0, 5, 4 and 1 kept tiles
-    row_ptr, row_cols = [0, 0, 5, 9, 10], [0, 2, 3, 5, 7, 1, 2, 3, 4, 6]
-    assert patterns.row_groups(row_ptr, row_cols, 4) == [
-        4, 0, 0, 0,
-        1, 0, 4, 0, 0, 2, 3, 5,
-        1, 4, 1, 0, 7, 7, 7, 7,
-        2, 5, 4, 0, 1, 2, 3, 4,
-        3, 9, 1, 0, 6, 6, 6, 6]
-    assert patterns.row_groups([0, 0, 0], [], 4) == [0, 0, 0, 0]
-    assert patterns.row_groups([0, 3], [1, 4, 6], 1) == [3, 0, 0, 0, 0, 0, 1, 0, 1, 0, 1, 1, 0, 4, 0, 2, 1, 0, 6]
 
 
 def test_tile_mask_expansion():

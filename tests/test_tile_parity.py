@@ -4,6 +4,7 @@ import pytest
 import torch
 
 from gpu_util import compare, device, f64, to_dev, tol, ard_dtype
+from plan_invariants import check_weight_grad_groups
 from oracle import patterns as opat
 from oracle import prng as oprng
 from oracle import tdp as otdp
@@ -31,7 +32,7 @@ def tile_plan(n, k, tile, words, check=True):
         assert arr(plan.d_row_cols, nnz) == L["row_cols"]
         assert arr(plan.d_col_rows, nnz) == L["col_rows"]
         assert arr(plan.d_flat, nnz) == L["flat"]
-        assert arr(plan.d_chunks, len(L["chunks"])) == L["chunks"]
+        check_weight_grad_groups(arr(plan.d_chunks, 4 + 8 * arr(plan.d_chunks, 1)[0]), L["row_ptr"], L["row_cols"])
     return plan
 
 
@@ -45,7 +46,7 @@ def check_lists(plan, ws, L, tn, tk, nnz):
     assert arr(plan.d_row_cols, nnz) == L["row_cols"]
     assert arr(plan.d_col_rows, nnz) == L["col_rows"]
     assert arr(plan.d_flat, nnz) == L["flat"]
-    assert arr(plan.d_chunks, len(L["chunks"])) == L["chunks"]
+    check_weight_grad_groups(arr(plan.d_chunks, 4 + 8 * arr(plan.d_chunks, 1)[0]), L["row_ptr"], L["row_cols"])
 
 
 def sampled_plan(n, k, tile, p, seed, stream, it):
