@@ -313,7 +313,7 @@ hipError_t launch_compact(const FcShape& s, const void* W, void* Wc, hipStream_t
 }
 
 // The kept rows offset + period * i of a row-major matrix (row stride ld): a
-// row-based pattern keeps an arithmetic progression of neurons (Sec. 3.2,
+// row-based pattern keeps an arithmetic progression of neurons (Sec. III-A,
 // Eq. 1), so the gather folds into the view's base and row stride and the
 // GEMM reads no index list. y, when set, is the gate source of the same shape.
 GemmOperand kept_rows(const void* p, const void* y, int64_t ld, int32_t period, int32_t offset, size_t esize,
