@@ -1,17 +1,21 @@
 #!/usr/bin/env python3
 """Benchmark of the Approximate Random Dropout hot path on one MI355X.
 
-Default workload: the paper's MLP 784-2048-2048-10 (fp32, batch 128, ReLU)
-with row-based dropout on both hidden layers. Each step samples a fresh
-pattern per hidden layer from the distribution K searched for p, plans it,
-gathers the compact weights of the layers whose inputs are dropped on the
-device, and runs fwd, bwd_data and bwd_weight of all three layers
-(bwd_data of the first layer is not needed; the two backward products of a
-layer are one call, one launch where both are small). The headline value is TFLOP/s
-counted on the work actually kept, at p = 0.5; the same steps at p = 0.3 and
-0.7 and at p = 0 (period 1: the same kernels with nothing dropped) give the
-speedups. Other workloads (--workload) are the single wide MLP layer set, the
-tile-pattern layer and the LSTM.
+Default workload: the wide MLP 8192-8192-8192-8192 (bf16 with fp32
+accumulation, batch 2048, ReLU) with row-based dropout on both hidden layers
+at p = 0.7. Each step samples a fresh pattern per hidden layer from the
+distribution K searched for p, plans it, gathers the compact weights of the
+layers whose inputs are dropped on the device, and runs fwd, bwd_data and
+bwd_weight of all three layers (bwd_data of the first layer is not needed).
+The headline value is TFLOP/s counted on the work actually kept; the same
+steps at p = 0.3 and 0.5 and at p = 0 (period 1: the same kernels with
+nothing dropped) give the speedups. Other workloads (--workload): the single
+FC layer, the 3-layer MLP 784-2048-2048-10, the tile-pattern layer, the LSTM
+layers.
+
+The roofline entry covers the layer GEMM calls: a second pass of the same
+steps brackets every call with HIP events on the step's stream, and
+achieved = sum of their kept FLOPs / sum of their durations.
 
 Prints one JSON line. Inputs are synthetic and resident in HBM before timing.
 """
@@ -92,7 +96,9 @@ class Mlp:
             args = (self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], in_plan, out_plan, 1.0, act,
                     self.dropped)
             self.descs.append(api.fc_desc(*args))
-            self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT) if l > 0 else self.descs[-1])
+            # a layer whose inputs are dropped reads the compact weights and
+            # writes the compact weight gradient dWc[kept_out][ldc] into dW
+            self.cdescs.append(api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT_GRAD) if l > 0 else self.descs[-1])
         # the calls of one step, in order, with their arguments resolved once.
         # A layer whose inputs are all kept in a step (period 1) needs no
         # compact weight copy: it reads W itself through the full-layout
@@ -129,8 +135,6 @@ class Mlp:
                                                              [P["W"][l] for l in sub], [P["Wc"][l] for l in sub])
         self.order = [("fwd", l) for l in range(self.L)]
         self.order += [("bwd", l) for l in reversed(range(1, self.L))] + [("bwd_weight", 0)]
-        # calls of one GEMM each: the candidates for the roofline call
-        self.roofline_keys = [k for k in self.order if k[0] != "bwd"]
 
     def patterns(self, it):
         return [self.api.ard_sample_row_pattern(self.K, PATTERN_SEED, l + 1, it) for l in range(self.L - 1)]
@@ -164,9 +168,9 @@ class Mlp:
             self.V = [torch.zeros_like(w) for w in self.dW]
             self.Vb = [torch.zeros_like(b) for b in self.db]
             P["V"], P["Vb"] = [v.data_ptr() for v in self.V], [v.data_ptr() for v in self.Vb]
-        descs = self.dense if dense else self.descs
         for l in range(self.L):
-            api.ard_fc_sgd_momentum(descs[l], P["W"][l], P["V"][l], P["dW"][l], P["bias"][l], P["Vb"][l], P["db"][l],
+            desc = self.dense[l] if dense else (self.cdescs[l] if l in self.step_compact else self.descs[l])
+            api.ard_fc_sgd_momentum(desc, P["W"][l], P["V"][l], P["dW"][l], P["bias"][l], P["Vb"][l], P["db"][l],
                                     1e-6, 0.9, st)
 
     def conventional_step(self, it):
@@ -209,20 +213,6 @@ class Mlp:
                 per[("bwd_weight", l)] = f
         return sum(per.values()), per
 
-    @staticmethod
-    def shape_label(shape):
-        return "M x N x K = %d x %d x %d" % tuple(shape)
-
-    def gemm_shape(self, pats, kind, l):
-        """(M, N, K) of the GEMM a call runs: fwd kept_out x B x kept_in, bwd_data
-        kept_in x B x kept_out, bwd_weight kept_out x kept_in x B."""
-        n = self.kept(pats)
-        if kind == "fwd":
-            return (n[l + 1], self.B, n[l])
-        if kind == "bwd_data":
-            return (n[l], self.B, n[l + 1])
-        return (n[l + 1], n[l], self.B)
-
     def prepare(self, it):
         """Samples this step's patterns, plans them and gathers the compact
         weights of the layers whose inputs are dropped. Returns the patterns and
@@ -235,39 +225,31 @@ class Mlp:
             api.ard_plan_rows(self.dims[l + 1], per, off, None, st, plan=self.plans[l])
         calls = dict(self.layer_calls[0][False])
         sub = tuple(l for l in range(1, self.L) if pats[l - 1][0] > 1)
+        self.step_compact = sub  # layers whose dW holds the compact gradient this step
         if sub:
             api.ard_fc_compact_weights_batch(self.compact_batches[sub], st)
         for l in range(1, self.L):
             calls.update(self.layer_calls[l][l in sub])
         return pats, calls
 
-    def step(self, it, timed_call=None, events=None):
+    def step(self, it, events=None):
+        """One step of iteration it. With events (a list of (start, end) event
+        pairs, consumed from the front), every call is bracketed by a pair
+        recorded on the current stream; returns the patterns and the list of
+        (call key, start, end) used."""
         pats, calls = self.prepare(it)
+        used = []
         for key in self.order:
             fn, args, kw = calls[key]
-            if key == timed_call:
-                events[0].record()
+            if events is not None:
+                e0, e1 = events.pop()
+                e0.record()
                 fn(*args, **kw)
-                events[1].record()
+                e1.record()
+                used.append((key, e0, e1))
             else:
                 fn(*args, **kw)
-        return pats
-
-    def replay(self, it, key, reps):
-        """Runs one call of step it reps times back to back and returns the
-        mean GPU time per launch (ms, HIP events on the call's stream around
-        the whole replay)."""
-        torch = self.torch
-        self.step(it)  # the whole step once: every input of the call (and saved state) is step it's
-        _, calls = self.prepare(it)
-        fn, args, kw = calls[key]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            fn(*args, **kw)
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / reps
+        return pats, used
 
     # ------------------------------------------------------------------ oracle
     def oracle_step(self, pats):
@@ -297,6 +279,85 @@ class Mlp:
         self._host = {"X0": self.X0.double().cpu().numpy().T.copy(),
                       "W": [w.double().cpu().numpy() for w in self.W],
                       "dY": self.dY[-1].double().cpu().numpy().T.copy()}
+
+
+class FcLayer:
+    """One fully connected layer whose output neurons take a row-based pattern
+    per step (Sec. III-A): fwd, then bwd_data and bwd_weight (one call). At
+    p = 0.5 the pattern keeps every second neuron (K = e_2, the offset drawn
+    per step); at other rates (dp, offset) come from the K searched for p."""
+
+    def __init__(self, name, n_in, n_out, batch, dtype, w_std, seed):
+        import torch
+        from paper_1805_08939_amd import api, synth
+        self.api, self.torch = api, torch
+        self.name, self.K, self.N, self.B, self.dtype = name, n_in, n_out, batch, dtype
+        self.ard_dtype = api.ARD_F32 if dtype == "f32" else api.ARD_BF16
+        dev = torch.device("cuda:0")
+        g = synth.generator(seed)
+        sdt = synth.storage_dtype(dtype)
+        X = synth.to_storage(synth.normal(g, (batch, n_in)), dtype)
+        W = synth.to_storage(synth.normal(g, (n_out, n_in), w_std), dtype)
+        dY = synth.to_storage(synth.normal(g, (batch, n_out)), dtype)
+        self._host_src = (X, W, dY)
+        self.Xt, self.W, self.dYt = X.T.contiguous().to(dev), W.to(dev), dY.T.contiguous().to(dev)
+        self.bias = torch.zeros(n_out, device=dev)
+        self.Yt = torch.zeros(n_out, batch, dtype=sdt, device=dev)
+        self.dXt = torch.zeros(n_in, batch, dtype=sdt, device=dev)
+        self.dW = torch.zeros(n_out, n_in, device=dev)
+        self.db = torch.zeros(n_out, device=dev)
+        self.plan = api.ard_row_plan()
+        self.desc = api.fc_desc(self.ard_dtype, batch, n_in, n_out, None, self.plan, 1.0, api.ARD_ACT_NONE,
+                                api.ARD_DROPPED_SKIP)
+        self.ws = torch.empty(max(api.ard_fc_workspace_bytes(
+            api.fc_desc(self.ard_dtype, batch, n_in, n_out)), 16) // 4, device=dev)
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.order = [("fwd", 0), ("bwd", 0)]
+        self.config = {"workload": name, "global_batch": batch, "layer": [n_in, n_out],
+                       "patterns": "row-based on the outputs: K = e_2 at p = 0.5 (every second neuron kept, offset "
+                                   "drawn per step), else sampled per step from K(p), n_max 16",
+                       "dropped": "skip"}
+
+    def set_rate(self, p):
+        import numpy as np
+        self.p = p
+        if p == 0.5:
+            self.Kdist = np.zeros(16)
+            self.Kdist[1] = 1.0
+        else:
+            self.Kdist, _ = self.api.ard_search_distribution(p)
+
+    def patterns(self, it):
+        return [self.api.ard_sample_row_pattern(self.Kdist, PATTERN_SEED, 1, it)]
+
+    def kept_flops(self, pats):
+        f = 2.0 * self.B * self.K * self.api.ard_row_kept(self.N, *pats[0])
+        per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
+        return 3.0 * f, per
+
+    def prepare(self, it):
+        api, st = self.api, self.stream
+        pats = self.patterns(it)
+        api.ard_plan_rows(self.N, *pats[0], None, st, plan=self.plan)
+        d, ws = self.desc, (self.ws.data_ptr(), self.ws.numel() * 4)
+        calls = {("fwd", 0): (api.ard_fc_fwd, (d, self.Xt, self.W, self.bias, self.Yt, ws, st), {}),
+                 ("bwd", 0): (api.ard_fc_bwd, (d, self.Xt, self.dYt, None, self.W, self.dXt, self.dW, self.db, ws,
+                                               st), {})}
+        return pats, calls
+
+    step = Mlp.step
+
+    def oracle_step(self, pats):
+        from oracle import fc as ofc
+        from oracle import patterns as opat
+        X, W, dY = self._host
+        m_in, m_out = opat.row_mask(self.K, 1, 0), opat.row_mask(self.N, *pats[0])
+        Y = ofc.fc_forward(X, W, None, m_in, m_out)
+        return ofc.fc_backward(X, W, Y, dY, m_in, m_out)
+
+    def host_copies(self):
+        from paper_1805_08939_amd import synth
+        self._host = tuple(synth.as_f64(t).numpy() for t in self._host_src)
 
 
 class TileLayer:
@@ -348,15 +409,6 @@ class TileLayer:
         per = {key: f for key in self.order}
         return sum(per.values()), per
 
-    def gemm_shape(self, pats, kind, l):
-        if isinstance(pats, int):
-            pats = self.patterns(pats)
-        return (self.N, self.B, self.K, pats[1])
-
-    @staticmethod
-    def shape_label(shape):
-        return "N x B x K = %d x %d x %d, %d kept 64 x 64 tiles" % tuple(shape)
-
     def prepare(self, it):
         api = self.api
         plan = api.ard_plan_tiles_bernoulli(self.N, self.K, self.tile, self.p, PATTERN_SEED, 0, it, self.bits_dev,
@@ -368,7 +420,6 @@ class TileLayer:
         return it, calls
 
     step = Mlp.step
-    replay = Mlp.replay
 
     def oracle_step(self, pats):
         import numpy as np
@@ -476,13 +527,6 @@ class Lstm:
         per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
         return 3.0 * f, per
 
-    def gemm_shape(self, pats, kind, l):
-        return (self.T, self.B, self.I, self.api.ard_row_kept(self.H, *pats[0]))
-
-    @staticmethod
-    def shape_label(shape):
-        return "T, B, I = %d, %d, %d, %d kept hidden units" % tuple(shape)
-
     def prepare(self, it):
         api, st = self.api, self.stream
         pats = self.patterns(it)
@@ -495,7 +539,6 @@ class Lstm:
         return pats, calls
 
     step = Mlp.step
-    replay = Mlp.replay
 
     def oracle_step(self, pats):
         from oracle import lstm as olstm
@@ -570,13 +613,6 @@ class LstmStack:
         per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
         return 3.0 * f, per
 
-    def gemm_shape(self, pats, kind, l):
-        return tuple([self.T, self.B, self.I] + self.kept(pats))
-
-    def shape_label(self, shape):
-        return "T, B, I = %d, %d, %d, kept hidden units per layer %s" % (shape[0], shape[1], shape[2],
-                                                                          list(shape[3:]))
-
     def prepare(self, it):
         api, st = self.api, self.stream
         pats = self.patterns(it)
@@ -598,7 +634,6 @@ class LstmStack:
         return pats, {("fwd", 0): (fwd, (), {}), ("bwd", 0): (bwd, (), {})}
 
     step = Mlp.step
-    replay = Mlp.replay
 
     def host_copies(self):
         self._host = {"X": self.X.double().cpu().numpy().transpose(0, 2, 1),
@@ -677,13 +712,6 @@ class LstmTile:
         per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
         return 3.0 * f, per
 
-    def gemm_shape(self, pats, kind, l):
-        return (self.T, self.B, self.I, self.H, self.tdp_bits[tuple(pats[0])][1])
-
-    @staticmethod
-    def shape_label(shape):
-        return "T, B, I, H = %d, %d, %d, %d, %d kept 64 x 64 tiles of W" % tuple(shape)
-
     def prepare(self, it):
         api, st = self.api, self.stream
         pats = self.patterns(it)
@@ -699,7 +727,6 @@ class LstmTile:
         return pats, calls
 
     step = Mlp.step
-    replay = Mlp.replay
 
     def host_copies(self):
         self._host = (self.X.double().cpu().numpy().transpose(0, 2, 1), self.W.double().cpu().numpy(),
@@ -719,6 +746,8 @@ class LstmTile:
 
 
 WORKLOADS = {
+    "fc784": dict(cls="FcLayer", name="fc-784x512-fp32-b64", n_in=784, n_out=512, batch=64, dtype="f32",
+                  w_std=0.05, seed=1805 + 0),
     "mlp784": dict(cls="Mlp", name="mlp-784-2048-2048-10-fp32-b128", dims=[784, 2048, 2048, 10], batch=128,
                    dtype="f32", init="xavier", seed=1805 + 1),
     "tile4096": dict(cls="TileLayer", name="tile-4096x4096-bf16-b512-t64", n=4096, k=4096, batch=512, tile=64,
@@ -738,37 +767,54 @@ WORKLOADS = {
 }
 
 
-def time_steps(wl, steps, warmup, it0, timed_call=None):
+def time_steps(wl, steps, warmup, it0):
+    """GPU time of `steps` steps after `warmup` untimed ones: one HIP event
+    pair on the step stream around the whole run; FLOPs counted afterwards
+    from the host sampler's patterns."""
     import torch
     for i in range(warmup):
         wl.step(it0 + i)
     torch.cuda.synchronize()
-    ev = None
-    durs = []
-    total_flops = 0.0
-    call_flops = 0.0
-    if timed_call is not None:
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     start.record()
-    shapes = []
-    all_pats = [wl.step(it0 + warmup + i, timed_call, ev[i] if ev else None) for i in range(steps)]
+    all_pats = [wl.step(it0 + warmup + i)[0] for i in range(steps)]
     end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    for i, pats in enumerate(all_pats):  # FLOP accounting off the timed path
-        f, per = wl.kept_flops(pats)
-        total_flops += f
-        if timed_call is not None:
-            call_flops += per[timed_call]
-            shapes.append((wl.gemm_shape(pats, *timed_call), per[timed_call], it0 + warmup + i))
-    gpu_ms = start.elapsed_time(end)
-    if ev:
-        durs = [a.elapsed_time(b) for a, b in ev]
-    return {"ms": gpu_ms, "wall_s": wall, "flops": total_flops, "call_ms": durs, "call_flops": call_flops,
-            "call_shapes": shapes}
+    total_flops = sum(wl.kept_flops(pats)[0] for pats in all_pats)  # FLOP accounting off the timed path
+    return {"ms": start.elapsed_time(end), "wall_s": wall, "flops": total_flops}
+
+
+def roofline_pass(wl, steps, warmup, it0):
+    """The same steps once more with every layer call bracketed by a HIP event
+    pair on the step stream. Returns, per call key and in total, the number of
+    calls, the summed event time and the summed kept FLOPs, plus the whole
+    pass's GPU time."""
+    import torch
+    for i in range(warmup):
+        wl.step(it0 + i)
+    torch.cuda.synchronize()
+    n = steps * len(wl.order)
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    runs = [wl.step(it0 + warmup + i, events) for i in range(steps)]
+    end.record()
+    torch.cuda.synchronize()
+    per = {}
+    for pats, used in runs:
+        _, fl = wl.kept_flops(pats)
+        for key, e0, e1 in used:
+            rec = per.setdefault(key, [0, 0.0, 0.0])
+            rec[0] += 1
+            rec[1] += e0.elapsed_time(e1)
+            rec[2] += fl[key]
+    calls = sum(r[0] for r in per.values())
+    ms = sum(r[1] for r in per.values())
+    flops = sum(r[2] for r in per.values())
+    return {"calls": calls, "ms": ms, "flops": flops, "per": per, "pass_ms": start.elapsed_time(end)}
 
 
 def time_conventional(wl, steps, warmup, it0):
@@ -810,20 +856,6 @@ def time_training(wl, steps, warmup, it0, conventional):
     return start.elapsed_time(end)
 
 
-def roofline_call(wl, first_it, steps):
-    """The one-GEMM call with the most kept work over the timed steps (summed kept
-    FLOPs; ties go to the first call of a step). The patterns are seeded, so
-    the choice is the same in every run of the same command."""
-    keys = getattr(wl, "roofline_keys", wl.order)
-    totals = {}
-    for i in range(steps):
-        _, per = wl.kept_flops(wl.patterns(first_it + i))
-        for key in keys:
-            totals[key] = totals.get(key, 0.0) + per.get(key, 0.0)
-    best = max(totals.values())
-    return next(k for k in keys if totals.get(k, 0.0) == best)
-
-
 def cpu_baseline(wl, p, budget_s):
     """The oracle on the host cores: as many steps as fit in ~budget_s."""
     try:
@@ -859,11 +891,12 @@ def source_digest():
     return h.hexdigest()
 
 
-def traffic_record(workload, kind, layer, shape):
-    """HBM bytes per launch of the roofline call, from the committed rocprofv3
-    counter summaries (FETCH_SIZE and WRITE_SIZE passes, each scaled by what the
-    counter reads for a plain copy of known size). None when no summary covers
-    this call and shape, or when the kernel sources changed since."""
+def traffic_record(workload, p, steps):
+    """HBM bytes per layer call of the roofline pass, from the committed
+    rocprofv3 counter summaries (FETCH_SIZE and WRITE_SIZE passes over the same
+    command, each scaled by what the counter reads for a plain copy of known
+    size). None when no summary covers this workload, rate and step count, or
+    when the kernel sources changed since."""
     pdir = os.path.join(ROOT, "profiles")
     if not os.path.isdir(pdir):
         return None
@@ -876,9 +909,9 @@ def traffic_record(workload, kind, layer, shape):
                 if not line.startswith("traffic-record: "):
                     continue
                 rec = json.loads(line[len("traffic-record: "):])
-                if (rec.get("workload") == workload and rec.get("call") == [kind, layer]
-                        and rec.get("shape") == list(shape) and rec.get("source_digest") == digest):
-                    return rec["bytes_per_launch"]
+                if (rec.get("workload") == workload and rec.get("p") == p and rec.get("steps") == steps
+                        and rec.get("source_digest") == digest):
+                    return rec["bytes_per_call"]
     return None
 
 
@@ -978,22 +1011,22 @@ def summarize_counters(path, top, last=0, tail=0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mlp784", choices=sorted(WORKLOADS))
-    ap.add_argument("--p", type=float, default=0.5, help="dropout rate of the headline value")
+    ap.add_argument("--workload", default="mlp8192", choices=sorted(WORKLOADS))
+    ap.add_argument("--p", type=float, default=0.7, help="dropout rate of the headline value")
     ap.add_argument("--dropped", default="skip", choices=["skip", "zero"],
                     help="MLP workloads: dropped outputs and gradients left untouched (skip) or written 0 (zero)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the conventional-dropout and training-step comparisons")
     ap.add_argument("--summarize-trace", metavar="CSV", help="print a per-kernel table of a rocprofv3 kernel trace")
     ap.add_argument("--summarize-counters", metavar="CSV", help="print per-kernel means of a rocprofv3 counter run")
     ap.add_argument("--top", type=int, default=25)
     ap.add_argument("--last", type=int, default=0, help="--summarize-trace / --summarize-counters: only the last N dispatches per kernel")
     ap.add_argument("--tail", type=int, default=0,
                     help="--summarize-trace / --summarize-counters: only the run's last N dispatches")
-    ap.add_argument("--replay", type=int, default=20,
-                    help="launches of the roofline call replayed after the timed steps to time the kernel")
     ap.add_argument("--digest", action="store_true", help="print the kernel source digest")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 1 GiB (3 times), the reference for HBM counters")
@@ -1022,7 +1055,7 @@ def main():
     from paper_1805_08939_amd import _ffi
     _ffi.lib()
     spec = dict(WORKLOADS[args.workload])
-    cls = {"Mlp": Mlp, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm,
+    cls = {"Mlp": Mlp, "FcLayer": FcLayer, "TileLayer": TileLayer, "TileLayerTdp": TileLayerTdp, "Lstm": Lstm,
            "LstmStack": LstmStack, "LstmTile": LstmTile}[spec.pop("cls")]
     if args.dropped != "skip":
         if cls is not Mlp:
@@ -1031,7 +1064,7 @@ def main():
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:
-        wl.host_copies()  # the oracle's inputs, taken before any GPU timing: the replay below is the last GPU work
+        wl.host_copies()  # the oracle's inputs, taken before any GPU timing
 
     rates = sorted({0.0, 0.3, 0.5, 0.7, args.p})
     # Alg. 1 on the host, once per rate (a one-time cost, outside the timed steps)
@@ -1046,20 +1079,23 @@ def main():
     results = {}
     for i, p in enumerate(rates):
         wl.set_rate(p)
-        it0 = 1_000_000 * (i + 1)
-        timed = None
-        if p == args.p:
-            timed = roofline_call(wl, it0 + args.warmup, args.steps)
-        r = time_steps(wl, args.steps, args.warmup, it0, timed)
-        r["timed_call"] = timed
+        r = time_steps(wl, args.steps, args.warmup, 1_000_000 * (i + 1))
         results[p] = r
         print(f"# p={p}: {r['ms'] / args.steps:.4f} ms/step, kept {r['flops'] / args.steps / 1e9:.3f} GFLOP/step, "
               f"{r['flops'] / (r['ms'] * 1e-3) / 1e12:.3f} TFLOP/s", file=sys.stderr, flush=True)
 
+    # the roofline: the headline steps again (same iterations, so the same
+    # patterns), every layer call bracketed by HIP events on the step stream
+    wl.set_rate(args.p)
+    head_it0 = 1_000_000 * (rates.index(args.p) + 1)
+    rp = roofline_pass(wl, args.steps, args.warmup, head_it0)
+    print(f"# roofline pass p={args.p}: {rp['calls']} layer calls, {rp['ms'] / rp['calls'] * 1e3:.2f} us per call, "
+          f"{rp['flops'] / (rp['ms'] * 1e-3) / 1e12:.3f} TFLOP/s over the calls", file=sys.stderr, flush=True)
+
     # the paper's own baseline (Sec. II-C, Sec. IV): conventional dropout on the
     # same network, dense GEMMs plus element masks, at the same rates
     conventional = None
-    if hasattr(wl, "conventional_step"):
+    if hasattr(wl, "conventional_step") and not args.no_baselines:
         conventional = {"ms_per_step": {}, "speedup_vs_conventional": {}, "training_time_reduction": {}}
         for i, p in enumerate(rates):
             if p == 0.0:
@@ -1076,7 +1112,7 @@ def main():
     # whole training steps: the same comparison with the optimizer update of
     # every layer after each step (the weights are restored afterwards)
     training = None
-    if hasattr(wl, "sgd_step"):
+    if hasattr(wl, "sgd_step") and not args.no_baselines:
         saved = [w.clone() for w in wl.W]
         training = {"approximate_ms": {}, "conventional_ms": {}, "training_time_reduction": {}}
         for i, p in enumerate(rates):
@@ -1100,34 +1136,18 @@ def main():
     t0 = results[0.0]["ms"]
     speedup = {f"{p}": t0 / results[p]["ms"] for p in rates if p > 0}
     kept_frac = {f"{p}": (results[p]["flops"] / results[0.0]["flops"]) for p in rates if p > 0}
-    # the roofline call's launches in the timed region, grouped by GEMM shape
-    # (patterns change per step); the shape with the most kept work is the
-    # roofline kernel: one tile configuration and launch grid
-    kind, layer = head["timed_call"]
-    groups = {}
-    for (shape, fl, it), ms in zip(head["call_shapes"], head["call_ms"]):
-        g = groups.setdefault(shape, [0, 0.0, 0.0, it])
-        g[0] += 1
-        g[1] += ms
-        g[2] += fl
-    shape, (count, ms_sum, fl_sum, shape_it) = max(groups.items(), key=lambda kv: (kv[1][2], kv[0]))
-    call_ms, call_flops = ms_sum / count, fl_sum / count
-    # the kernel's own launch duration: the same call at the same shape replayed
-    # back to back right after the timed steps (in the steps, a small call's
-    # event bracket also holds the time its launch waits for the host)
-    wl.set_rate(args.p)
-    launch_ms = wl.replay(shape_it, (kind, layer), args.replay)
-    print(f"# replayed {kind} layer {layer} of step {shape_it} ({shape}) {args.replay} times: "
-          f"{launch_ms * 1e3:.2f} us per launch", file=sys.stderr, flush=True)
-    achieved = call_flops / (launch_ms * 1e-3) / 1e12
+    achieved = rp["flops"] / (rp["ms"] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
                 "frac": achieved / PEAK_TFLOPS[dtype],
-                "traffic": traffic_record(spec["name"], kind, layer, shape),
-                "kernel": f"{kind} call, layer {layer}, {wl.shape_label(shape)}",
-                "avg_launch_us": launch_ms * 1e3, "launches": args.replay, "flops_per_launch": call_flops,
-                "in_step": {"avg_call_us": call_ms * 1e3, "calls": count,
-                            "achieved": call_flops / (call_ms * 1e-3) / 1e12},
-                "call_share_of_step": sum(head["call_ms"]) / head["ms"]}
+                "traffic": traffic_record(spec["name"], args.p, args.steps),
+                "kernel": "every layer GEMM call of the timed steps at p=%g (%s), kept FLOPs only" % (
+                    args.p, ", ".join("%s %d" % k for k in wl.order)),
+                "avg_launch_us": rp["ms"] / rp["calls"] * 1e3, "launches": rp["calls"],
+                "flops_per_launch": rp["flops"] / rp["calls"],
+                "per_call": {"%s %d" % k: {"calls": r[0], "avg_us": r[1] / r[0] * 1e3,
+                                           "tflops": r[2] / (r[1] * 1e-3) / 1e12 if r[1] > 0 else 0.0}
+                             for k, r in rp["per"].items()},
+                "call_share_of_step": rp["ms"] / rp["pass_ms"]}
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms"] / args.steps, "higher_is_better": True,
@@ -1135,6 +1155,7 @@ def main():
         "config": dict(wl.config, p=args.p),
         "speedup_vs_p0": speedup,
         "kept_flop_fraction": kept_frac,
+        "time_fraction_vs_p0": {f"{p}": results[p]["ms"] / t0 for p in rates if p > 0},
         "per_p": {f"{p}": {"ms_per_step": results[p]["ms"] / args.steps,
                            "host_ms_per_step": results[p]["wall_s"] * 1e3 / args.steps,
                            "tflops_kept": results[p]["flops"] / (results[p]["ms"] * 1e-3) / 1e12}

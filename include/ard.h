@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define ARD_VERSION 1
+#define ARD_VERSION 2
 
 typedef enum {
   ARD_OK = 0,
@@ -239,17 +239,31 @@ int ard_plan_tiles_bernoulli(int32_t n, int32_t k, int32_t tile, double p, uint6
 typedef enum { ARD_ACT_NONE = 0, ARD_ACT_RELU = 1 } ard_act;
 typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
 /*
- * How the W argument of fwd / bwd_data is stored:
- *   ARD_WEIGHTS_FULL   : the full W[N][K];
- *   ARD_WEIGHTS_COMPACT: the compact Wc[kept_out][ldc] written by
- *                        ard_fc_compact_weights for this descriptor's patterns,
- *                        Wc[i][j] = W[S_out(i)][S_in(j)] (Sec. III-A's compact
- *                        weight matrix), ldc = ard_fc_compact_ld(desc).
+ * How the W argument of fwd / bwd_data (and the dW of bwd_weight) is stored:
+ *   ARD_WEIGHTS_FULL        : the full W[N][K]; dW[N][K].
+ *   ARD_WEIGHTS_COMPACT     : the compact Wc[kept_out][ldc] written by
+ *                             ard_fc_compact_weights for this descriptor's
+ *                             patterns, Wc[i][j] = W[S_out(i)][S_in(j)]
+ *                             (Sec. III-A's compact weight matrix),
+ *                             ldc = ard_fc_compact_ld(desc); dW[N][K].
+ *   ARD_WEIGHTS_COMPACT_GRAD: W as for COMPACT, and bwd_weight writes the
+ *                             gradient of the compact matrix,
+ *                             dWc[i][j] = dW[S_out(i)][S_in(j)], as fp32
+ *                             [kept_out][ldc] (columns kept_in..ldc-1 are not
+ *                             written; the dropped/ZERO rule does not apply to
+ *                             it). Every store of dW is then a whole row run:
+ *                             with a strided input side, a full-layout dW
+ *                             leaves every 32-byte sector partly written.
+ *                             ard_fc_sgd_momentum takes dW in this layout too.
  * With FULL weights and a gathered input side, fwd and bwd_data build the
  * compact copy in their workspace themselves; a training step that compacts
  * once and passes COMPACT to both saves one pass over W.
  */
-typedef enum { ARD_WEIGHTS_FULL = 0, ARD_WEIGHTS_COMPACT = 1 } ard_weight_layout;
+typedef enum {
+  ARD_WEIGHTS_FULL = 0,
+  ARD_WEIGHTS_COMPACT = 1,
+  ARD_WEIGHTS_COMPACT_GRAD = 2
+} ard_weight_layout;
 
 typedef struct {
   int32_t dtype;        /* ard_dtype */
@@ -318,8 +332,10 @@ int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const v
  * momentum SGD): for every kept output row n and kept input column k,
  *   V[n][k] = momentum * V[n][k] + dW[n][k],  W[n][k] -= lr * V[n][k],
  * and for the kept rows' bias entries the same with Vb, dbias. W is the full
- * [N][K] matrix of the descriptor's dtype (its weight_layout is ignored), V,
- * dW [N][K] fp32, bias, Vb, dbias [N] fp32 (all three given or all NULL).
+ * [N][K] matrix of the descriptor's dtype, V [N][K] fp32, dW [N][K] fp32, or
+ * the compact dWc[kept_out][ldc] when the descriptor's weight_layout is
+ * ARD_WEIGHTS_COMPACT_GRAD, bias, Vb, dbias [N] fp32 (all three given or all
+ * NULL).
  * Dropped weights, their momentum and their bias entries are left untouched:
  * they are frozen for the step (the reading of an update restricted to the
  * kept rows). All device, caller-owned.

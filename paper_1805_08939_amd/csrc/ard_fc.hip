@@ -47,10 +47,11 @@ __global__ void zero_dropped_weights_kernel(float* __restrict__ dW, int32_t K, i
 // rows n = out_offset + out_period i and kept columns k = in_offset +
 // in_period j, V = mu V + dW and W -= lr V; the same for the bias entries of
 // kept rows. Dropped weights, their momentum and their bias entries keep their
-// values (frozen for the step). One block per kept row.
+// values (frozen for the step). One block per kept row. ldg > 0: the gradient
+// is the compact dWc[i][j] with rows of ldg; else dW[n][k], rows of K.
 template <typename T>
 __global__ void __launch_bounds__(256) sgd_momentum_kernel(T* __restrict__ W, float* __restrict__ V,
-                                                           const float* __restrict__ dW, int32_t K,
+                                                           const float* __restrict__ dW, int32_t K, int64_t ldg,
                                                            int32_t out_period, int32_t out_offset, int32_t in_period,
                                                            int32_t in_offset, int32_t kin, float* __restrict__ bias,
                                                            float* __restrict__ Vb, const float* __restrict__ db,
@@ -58,10 +59,10 @@ __global__ void __launch_bounds__(256) sgd_momentum_kernel(T* __restrict__ W, fl
   const int64_t n = out_offset + static_cast<int64_t>(out_period) * blockIdx.x;
   T* w = W + n * K;
   float* v = V + n * K;
-  const float* g = dW + n * K;
+  const float* g = ldg > 0 ? dW + static_cast<int64_t>(blockIdx.x) * ldg : dW + n * K;
   for (int64_t j = threadIdx.x; j < kin; j += 256) {
     const int64_t k = in_offset + static_cast<int64_t>(in_period) * j;
-    const float vn = mu * v[k] + g[k];
+    const float vn = mu * v[k] + g[ldg > 0 ? j : k];
     v[k] = vn;
     w[k] = from_f32<T>(to_f32(w[k]) - lr * vn);
   }
@@ -193,6 +194,7 @@ struct FcShape {
   size_t esize;
   int64_t ldc;                       // compact weight row length
   bool compact_given;                // W argument is the compact matrix
+  bool grad_compact;                 // dW is written as the compact dWc[kout][ldc]
   bool needs_compact;                // fwd / bwd_data gather W through a compact copy
 };
 
@@ -207,7 +209,8 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
     return fail(ARD_ERR_INVALID_ARG, "unknown activation %d", d->act);
   if (d->dropped != ARD_DROPPED_ZERO && d->dropped != ARD_DROPPED_SKIP)
     return fail(ARD_ERR_INVALID_ARG, "unknown dropped-output mode %d", d->dropped);
-  if (d->weight_layout != ARD_WEIGHTS_FULL && d->weight_layout != ARD_WEIGHTS_COMPACT)
+  if (d->weight_layout != ARD_WEIGHTS_FULL && d->weight_layout != ARD_WEIGHTS_COMPACT &&
+      d->weight_layout != ARD_WEIGHTS_COMPACT_GRAD)
     return fail(ARD_ERR_INVALID_ARG, "unknown weight layout %d", d->weight_layout);
   if (!(d->scale == d->scale) || d->scale == __builtin_inff() || d->scale == -__builtin_inff())
     return fail(ARD_ERR_INVALID_ARG, "scale must be finite");
@@ -228,7 +231,8 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   s->out_offset = out_all ? 0 : d->out_plan->offset;
   s->esize = d->dtype == ARD_BF16 ? 2 : 4;
   s->ldc = (static_cast<int64_t>(s->kin) + 7) / 8 * 8;
-  s->compact_given = d->weight_layout == ARD_WEIGHTS_COMPACT;
+  s->compact_given = d->weight_layout != ARD_WEIGHTS_FULL;
+  s->grad_compact = d->weight_layout == ARD_WEIGHTS_COMPACT_GRAD;
   s->needs_compact = !s->compact_given && s->in_period > 1;
   return ARD_OK;
 }
@@ -386,7 +390,7 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
                     nullptr);
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok(g, sizeof(T))) {
+  if (fast_ok<false, true>(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -432,8 +436,11 @@ GemmArgs bwd_weight_args(const ard_fc_desc* d, const FcShape& s, const void* Xt,
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   g.a = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
   g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
-  g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
-                    d->scale, nullptr);
+  if (s.grad_compact)  // dWc[i][j]: contiguous rows of ldc
+    g.c = strided_out(dW, s.ldc, sizeof(float), 1, 0, 1, 0, nullptr, 0, d->scale, nullptr);
+  else
+    g.c = strided_out(dW, s.K, sizeof(float), s.out_period, s.out_offset, s.in_period, s.in_offset, nullptr, 0,
+                      d->scale, nullptr);
   return g;
 }
 
@@ -463,9 +470,11 @@ int finish_bwd_weight(const ard_fc_desc* d, const FcShape& s, const void* dYt, c
     ARD_LAUNCH_CHECK();
   }
   if (d->dropped == ARD_DROPPED_ZERO && (s.out_period > 1 || s.in_period > 1)) {
-    hipLaunchKernelGGL(zero_dropped_weights_kernel, dim3(s.N), dim3(256), 0, stream, dW, s.K,
-                       s.out_period, s.out_offset, s.in_period, s.in_offset);
-    ARD_LAUNCH_CHECK();
+    if (!s.grad_compact) {  // a compact gradient has no dropped entries
+      hipLaunchKernelGGL(zero_dropped_weights_kernel, dim3(s.N), dim3(256), 0, stream, dW, s.K,
+                         s.out_period, s.out_offset, s.in_period, s.in_offset);
+      ARD_LAUNCH_CHECK();
+    }
     if (dbias && s.out_period > 1) {
       hipLaunchKernelGGL(zero_dropped_rows_kernel<float>, dim3(s.N), dim3(64), 0, stream, dbias,
                          static_cast<int64_t>(1), 1, s.out_period, s.out_offset);
@@ -481,7 +490,7 @@ int run_bwd_data(const ard_fc_desc* d, const FcShape& s, const GemmArgs& g, cons
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok(g, sizeof(T))) {
+  if (fast_ok<true, true>(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
@@ -512,7 +521,7 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
   bool dbias_done = false;
-  if (fast_ok(g, sizeof(T))) {
+  if (fast_ok<false, false>(g, sizeof(T))) {
     // dbias = scale * G 1: the row sums of A, taken by the same kernel
     if (dbias) {
       g.rsum = dbias + s.out_offset;
@@ -543,7 +552,7 @@ int fc_bwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   if (st != ARD_OK) return st;
   const GemmArgs gd = bwd_data_args<T>(d, s, dYt, Yt, wv.op, dXt, Xgate);
   GemmArgs gw = bwd_weight_args<T>(d, s, Xt, dYt, Yt, dW);
-  if (fast_ok(gd, sizeof(T)) && fast_ok(gw, sizeof(T)) && fast_pair_ok<T>(gd, gw)) {
+  if (fast_ok<true, true>(gd, sizeof(T)) && fast_ok<false, false>(gw, sizeof(T)) && fast_pair_ok<T>(gd, gw)) {
     if (dbias) {
       gw.rsum = dbias + s.out_offset;
       gw.rsum_ld = s.out_period;
@@ -660,12 +669,14 @@ int ard_fc_sgd_momentum(const ard_fc_desc* desc, void* W, float* V, const float*
   if (!(lr == lr) || !(momentum == momentum)) return fail(ARD_ERR_INVALID_ARG, "lr and momentum must be numbers");
   if (s.kout == 0) return ARD_OK;
   hipStream_t sm = static_cast<hipStream_t>(stream);
+  const int64_t ldg = s.grad_compact ? s.ldc : 0;
   if (desc->dtype == ARD_BF16)
     hipLaunchKernelGGL(sgd_momentum_kernel<bf16>, dim3(s.kout), dim3(256), 0, sm, static_cast<bf16*>(W), V, dW, s.K,
-                       s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr, momentum);
+                       ldg, s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr,
+                       momentum);
   else
     hipLaunchKernelGGL(sgd_momentum_kernel<float>, dim3(s.kout), dim3(256), 0, sm, static_cast<float*>(W), V, dW,
-                       s.K, s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr,
+                       s.K, ldg, s.out_period, s.out_offset, s.in_period, s.in_offset, s.kin, bias, Vb, dbias, lr,
                        momentum);
   ARD_LAUNCH_CHECK();
   return ARD_OK;

@@ -773,19 +773,25 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_pair_kernel(GemmArgs g1, Ge
   }
 }
 
-// Whether a problem can run on fast_gemm_kernel: every operand is a plain
-// strided view read in whole 16-byte chunks, and every chunk of a slab lies
-// less than 2^31 bytes past the slab's first element.
+// Whether a problem can run on fast_gemm_kernel with operand A m-contiguous
+// (AMC) or not, B n-contiguous (BMC) or not: every operand is a plain strided
+// view read in whole 16-byte chunks, and every chunk of a slab lies less than
+// 2^31 bytes past the slab's first element (the lanes' 32-bit load offsets;
+// the slab base itself is a 64-bit pointer). A slab of a k-contiguous operand
+// spans rows 0 .. ext - 1 of ld elements, BK <= 256 k each; one of an
+// m/n-contiguous operand spans at most 256 k-rows of ld elements and columns
+// 0 .. ext - 1.
+template <bool AMC, bool BMC>
 inline bool fast_ok(const GemmArgs& g, size_t esize) {
   const int64_t epc = static_cast<int64_t>(16 / esize);
-  auto ok = [epc, esize, &g](const GemmOperand& o, int ext) {
-    int64_t rows = ext > g.K ? ext : g.K;
-    rows = (rows > 256 ? rows : 256) + 1;  // a slab spans at most 256 k-rows
+  auto ok = [epc, esize](const GemmOperand& o, int ext, bool mc) {
+    const int64_t e = ext > 0 ? ext : 1;
+    const int64_t span = mc ? e + 256 * o.ld : (e - 1) * o.ld + 256;
     return o.ridx == nullptr && o.cidx == nullptr && o.y == nullptr && o.ld % epc == 0 && o.bstride % epc == 0 &&
-           o.kbstride % epc == 0 && (reinterpret_cast<uintptr_t>(o.p) & 15u) == 0 &&
-           rows * o.ld * static_cast<int64_t>(esize) < (int64_t{1} << 31);
+           o.kbstride % epc == 0 && (reinterpret_cast<uintptr_t>(o.p) & 15u) == 0 && o.ld >= 0 &&
+           span * static_cast<int64_t>(esize) < (int64_t{1} << 31);
   };
-  return ok(g.a, g.M) && ok(g.b, g.N);
+  return ok(g.a, g.M, AMC) && ok(g.b, g.N, BMC);
 }
 
 // Configurations: large tiles for large grids, 32x32 tiles with the k of each

@@ -542,7 +542,7 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   g.c = {s.Z, L.B, nullptr, nullptr, L.G4 * L.B, reinterpret_cast<const float*>(w + L.bc), 0, 1.0f};
   const bool kw_vec = L.KW % 4 == 0;
   const bool b_vec = L.B % 4 == 0 && L.I % 4 == 0;
-  if (fast_ok(g, sizeof(float))) {
+  if (fast_ok<false, true>(g, sizeof(float))) {
     ARD_HIP_CHECK((run_fast_gemm<float, false, true, float, EPI_FWD>(g, static_cast<int>(L.T), sm, nullptr)));
   } else {
     ARD_HIP_CHECK((run_gemm<float, float, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -660,7 +660,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     gr.a = {s.Wc + L.Ic, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
     gr.b = {s.dA, nullptr, L.B, nullptr, nullptr, gr.K * L.B, 0, 1.0f, 0};
     gr.c = {part, L.B, nullptr, nullptr, nsB, nullptr, 0, 1.0f};
-    rec_fast = fast_ok(gr, sizeof(float));
+    rec_fast = fast_ok<true, true>(gr, sizeof(float));
     if (rec_fast) {
       ks = gr.K;
       splits = fs;
@@ -734,7 +734,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     gr.b = {s.Hc, nullptr, L.B, nullptr, nullptr, 0, 0, 1.0f, nsB};
     gr.c.p = dW + static_cast<int64_t>(offset) * colsW + L.I + offset;
     gr.c.col_stride = period;
-    if (fast_ok(g, sizeof(float)) && fast_ok(gr, sizeof(float))) {
+    if (fast_ok<false, false>(g, sizeof(float)) && fast_ok<false, false>(gr, sizeof(float))) {
       // dbias[q H + S(u)] = sum over t, b of dA: the row sums of the first product's A
       if (dbias) {
         g.rsum = dbias + offset;
@@ -794,7 +794,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     g.b = {s.dA, nullptr, L.B, nullptr, nullptr, L.G4 * L.B, 0, 1.0f, 0};
     // rows io + ip * k of dX[t]; the rows of dropped inputs are written 0
     g.c = {static_cast<float*>(dX) + L.io * L.B, L.ip * L.B, nullptr, nullptr, L.I * L.B, nullptr, 0, 1.0f};
-    if (fast_ok(g, sizeof(float))) {
+    if (fast_ok<true, true>(g, sizeof(float))) {
       ARD_HIP_CHECK((run_fast_gemm<float, true, true, float, EPI_FWD>(g, static_cast<int>(L.T), sm, nullptr)));
     } else {
       ARD_HIP_CHECK((run_gemm<float, float, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(

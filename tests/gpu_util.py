@@ -73,3 +73,22 @@ def workspace(nbytes):
     if nbytes == 0:
         return None
     return torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=device())
+
+
+def full_weight_grad(mlp, l, pats, fill):
+    """Layer l's weight gradient after a step of the benchmark's MLP, as a
+    full [N][K] fp64 array: a layer whose inputs were dropped that step wrote
+    the compact gradient dWc[kept_out][ldc] into its dW buffer; its entries are
+    placed at [S_out][S_in] and every other entry gets fill."""
+    dW = mlp.dW[l].double().cpu().numpy()
+    if l not in mlp.step_compact:
+        return dW
+    N, K = dW.shape
+    pin = pats[l - 1]
+    pout = pats[l] if l < mlp.L - 1 else (1, 0)
+    Sin, Sout = opat.row_kept_list(K, *pin), opat.row_kept_list(N, *pout)
+    ldc = (len(Sin) + 7) // 8 * 8
+    dWc = dW.reshape(-1)[:len(Sout) * ldc].reshape(len(Sout), ldc)[:, :len(Sin)]
+    full = np.full((N, K), fill)
+    full[np.ix_(Sout, Sin)] = dWc
+    return full

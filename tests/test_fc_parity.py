@@ -82,6 +82,29 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
         api.ard_fc_bwd_data(cdesc, dYt, Yst, Wc, dXt2, cws)
         torch.cuda.synchronize()
         assert torch.equal(Yt2, Yt) and torch.equal(dXt2, dXt)
+    if not poison:
+        # the compact weight gradient: dWc[i][j] = dW[S_out(i)][S_in(j)] bit
+        # for bit, through bwd_weight and through the one-call backward
+        gdesc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped,
+                            api.ARD_WEIGHTS_COMPACT_GRAD)
+        Sin, Sout = opat.row_kept_list(K, *pin), opat.row_kept_list(N, *pout)
+        ldc = api.ard_fc_compact_ld(gdesc)
+        Wc = torch.empty(max(api.ard_fc_compact_bytes(gdesc), 16) // 2, dtype=torch.int16, device=device())
+        api.ard_fc_compact_weights(gdesc, Wd, Wc)
+        gws = workspace(api.ard_fc_workspace_bytes(gdesc))
+        nc = len(Sout) * ldc
+        dWc_buf = torch.full((max(nc, 4),), 7.0, device=device())  # never a null pointer
+        dWc2_buf, db3, dXt3 = dWc_buf.clone(), torch.full_like(db, fill), torch.full_like(dXt, fill)
+        db4 = torch.full_like(db, fill)
+        api.ard_fc_bwd_weight(gdesc, Xt, dYt, Yst, dWc_buf, db3, gws)
+        api.ard_fc_bwd(gdesc, Xt, dYt, Yst, Wc, dXt3, dWc2_buf, db4, gws)
+        torch.cuda.synchronize()
+        dWc, dWc2 = dWc_buf[:nc].view(len(Sout), ldc), dWc2_buf[:nc].view(len(Sout), ldc)
+        want_c = dW[torch.tensor(Sout, dtype=torch.long, device=device())][:, torch.tensor(Sin, dtype=torch.long,
+                                                                                              device=device())]
+        assert torch.equal(dWc[:, :len(Sin)], want_c) and torch.equal(dWc2_buf, dWc_buf)
+        assert (dWc[:, len(Sin):] == 7.0).all(), "padding columns were written"
+        assert torch.equal(db3, db) and torch.equal(db4, db) and torch.equal(dXt3, dXt)
 
     Xa, Wa = np.abs(f64(X) * m_in[None, :]), np.abs(f64(W))
     G = ofc.fc_output_grad(f64(Ys), f64(dY), m_out, scale, act)
@@ -464,3 +487,32 @@ def test_sgd_momentum_against_oracle(dtype, pin, pout):
         Wo = np.where(keep, f64(Wd), Wo)
     with pytest.raises(api.ArdError):
         api.ard_fc_sgd_momentum(desc, Wd, Vd, to_dev(dW), bd, None, to_dev(db), lr, mu)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("pin,pout", [((1, 0), (1, 0)), ((3, 1), (2, 0)), ((5, 4), (1, 0)), ((2, 0), (7, 6))])
+def test_sgd_momentum_compact_gradient(dtype, pin, pout):
+    """The update fed the compact gradient dWc[kept_out][ldc] (layout
+    ARD_WEIGHTS_COMPACT_GRAD) equals, bit for bit, the update fed the same
+    values in the full layout."""
+    d = device()
+    N, K, lr, mu = 130, 260, 0.01, 0.9
+    g = synth.generator(78)
+    W = synth.to_storage(synth.normal(g, (N, K)), dtype)
+    V, b, Vb = synth.normal(g, (N, K), 0.1), synth.normal(g, (N,)), synth.normal(g, (N,), 0.1)
+    dW, db = synth.normal(g, (N, K)), synth.normal(g, (N,))
+    args = (ard_dtype(dtype), 8, K, N, row_plan(K, *pin, with_list=False), row_plan(N, *pout, with_list=False), 1.0,
+            api.ARD_ACT_NONE, api.ARD_DROPPED_SKIP)
+    full, comp = api.fc_desc(*args), api.fc_desc(*args, api.ARD_WEIGHTS_COMPACT_GRAD)
+    Sin, Sout = opat.row_kept_list(K, *pin), opat.row_kept_list(N, *pout)
+    ldc = api.ard_fc_compact_ld(comp)
+    dWc = torch.full((len(Sout), ldc), float("nan"))
+    dWc[:, :len(Sin)] = dW[Sout][:, Sin]
+    outs = []
+    for desc, grad in ((full, dW), (comp, dWc)):
+        Wd, Vd, bd, Vbd = to_dev(W), to_dev(V), to_dev(b), to_dev(Vb)
+        api.ard_fc_sgd_momentum(desc, Wd, Vd, to_dev(grad), bd, Vbd, to_dev(db), lr, mu)
+        outs.append((Wd, Vd, bd, Vbd))
+    torch.cuda.synchronize()
+    for a, c in zip(*outs):
+        assert torch.equal(a, c)
