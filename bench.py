@@ -41,7 +41,7 @@ class Mlp:
     """An MLP whose hidden layers take row-based dropout patterns sampled per
     step from K(p). Layers are FC: Xt[K][B] -> Yt[N][B]."""
 
-    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False, dropped="skip"):
+    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False, dropped="skip", streams=1):
         import torch
         from paper_1805_08939_amd import api, synth
         self.api, self.torch = api, torch
@@ -70,9 +70,18 @@ class Mlp:
         self.Wc = [None] + [torch.zeros(dims[l + 1] * ((dims[l] + 7) // 8 * 8), dtype=sdt, device=dev)
                             for l in range(1, L)]
         self.ws = torch.empty(2 * 256 * 256 * 256, dtype=torch.float32, device=dev)
+        # streams == 2: the step runs the compaction and the weight-gradient
+        # products of the hidden layers on a second stream (same priority),
+        # with its own split-K workspace, beside the chain fwd -> bwd_data
+        self.streams = streams
+        if streams == 2:
+            self.side = torch.cuda.Stream(device=dev)
+            self.ws_side = torch.empty_like(self.ws)
+            self.ev = [torch.cuda.Event() for _ in range(5)]
         self.K = None
         self.config = {"workload": name, "global_batch": batch, "layers": dims,
-                       "patterns": "row-based, sampled per step from K(p), n_max 16", "dropped": dropped}
+                       "patterns": "row-based, sampled per step from K(p), n_max 16", "dropped": dropped,
+                       "streams": streams}
         self.dropped = api.ARD_DROPPED_ZERO if dropped == "zero" else api.ARD_DROPPED_SKIP
         # raw device addresses and the stream handle, resolved once: the step
         # then costs one C call per launch with no per-call tensor lookups
@@ -125,6 +134,26 @@ class Mlp:
 
         self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l > 0 else None}
                             for l in range(self.L)]
+
+        def split_calls(l, compact):
+            """The layer's products as separate calls: fwd and bwd_data on the
+            step stream, bwd_weight of a hidden layer on the second stream."""
+            desc = self.cdescs[l] if compact else self.descs[l]
+            w = P["Wc"][l] if compact else P["W"][l]
+            calls = {("fwd", l): (api.ard_fc_fwd, (desc, acts[l], w, P["bias"][l], P["Y"][l], ws, st), {})}
+            if l > 0:
+                calls[("bwd_data", l)] = (api.ard_fc_bwd_data, (desc, P["dY"][l], None, w, P["dY"][l - 1], ws, st),
+                                          {"Xgate": acts[l]})
+                side = (self.ws_side.data_ptr(), self.ws_side.numel() * 4), self.side.cuda_stream
+            else:
+                side = ws, st
+            calls[("bwd_weight", l)] = (api.ard_fc_bwd_weight, (desc, acts[l], P["dY"][l], None, P["dW"][l],
+                                                                P["db"][l]) + side, {})
+            return calls
+
+        if self.streams == 2:
+            self.split_calls = [{False: split_calls(l, False), True: split_calls(l, True) if l > 0 else None}
+                                for l in range(self.L)]
         # one compaction launch per step for the layers whose inputs are
         # dropped: the marshalled arguments of every subset, built once
         import itertools
@@ -232,11 +261,61 @@ class Mlp:
             calls.update(self.layer_calls[l][l in sub])
         return pats, calls
 
+    def step_overlapped(self, it):
+        """One step on two streams. The step stream runs the dependent chain
+        fwd 0 .. L-1, bwd_data L-1 .. 1, bwd_weight 0; the second stream runs
+        the compaction (joined before the first layer that reads compact
+        weights) and the weight-gradient products of the layers above the
+        first (each after the step stream has produced its operands), and is
+        joined at the end of the step, so the next step (or anything after
+        it on the step stream) sees every result."""
+        api, P, st = self.api, self.ptr, self.stream
+        torch = self.torch
+        main, side, ev = torch.cuda.current_stream(), self.side, self.ev
+        pats = self.patterns(it)
+        for l, (per, off) in enumerate(pats):
+            api.ard_plan_rows(self.dims[l + 1], per, off, None, st, plan=self.plans[l])
+        sub = tuple(l for l in range(1, self.L) if pats[l - 1][0] > 1)
+        self.step_compact = sub
+        calls = [self.split_calls[l][l in sub] for l in range(self.L)]
+
+        def run(key):
+            fn, args, kw = calls[key[1]][key]
+            fn(*args, **kw)
+
+        if sub:
+            ev[0].record(main)
+            side.wait_event(ev[0])  # the previous step's readers of the compact weights are done
+            api.ard_fc_compact_weights_batch(self.compact_batches[sub], side.cuda_stream)
+            ev[1].record(side)
+        for l in range(self.L):
+            if l == 1 and sub:
+                main.wait_event(ev[1])
+            run(("fwd", l))
+            if l == self.L - 2:  # the input of the top layer is ready: its weight gradient can start
+                ev[2].record(main)
+        side.wait_event(ev[2])
+        run(("bwd_weight", self.L - 1))
+        for l in reversed(range(1, self.L)):
+            run(("bwd_data", l))
+            if l > 1:
+                ev[3].record(main)
+                side.wait_event(ev[3])
+                run(("bwd_weight", l - 1))
+        run(("bwd_weight", 0))
+        ev[4].record(side)
+        main.wait_event(ev[4])
+        return pats, []
+
     def step(self, it, events=None):
         """One step of iteration it. With events (a list of (start, end) event
         pairs, consumed from the front), every call is bracketed by a pair
-        recorded on the current stream; returns the patterns and the list of
-        (call key, start, end) used."""
+        recorded on the current stream, and the calls run one after the other
+        on the step stream; returns the patterns and the list of (call key,
+        start, end) used. Without events, a two-stream workload runs the
+        overlapped schedule."""
+        if events is None and getattr(self, "streams", 1) == 2:
+            return self.step_overlapped(it)
         pats, calls = self.prepare(it)
         used = []
         for key in self.order:
@@ -763,7 +842,7 @@ WORKLOADS = {
     "lstm1024tile": dict(cls="LstmTile", name="lstm-t35-b64-i1024-h1024-fp32-tile64", T=35, batch=64, inputs=1024,
                          hidden=1024, tile=64, dtype="f32", seed=1805 + 3),
     "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
-                    dtype="bf16", init="he", seed=1805 + 4),
+                    dtype="bf16", init="he", seed=1805 + 4, streams=2),
 }
 
 
