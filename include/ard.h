@@ -312,6 +312,22 @@ int ard_fc_fwd(const ard_fc_desc* desc, const void* Xt, const void* W, const flo
  */
 int ard_fc_bwd_data(const ard_fc_desc* desc, const void* dYt, const void* Yt, const void* W,
                     void* dXt, const void* Xgate, void* ws, size_t ws_bytes, void* stream);
+/*
+ * ard_fc_fwd for callers that cannot allocate device memory or pass a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. The same computation, kernels and results, bit for bit,
+ * as ard_fc_fwd with a workspace; the scratch the layer needs (the compact
+ * weight copy of a gathered input side, split-contraction partial sums) comes
+ * from a static device array of the library instead: 32 MiB per GPU, kept
+ * from the first such call on that GPU until the process ends. A layer whose
+ * ard_fc_workspace_bytes exceeds 32 MiB is rejected with ARD_ERR_WORKSPACE
+ * before any launch. Nothing in the scratch needs to start at zero (a call
+ * reads only what it wrote), but every call on one GPU shares that GPU's
+ * array: calls that overlap in time on one GPU (other streams, other threads)
+ * race and must be serialised by the caller. No call allocates or frees.
+ */
+int ard_fc_fwd_noalloc(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias,
+                       void* Yt, void* stream);
 /* dbias may be NULL. */
 int ard_fc_bwd_weight(const ard_fc_desc* desc, const void* Xt, const void* dYt, const void* Yt,
                       float* dW, float* dbias, void* ws, size_t ws_bytes, void* stream);

@@ -95,6 +95,7 @@ SIGNATURES = {
                                                     ctypes.POINTER(c_vp), ctypes.POINTER(c_vp), c_vp]),
     "ard_fc_workspace_bytes": (c_size, [ctypes.POINTER(ard_fc_desc)]),
     "ard_fc_fwd": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "ard_fc_fwd_noalloc": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp]),
     "ard_fc_bwd_data": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                        c_size, c_vp]),
     "ard_fc_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_fc_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,

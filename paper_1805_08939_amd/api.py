@@ -223,6 +223,12 @@ def ard_fc_fwd(desc, Xt, W, bias, Yt, ws=None, stream=None):
                                  _stream(stream)))
 
 
+def ard_fc_fwd_noalloc(desc, Xt, W, bias, Yt, stream=None):
+    """ard_fc_fwd with the library's static per-GPU scratch instead of a workspace."""
+    _check(_ffi.lib().ard_fc_fwd_noalloc(ctypes.byref(desc), _ptr(Xt), _ptr(W), _ptr(bias), _ptr(Yt),
+                                         _stream(stream)))
+
+
 def ard_fc_bwd_data(desc, dYt, Yt, W, dXt, ws=None, stream=None, Xgate=None):
     p, n = _ws(ws)
     _check(_ffi.lib().ard_fc_bwd_data(ctypes.byref(desc), _ptr(dYt), _ptr(Yt), _ptr(W), _ptr(dXt),

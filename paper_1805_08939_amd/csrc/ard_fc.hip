@@ -8,6 +8,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "ard_gemm.hpp"
 #include "ard_gemm_fast.hpp"
 #include "ard_internal.hpp"
@@ -574,9 +576,63 @@ int fc_bwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
 }  // namespace
 }  // namespace ard
 
+// The scratch of ard_fc_fwd_noalloc: a file-scope device array, one copy per
+// GPU the library runs on, held until the process ends. Its host-side name is
+// only a stand-in for the symbol: host code uses the per-device address that
+// hipGetSymbolAddress returns, never the name.
+constexpr size_t kNoAllocScratchBytes = size_t{32} << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace ard {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of scratch, looked up on the first call on that
+// device (with it current) and kept.
+int device_scratch(void** out) {
+  int dev = -1;
+  ARD_HIP_CHECK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ARD_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    ARD_HIP_CHECK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ARD_OK;
+}
+
+}  // namespace
+}  // namespace ard
+
 using namespace ard;
 
 extern "C" {
+
+int ard_fc_fwd_noalloc(const ard_fc_desc* desc, const void* Xt, const void* W, const float* bias, void* Yt,
+                       void* stream) {
+  clear_error();
+  FcShape s;
+  int st = check_desc(desc, &s);
+  if (st != ARD_OK) return st;
+  if ((st = check_ptr(Xt, "Xt")) || (st = check_ptr(W, "W")) || (st = check_ptr(Yt, "Yt")))
+    return st;
+  if (bias && !aligned16(bias)) return fail(ARD_ERR_INVALID_ARG, "bias is not 16-byte aligned");
+  const size_t need = workspace_bytes(s, desc->dtype);
+  if (need > kNoAllocScratchBytes)
+    return fail(ARD_ERR_WORKSPACE,
+                "the layer needs %zu bytes of scratch, the static scratch holds %zu (use ard_fc_fwd with a workspace)",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0 && (st = device_scratch(&ws)) != ARD_OK) return st;
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (desc->dtype == ARD_BF16) return fc_fwd_impl<bf16>(desc, s, Xt, W, bias, Yt, ws, sm);
+  return fc_fwd_impl<float>(desc, s, Xt, W, bias, Yt, ws, sm);
+}
 
 int ard_plan_rows(int32_t n, int32_t period, int32_t offset, int32_t* d_idx, ard_row_plan* plan,
                   void* stream) {
