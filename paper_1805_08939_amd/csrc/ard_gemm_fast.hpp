@@ -407,21 +407,27 @@ struct SlabLoader {
 };
 
 // Tile order. Workgroup i runs on XCD i % 8, each XCD with its own L2, so
-// XCD x takes a contiguous run of positions t in a grouped order: kGroupRows
-// tile rows at a time, column by column within the group. The workgroups
-// running together on one XCD then share a few A row panels and a few B
-// column panels instead of each bringing its own. Returns the tile row and
-// column of workgroup bid in a grid of nx columns and ny rows.
-__device__ __forceinline__ void grouped_tile(int bid, int nx, int ny, int& row, int& col) {
-  const int nxy = nx * ny;
-  const int xcd = bid % 8, per = nxy / 8, extra = nxy % 8;
-  const int t = xcd * per + (xcd < extra ? xcd : extra) + bid / 8;
+// XCD x takes a contiguous run of positions t (xcd_position) in a grouped
+// order: kGroupRows tile rows at a time, column by column within the group.
+// The workgroups running together on one XCD then share a few A row panels
+// and a few B column panels instead of each bringing its own. grouped_tile
+// returns the tile row and column of workgroup bid in a grid of nx columns and
+// ny rows.
+__device__ __forceinline__ int xcd_position(int bid, int total) {
+  const int xcd = bid % 8, per = total / 8, extra = total % 8;
+  return xcd * per + (xcd < extra ? xcd : extra) + bid / 8;
+}
+// Tile row and column of position t of an nx x ny grid in the grouped order.
+__device__ __forceinline__ void grouped_order(int t, int nx, int ny, int& row, int& col) {
   constexpr int kGroupRows = 8;
   const int first_row = (t / (kGroupRows * nx)) * kGroupRows;
   const int rows = ny - first_row < kGroupRows ? ny - first_row : kGroupRows;
   const int local = t % (kGroupRows * nx);
   col = local / rows;
   row = first_row + local % rows;
+}
+__device__ __forceinline__ void grouped_tile(int bid, int nx, int ny, int& row, int& col) {
+  grouped_order(xcd_position(bid, nx * ny), nx, ny, row, col);
 }
 
 // The slab pipeline of one workgroup: nslab slabs that the loader issues one
@@ -611,10 +617,8 @@ __device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg:
 // One workgroup's output tile: position bid of an nx x ny tile grid in the
 // grouped order, batch-and-split index bzs.
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
-__device__ __forceinline__ void fast_gemm_tile(const GemmArgs& g, int bid, int nx, int ny, int bzs, char* smem) {
+__device__ __forceinline__ void fast_gemm_tile(const GemmArgs& g, int tile_row, int tile_col, int bzs, char* smem) {
   using T = typename Cfg::T;
-  int tile_row, tile_col;
-  grouped_tile(bid, nx, ny, tile_row, tile_col);
   const int n0 = tile_col * Cfg::BN;
   const int m0 = tile_row * Cfg::BM;
   const int splits = g.splits > 1 ? g.splits : 1;
@@ -748,11 +752,21 @@ __device__ __forceinline__ void fast_gemm_tile(const GemmArgs& g, int bid, int n
   }
 }
 
+// The grid is nx x ny output tiles times nz (batch entries times k splits).
+// XCD positions run over the whole grid, z-major: a z-slice (one batch entry
+// and k range) goes to as few XCDs as possible, so that with a split
+// contraction the workgroups on one XCD share the A and B panels of one k
+// range (split z on XCD z when the tiles of a slice are a multiple of 8)
+// instead of each XCD holding a few tiles of every k range.
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  fast_gemm_tile<Cfg, AMC, BMC, OutT, EPI, RSUM>(g, blockIdx.y * gridDim.x + blockIdx.x, gridDim.x, gridDim.y,
-                                                 blockIdx.z, smem);
+  const int nx = gridDim.x, ny = gridDim.y, nxy = nx * ny;
+  const int bid = (blockIdx.z * ny + blockIdx.y) * nx + blockIdx.x;
+  const int t = xcd_position(bid, nxy * gridDim.z);
+  int tile_row, tile_col;
+  grouped_order(t % nxy, nx, ny, tile_row, tile_col);
+  fast_gemm_tile<Cfg, AMC, BMC, OutT, EPI, RSUM>(g, tile_row, tile_col, t / nxy, smem);
 }
 
 // Two independent GEMMs of one configuration in one launch (no batch, no k
@@ -765,11 +779,14 @@ __global__ void __launch_bounds__(Cfg::NT) fast_gemm_pair_kernel(GemmArgs g1, Ge
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int nx1 = (g1.N + Cfg::BN - 1) / Cfg::BN, ny1 = (g1.M + Cfg::BM - 1) / Cfg::BM;
   const int b = static_cast<int>(blockIdx.x);
+  int row, col;
   if (b < nx1 * ny1) {
-    fast_gemm_tile<Cfg, AMC1, BMC1, OutT1, EPI1, RSUM1>(g1, b, nx1, ny1, 0, smem);
+    grouped_tile(b, nx1, ny1, row, col);
+    fast_gemm_tile<Cfg, AMC1, BMC1, OutT1, EPI1, RSUM1>(g1, row, col, 0, smem);
   } else {
     const int nx2 = (g2.N + Cfg::BN - 1) / Cfg::BN, ny2 = (g2.M + Cfg::BM - 1) / Cfg::BM;
-    fast_gemm_tile<Cfg, AMC2, BMC2, OutT2, EPI2, RSUM2>(g2, b - nx1 * ny1, nx2, ny2, 0, smem);
+    grouped_tile(b - nx1 * ny1, nx2, ny2, row, col);
+    fast_gemm_tile<Cfg, AMC2, BMC2, OutT2, EPI2, RSUM2>(g2, row, col, 0, smem);
   }
 }
 
