@@ -242,6 +242,21 @@ class Mlp:
                 per[("bwd_weight", l)] = f
         return sum(per.values()), per
 
+    def kept_bytes(self, pats):
+        """Per-call algorithmic HBM bytes: the kept operands read once and the
+        kept outputs written once (weights and activations in the storage
+        dtype, weight and bias gradients fp32); bwd_data also reads the ReLU
+        gate of the layer below."""
+        n, B = self.kept(pats), self.B
+        es = 2 if self.dtype == "bf16" else 4
+        per = {}
+        for l in range(self.L):
+            w, x, y = n[l + 1] * n[l] * es, n[l] * B * es, n[l + 1] * B * es
+            per[("fwd", l)] = w + x + y
+            dw = y + x + n[l + 1] * n[l] * 4 + 4 * n[l + 1]
+            per[("bwd", l) if l > 0 else ("bwd_weight", l)] = dw + (w + y + 2 * x if l > 0 else 0)
+        return per
+
     def prepare(self, it):
         """Samples this step's patterns, plans them and gathers the compact
         weights of the layers whose inputs are dropped. Returns the patterns and
@@ -883,17 +898,21 @@ def roofline_pass(wl, steps, warmup, it0):
     end.record()
     torch.cuda.synchronize()
     per = {}
+    nbytes = 0.0
     for pats, used in runs:
         _, fl = wl.kept_flops(pats)
+        by = wl.kept_bytes(pats) if hasattr(wl, "kept_bytes") else {}
         for key, e0, e1 in used:
             rec = per.setdefault(key, [0, 0.0, 0.0])
             rec[0] += 1
             rec[1] += e0.elapsed_time(e1)
             rec[2] += fl[key]
+            nbytes += by.get(key, 0.0)
     calls = sum(r[0] for r in per.values())
     ms = sum(r[1] for r in per.values())
     flops = sum(r[2] for r in per.values())
-    return {"calls": calls, "ms": ms, "flops": flops, "per": per, "pass_ms": start.elapsed_time(end)}
+    return {"calls": calls, "ms": ms, "flops": flops, "per": per, "pass_ms": start.elapsed_time(end),
+            "bytes": nbytes}
 
 
 def time_conventional(wl, steps, warmup, it0):
@@ -1055,6 +1074,65 @@ def summarize_trace(path, top, last=0, tail=0):
         print(f"| {n} | {us:.1f} | {us / n:.2f} | {100 * us / tot:.2f} | {grid[0]}x{grid[1]}x{grid[2]} | `{name}` |")
 
 
+MARKER = "FillFunctor<short>"
+EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel")  # per-step work outside the layer calls
+
+
+def summarize_pass(path, top, calls, kind):
+    """The kernels of bench.py's roofline pass, between the two marker fills,
+    from a rocprofv3 kernel trace (kind "trace": time per kernel) or counter
+    collection (kind "counters": counter sums per kernel), per layer call of
+    the pass (`calls` of them)."""
+    import csv
+    with open(path) as fh:
+        rows = list(csv.DictReader(fh))
+    if kind == "trace":
+        recs = sorted((int(_col(r, "Start_Timestamp")), r) for r in rows)
+        marks = [i for i, (_, r) in enumerate(recs) if MARKER in _col(r, "Kernel_Name")]
+        assert len(marks) >= 2, "marker fills not found"
+        inside = [r for _, r in recs[marks[0] + 1:marks[1]] if not any(x in _col(r, "Kernel_Name") for x in EXCLUDE)]
+        per = {}
+        for r in inside:
+            name = _short_kernel(_col(r, "Kernel_Name"))
+            us = (int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1000.0
+            a = per.setdefault(name, [0, 0.0])
+            a[0] += 1
+            a[1] += us
+        tot = sum(v[1] for v in per.values())
+        print(f"roofline pass: {len(inside)} kernels, {tot:.1f} us of kernel time, {tot / calls:.2f} us per layer "
+              f"call ({calls} calls)")
+        print("| dispatches | total us | avg us | us per layer call | % | kernel |")
+        print("|---:|---:|---:|---:|---:|---|")
+        for name, (n, us) in sorted(per.items(), key=lambda kv: -kv[1][1])[:top]:
+            print(f"| {n} | {us:.1f} | {us / n:.2f} | {us / calls:.2f} | {100 * us / tot:.2f} | `{name}` |")
+        return
+    disp = {}
+    for r in rows:
+        d = int(_col(r, "Dispatch_Id"))
+        e = disp.setdefault(d, {"name": _col(r, "Kernel_Name"), "v": {}})
+        c = _col(r, "Counter_Name")
+        e["v"][c] = e["v"].get(c, 0.0) + float(_col(r, "Counter_Value"))
+    ids = sorted(disp)
+    marks = [d for d in ids if MARKER in disp[d]["name"]]
+    assert len(marks) >= 2, "marker fills not found"
+    # the step's compaction runs between the calls, outside their event brackets
+    inside = [disp[d] for d in ids if marks[0] < d < marks[1] and not any(x in disp[d]["name"] for x in EXCLUDE)]
+    per, tot = {}, {}
+    for e in inside:
+        name = _short_kernel(e["name"])
+        for c, v in e["v"].items():
+            a = per.setdefault((name, c), [0, 0.0])
+            a[0] += 1
+            a[1] += v
+            tot[c] = tot.get(c, 0.0) + v
+    for c, v in sorted(tot.items()):
+        print(f"roofline pass: {c} sum {v:.1f} over {len(inside)} dispatches, {v / calls:.1f} per layer call")
+    print("| dispatches | sum | per layer call | counter | kernel |")
+    print("|---:|---:|---:|---|---|")
+    for (name, c), (n, v) in sorted(per.items(), key=lambda kv: -kv[1][1])[:top]:
+        print(f"| {n} | {v:.1f} | {v / calls:.1f} | {c} | `{name}` |")
+
+
 def summarize_counters(path, top, last=0, tail=0):
     """Per (kernel, grid size, counter) mean value per dispatch of a rocprofv3
     counter collection (CSV); with last > 0 only each kernel's last
@@ -1106,6 +1184,9 @@ def main():
     ap.add_argument("--last", type=int, default=0, help="--summarize-trace / --summarize-counters: only the last N dispatches per kernel")
     ap.add_argument("--tail", type=int, default=0,
                     help="--summarize-trace / --summarize-counters: only the run's last N dispatches")
+    ap.add_argument("--summarize-pass", metavar="CSV",
+                    help="per-kernel table of the roofline pass from a rocprofv3 trace or counter CSV of this command")
+    ap.add_argument("--pass-kind", default="trace", choices=["trace", "counters"])
     ap.add_argument("--digest", action="store_true", help="print the kernel source digest")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of 1 GiB (3 times), the reference for HBM counters")
@@ -1114,6 +1195,10 @@ def main():
         return summarize_trace(args.summarize_trace, args.top, args.last, args.tail)
     if args.summarize_counters:
         return summarize_counters(args.summarize_counters, args.top, args.last, args.tail)
+    if args.summarize_pass:
+        spec = WORKLOADS[args.workload]
+        per_step = {"Mlp": 2 * (len(spec.get("dims", ())) - 1), "TileLayer": 3, "TileLayerTdp": 3}.get(spec["cls"], 2)
+        return summarize_pass(args.summarize_pass, args.top, args.steps * per_step, args.pass_kind)
     if args.digest:
         return print(source_digest())
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -1167,7 +1252,12 @@ def main():
     # patterns), every layer call bracketed by HIP events on the step stream
     wl.set_rate(args.p)
     head_it0 = 1_000_000 * (rates.index(args.p) + 1)
+    # a one-element int16 fill before and after the pass marks its kernels in a
+    # rocprofv3 trace or counter run of this command (--summarize-pass)
+    marker = torch.empty(1, dtype=torch.int16, device="cuda:0")
+    marker.fill_(1)
     rp = roofline_pass(wl, args.steps, args.warmup, head_it0)
+    marker.fill_(2)
     print(f"# roofline pass p={args.p}: {rp['calls']} layer calls, {rp['ms'] / rp['calls'] * 1e3:.2f} us per call, "
           f"{rp['flops'] / (rp['ms'] * 1e-3) / 1e12:.3f} TFLOP/s over the calls", file=sys.stderr, flush=True)
 
@@ -1223,6 +1313,7 @@ def main():
                     args.p, ", ".join("%s %d" % k for k in wl.order)),
                 "avg_launch_us": rp["ms"] / rp["calls"] * 1e3, "launches": rp["calls"],
                 "flops_per_launch": rp["flops"] / rp["calls"],
+                "algorithmic_bytes_per_launch": rp["bytes"] / rp["calls"] if rp["bytes"] else None,
                 "per_call": {"%s %d" % k: {"calls": r[0], "avg_us": r[1] / r[0] * 1e3,
                                            "tflops": r[2] / (r[1] * 1e-3) / 1e12 if r[1] > 0 else 0.0}
                              for k, r in rp["per"].items()},

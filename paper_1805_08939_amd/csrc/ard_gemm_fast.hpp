@@ -753,20 +753,29 @@ __device__ __forceinline__ void fast_gemm_tile(const GemmArgs& g, int tile_row, 
 }
 
 // The grid is nx x ny output tiles times nz (batch entries times k splits).
-// XCD positions run over the whole grid, z-major: a z-slice (one batch entry
-// and k range) goes to as few XCDs as possible, so that with a split
-// contraction the workgroups on one XCD share the A and B panels of one k
-// range (split z on XCD z when the tiles of a slice are a multiple of 8)
-// instead of each XCD holding a few tiles of every k range.
+// When every z-slice reads its own operands (a split contraction, or a batch
+// with no operand shared between entries), XCD positions run over the whole
+// grid, z-major: a z-slice goes to as few XCDs as possible, so that the
+// workgroups on one XCD share the A and B panels of one slice (split z on
+// XCD z when the tiles of a slice are a multiple of 8) instead of each XCD
+// holding a few tiles of every slice. When an operand is shared by the batch
+// entries (batch stride 0), positions run within each slice: XCD x then holds
+// the same tiles of every entry and the shared panels stay in its L2.
 template <class Cfg, bool AMC, bool BMC, typename OutT, int EPI, bool RSUM = false>
 __global__ void __launch_bounds__(Cfg::NT) fast_gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int nx = gridDim.x, ny = gridDim.y, nxy = nx * ny;
-  const int bid = (blockIdx.z * ny + blockIdx.y) * nx + blockIdx.x;
-  const int t = xcd_position(bid, nxy * gridDim.z);
-  int tile_row, tile_col;
-  grouped_order(t % nxy, nx, ny, tile_row, tile_col);
-  fast_gemm_tile<Cfg, AMC, BMC, OutT, EPI, RSUM>(g, tile_row, tile_col, t / nxy, smem);
+  int tile_row, tile_col, z;
+  if (gridDim.z > 1 && g.splits <= 1 && (g.a.bstride == 0 || g.b.bstride == 0)) {
+    grouped_tile(blockIdx.y * nx + blockIdx.x, nx, ny, tile_row, tile_col);
+    z = blockIdx.z;
+  } else {
+    const int bid = (blockIdx.z * ny + blockIdx.y) * nx + blockIdx.x;
+    const int t = xcd_position(bid, nxy * gridDim.z);
+    grouped_order(t % nxy, nx, ny, tile_row, tile_col);
+    z = t / nxy;
+  }
+  fast_gemm_tile<Cfg, AMC, BMC, OutT, EPI, RSUM>(g, tile_row, tile_col, z, smem);
 }
 
 // Two independent GEMMs of one configuration in one launch (no batch, no k
