@@ -479,9 +479,16 @@ class TileLayer:
         self.dXt = torch.empty(k, batch, dtype=sdt, device=dev)
         self.dW = torch.empty(n, k, dtype=torch.float32, device=dev)
         self.words = (self.tn * self.tk + 31) // 32
-        self.bits_dev = torch.empty(self.words, dtype=torch.int32, device=dev)
-        self.plan_ws = torch.empty(max(api.ard_tile_plan_workspace_bytes(self.tn, self.tk), 16) // 4,
-                                   dtype=torch.int32, device=dev)
+        # two plan buffers: the plan of step i + 1 is built on a second stream
+        # (same priority) while step i's products run (see step_pipelined)
+        self.bits_bufs = [torch.empty(self.words, dtype=torch.int32, device=dev) for _ in range(2)]
+        self.ws_bufs = [torch.empty(max(api.ard_tile_plan_workspace_bytes(self.tn, self.tk), 16) // 4,
+                                    dtype=torch.int32, device=dev) for _ in range(2)]
+        self.bits_dev, self.plan_ws = self.bits_bufs[0], self.ws_bufs[0]
+        self.side = torch.cuda.Stream(device=dev)
+        self.ev_plan = [torch.cuda.Event() for _ in range(2)]
+        self.ev_done = [torch.cuda.Event() for _ in range(2)]
+        self.planned = {}  # buffer -> (step, plan) built into it
         self.desc = api.tile_desc(api.ARD_BF16 if dtype == "bf16" else api.ARD_F32, batch, k, n, 1.0,
                                   api.ARD_DROPPED_SKIP)
         self.stream = torch.cuda.current_stream().cuda_stream
@@ -491,10 +498,43 @@ class TileLayer:
 
     def set_rate(self, p):
         self.p = p
+        self.planned = {}
 
     def patterns(self, it):
         bits = self.api.ard_tile_bitmap_bernoulli(self.tn, self.tk, self.p, PATTERN_SEED, 0, it)
         return bits, self.api.ard_bitmap_popcount(bits, self.tn * self.tk)
+
+    def plan_into(self, it, buf, stream):
+        """Draws step it's bitmap and plans it on the device, into plan buffer buf."""
+        return self.api.ard_plan_tiles_bernoulli(self.N, self.K, self.tile, self.p, PATTERN_SEED, 0, it,
+                                                 self.bits_bufs[buf], self.ws_bufs[buf], stream)
+
+    def layer_calls(self, plan):
+        api, d, st = self.api, self.desc, self.stream
+        return {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
+                ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
+                ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
+
+    def step_pipelined(self, it):
+        """Step it with the plan built one step ahead: the second stream plans
+        step it + 1 into the other buffer (once step it - 1, its last reader,
+        is done) while the step stream runs step it's products on the plan
+        built during step it - 1 (or now, at the start of a run of steps)."""
+        torch = self.torch
+        main, side = torch.cuda.current_stream(), self.side
+        b, nb = it % 2, (it + 1) % 2
+        if self.planned.get(b, (None,))[0] != it:  # first step of a run: plan it now
+            side.wait_stream(main)
+            self.planned[b] = (it, self.plan_into(it, b, side.cuda_stream))
+            self.ev_plan[b].record(side)
+        side.wait_event(self.ev_done[nb])
+        self.planned[nb] = (it + 1, self.plan_into(it + 1, nb, side.cuda_stream))
+        self.ev_plan[nb].record(side)
+        main.wait_event(self.ev_plan[b])
+        for fn, args, kw in (self.layer_calls(self.planned[b][1])[k] for k in self.order):
+            fn(*args, **kw)
+        self.ev_done[b].record(main)
+        return it, []
 
     def kept_flops(self, pats):
         if isinstance(pats, int):  # a step number: its pattern from the host sampler
@@ -504,16 +544,15 @@ class TileLayer:
         return sum(per.values()), per
 
     def prepare(self, it):
-        api = self.api
-        plan = api.ard_plan_tiles_bernoulli(self.N, self.K, self.tile, self.p, PATTERN_SEED, 0, it, self.bits_dev,
-                                            self.plan_ws, self.stream)
-        d, st = self.desc, self.stream
-        calls = {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
-                 ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
-                 ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
-        return it, calls
+        self.planned = {}
+        return it, self.layer_calls(self.plan_into(it, 0, self.stream))
 
-    step = Mlp.step
+    def step(self, it, events=None):
+        """Without events the pipelined step; with events (the roofline pass)
+        the plan and the products one after the other on the step stream."""
+        if events is None:
+            return self.step_pipelined(it)
+        return Mlp.step(self, it, events)
 
     def oracle_step(self, pats):
         import numpy as np
@@ -544,6 +583,7 @@ class TileLayerTdp(TileLayer):
     def set_rate(self, p):
         api, torch = self.api, self.torch
         self.p = p
+        self.planned = {}
         self.Kdist, _ = api.ard_search_distribution(p)
         for per in range(1, len(self.Kdist) + 1):
             for off in range(per):
@@ -557,16 +597,11 @@ class TileLayerTdp(TileLayer):
         _, nnz, bits = self.tdp_bits[(per, off)]
         return bits, nnz, (per, off)
 
-    def prepare(self, it):
-        api = self.api
-        _, nnz, _ = pats = self.patterns(it)
-        dbits = self.tdp_bits[pats[2]][0]
-        plan = api.ard_plan_tiles(self.N, self.K, self.tile, dbits, nnz, self.plan_ws, self.stream)
-        d, st = self.desc, self.stream
-        calls = {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
-                 ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
-                 ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
-        return it, calls
+    def plan_into(self, it, buf, stream):
+        """Plans step it's (dp, offset) bitmap (resident on the device) into plan buffer buf."""
+        _, nnz, pat = self.patterns(it)
+        return self.api.ard_plan_tiles(self.N, self.K, self.tile, self.tdp_bits[pat][0], nnz, self.ws_bufs[buf],
+                                       stream)
 
 
 class Lstm:
@@ -1175,6 +1210,8 @@ def main():
     ap.add_argument("--dropped", default="skip", choices=["skip", "zero"],
                     help="MLP workloads: dropped outputs and gradients left untouched (skip) or written 0 (zero)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--streams", type=int, choices=[1, 2], default=None,
+                    help="MLP workloads: one stream, or two (compaction and weight gradients beside the chain)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baselines", action="store_true",
                     help="skip the conventional-dropout and training-step comparisons")
@@ -1225,6 +1262,10 @@ def main():
         if cls is not Mlp:
             sys.exit("--dropped zero applies to the MLP workloads")
         spec["dropped"] = args.dropped
+    if args.streams is not None:
+        if cls is not Mlp:
+            sys.exit("--streams applies to the MLP workloads")
+        spec["streams"] = args.streams
     wl = cls(**spec)
     dtype = spec["dtype"]
     if not args.no_cpu_baseline:

@@ -149,15 +149,18 @@ def test_tile_layer_full_size():
     tl = bench.TileLayer(**spec)
     tl.host_copies()
     X, W, dY = tl._host
-    for p, it in ((0.5, 3), (0.7, 4)):
-        tl.set_rate(p)
+    # steps 3 and 4 in a row: step 4 runs on the plan built during step 3
+    for p, it in ((0.5, 3), (0.5, 4), (0.7, 9)):
+        if p != getattr(tl, "p", None):
+            tl.set_rate(p)
         nan = float("nan")
         for t in (tl.Yt, tl.dXt, tl.dW):
             t.fill_(nan)
         tl.step(it)
         torch.cuda.synchronize()
         words = oprng.tile_bitmap_bernoulli(tl.tn, tl.tk, p, 8939, 0, it)
-        assert [int(w) for w in tl.bits_dev.cpu().numpy().view(np.uint32)] == [int(w) for w in words]
+        bits = tl.bits_bufs[it % 2]  # the step's plan buffer
+        assert [int(w) for w in bits.cpu().numpy().view(np.uint32)] == [int(w) for w in words]
         M = opat.tile_mask(words, tl.tn, tl.tk, tl.tile)
         Y64 = otdp.tdp_forward(X, W, M)
         dX64, dW64 = otdp.tdp_backward(X, W, dY, M)
