@@ -429,6 +429,13 @@ class FcLayer:
         per = {("fwd", 0): f, ("bwd", 0): 2.0 * f}
         return 3.0 * f, per
 
+    def kept_bytes(self, pats):
+        """Algorithmic HBM bytes per call (see Mlp.kept_bytes)."""
+        es = 2 if self.dtype == "bf16" else 4
+        n = self.api.ard_row_kept(self.N, *pats[0])
+        w, x, y = n * self.K * es, self.K * self.B * es, n * self.B * es
+        return {("fwd", 0): w + x + y, ("bwd", 0): (w + y + x) + (y + x + 4 * n * self.K + 4 * n)}
+
     def prepare(self, it):
         api, st = self.api, self.stream
         pats = self.patterns(it)
@@ -542,6 +549,16 @@ class TileLayer:
         f = 2.0 * self.B * self.tile * self.tile * pats[1]
         per = {key: f for key in self.order}
         return sum(per.values()), per
+
+    def kept_bytes(self, pats):
+        """Algorithmic HBM bytes per call: the kept tiles of W (read) or dW
+        (fp32, written), the activations and outputs of every row once."""
+        if isinstance(pats, int):
+            pats = self.patterns(pats)
+        es = 2 if self.dtype == "bf16" else 4
+        wt = pats[1] * self.tile * self.tile
+        x, y = self.K * self.B * es, self.N * self.B * es
+        return {("fwd", 0): wt * es + x + y, ("bwd_data", 0): wt * es + y + x, ("bwd_weight", 0): y + x + 4 * wt}
 
     def prepare(self, it):
         self.planned = {}
@@ -920,17 +937,22 @@ def roofline_pass(wl, steps, warmup, it0):
     """The same steps once more with every layer call bracketed by a HIP event
     pair on the step stream. Returns, per call key and in total, the number of
     calls, the summed event time and the summed kept FLOPs, plus the whole
-    pass's GPU time."""
+    pass's GPU time. A one-element int16 fill before and after the timed steps
+    marks their kernels in a rocprofv3 trace or counter run of this command
+    (--summarize-pass)."""
     import torch
     for i in range(warmup):
         wl.step(it0 + i)
     torch.cuda.synchronize()
+    marker = torch.empty(1, dtype=torch.int16, device="cuda:0")
+    marker.fill_(1)
     n = steps * len(wl.order)
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     runs = [wl.step(it0 + warmup + i, events) for i in range(steps)]
     end.record()
+    marker.fill_(2)
     torch.cuda.synchronize()
     per = {}
     nbytes = 0.0
@@ -1110,7 +1132,7 @@ def summarize_trace(path, top, last=0, tail=0):
 
 
 MARKER = "FillFunctor<short>"
-EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel")  # per-step work outside the layer calls
+EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel", "plan_rows_kernel")  # per-step work outside the layer calls
 
 
 def summarize_pass(path, top, calls, kind):
@@ -1293,12 +1315,7 @@ def main():
     # patterns), every layer call bracketed by HIP events on the step stream
     wl.set_rate(args.p)
     head_it0 = 1_000_000 * (rates.index(args.p) + 1)
-    # a one-element int16 fill before and after the pass marks its kernels in a
-    # rocprofv3 trace or counter run of this command (--summarize-pass)
-    marker = torch.empty(1, dtype=torch.int16, device="cuda:0")
-    marker.fill_(1)
     rp = roofline_pass(wl, args.steps, args.warmup, head_it0)
-    marker.fill_(2)
     print(f"# roofline pass p={args.p}: {rp['calls']} layer calls, {rp['ms'] / rp['calls'] * 1e3:.2f} us per call, "
           f"{rp['flops'] / (rp['ms'] * 1e-3) / 1e12:.3f} TFLOP/s over the calls", file=sys.stderr, flush=True)
 

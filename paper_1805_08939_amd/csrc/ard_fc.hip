@@ -153,8 +153,20 @@ __device__ __forceinline__ void compact_row(const CompactJob<T>& jb, int64_t i, 
       const int64_t n = K - s0 < SEG ? K - s0 : SEG;  // columns of this segment
       __syncthreads();  // the previous segment is no longer read
       if (jb.vec) {
-        for (int64_t c = t * EPC; c < n; c += 256 * EPC)
-          *reinterpret_cast<u32x4*>(seg + c) = *reinterpret_cast<const u32x4*>(row + s0 + c);
+        // every load of the segment in flight before the first LDS store (a
+        // loop of load-then-store waits out one memory latency per chunk)
+        constexpr int PER = SEG / EPC / 256;  // 16-byte chunks per thread per segment
+        u32x4 v[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const int64_t c = static_cast<int64_t>(t + u * 256) * EPC;
+          if (c < n) v[u] = *reinterpret_cast<const u32x4*>(row + s0 + c);
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const int64_t c = static_cast<int64_t>(t + u * 256) * EPC;
+          if (c < n) *reinterpret_cast<u32x4*>(seg + c) = v[u];
+        }
       } else {
         for (int64_t c = t; c < n; c += 256) seg[c] = row[s0 + c];
       }
