@@ -913,10 +913,31 @@ WORKLOADS = {
 }
 
 
+class NoGC:
+    """Python's cyclic garbage collector off for a timed region: a collection
+    pass stalls the host (and so a host-fed GPU queue) for milliseconds."""
+
+    def __enter__(self):
+        import gc
+        self.was = gc.isenabled()
+        gc.collect()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        import gc
+        if self.was:
+            gc.enable()
+
+
 def time_steps(wl, steps, warmup, it0):
     """GPU time of `steps` steps after `warmup` untimed ones: one HIP event
     pair on the step stream around the whole run; FLOPs counted afterwards
     from the host sampler's patterns."""
+    with NoGC():
+        return _time_steps(wl, steps, warmup, it0)
+
+
+def _time_steps(wl, steps, warmup, it0):
     import torch
     for i in range(warmup):
         wl.step(it0 + i)
@@ -934,6 +955,11 @@ def time_steps(wl, steps, warmup, it0):
 
 
 def roofline_pass(wl, steps, warmup, it0):
+    with NoGC():
+        return _roofline_pass(wl, steps, warmup, it0)
+
+
+def _roofline_pass(wl, steps, warmup, it0):
     """The same steps once more with every layer call bracketed by a HIP event
     pair on the step stream. Returns, per call key and in total, the number of
     calls, the summed event time and the summed kept FLOPs, plus the whole
@@ -944,14 +970,18 @@ def roofline_pass(wl, steps, warmup, it0):
     for i in range(warmup):
         wl.step(it0 + i)
     torch.cuda.synchronize()
+    lead = spin_cycles(LEAD_MS)
     marker = torch.empty(1, dtype=torch.int16, device="cuda:0")
     marker.fill_(1)
     n = steps * len(wl.order)
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    runs = [wl.step(it0 + warmup + i, events) for i in range(steps)]
-    end.record()
+    runs = []
+    for i in range(steps):
+        # a bounded spin ahead of each step keeps the GPU busy while the host
+        # enqueues the step, so an event pair brackets the call's kernels and
+        # not the host's launch latency
+        torch.cuda._sleep(lead)
+        runs.append(wl.step(it0 + warmup + i, events))
     marker.fill_(2)
     torch.cuda.synchronize()
     per = {}
@@ -968,13 +998,39 @@ def roofline_pass(wl, steps, warmup, it0):
     calls = sum(r[0] for r in per.values())
     ms = sum(r[1] for r in per.values())
     flops = sum(r[2] for r in per.values())
-    return {"calls": calls, "ms": ms, "flops": flops, "per": per, "pass_ms": start.elapsed_time(end),
-            "bytes": nbytes}
+    return {"calls": calls, "ms": ms, "flops": flops, "per": per, "bytes": nbytes}
+
+
+LEAD_MS = 2.0  # GPU spin ahead of each step of the roofline pass
+
+
+def spin_cycles(ms):
+    """Cycles of torch's spin kernel that take about ms milliseconds on this
+    GPU (measured once with a HIP event pair)."""
+    import torch
+    global _SPIN_PER_MS
+    if _SPIN_PER_MS is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)
+        e0.record()
+        torch.cuda._sleep(1_000_000)
+        e1.record()
+        torch.cuda.synchronize()
+        _SPIN_PER_MS = 1_000_000 / max(e0.elapsed_time(e1), 1e-3)
+    return int(ms * _SPIN_PER_MS)
+
+
+_SPIN_PER_MS = None
 
 
 def time_conventional(wl, steps, warmup, it0):
     """GPU ms of `steps` conventional-dropout steps after `warmup` untimed ones
     (the same timing as the approximate-dropout steps)."""
+    with NoGC():
+        return _time_conventional(wl, steps, warmup, it0)
+
+
+def _time_conventional(wl, steps, warmup, it0):
     import torch
     for i in range(warmup):
         wl.conventional_step(it0 + i)
@@ -991,6 +1047,11 @@ def time_conventional(wl, steps, warmup, it0):
 def time_training(wl, steps, warmup, it0, conventional):
     """GPU ms of `steps` training steps (a step of the path, or of the
     conventional network, followed by the momentum-SGD update of every layer)."""
+    with NoGC():
+        return _time_training(wl, steps, warmup, it0, conventional)
+
+
+def _time_training(wl, steps, warmup, it0, conventional):
     import torch
 
     def one(it):
@@ -1108,7 +1169,7 @@ def summarize_trace(path, top, last=0, tail=0):
     last tail dispatches (a replayed call)."""
     import csv
     with open(path) as fh:
-        recs = sorted((int(_col(r, "Start_Timestamp")), r) for r in csv.DictReader(fh))
+        recs = sorted(((int(_col(r, "Start_Timestamp")), r) for r in csv.DictReader(fh)), key=lambda t: t[0])
     if tail > 0:
         recs = recs[-tail:]
     agg = {}
@@ -1132,7 +1193,8 @@ def summarize_trace(path, top, last=0, tail=0):
 
 
 MARKER = "FillFunctor<short>"
-EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel", "plan_rows_kernel")  # per-step work outside the layer calls
+# per-step work outside the layer calls, and the pass's spin kernel
+EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel", "plan_rows_kernel", "spin_kernel")
 
 
 def summarize_pass(path, top, calls, kind):
@@ -1144,7 +1206,7 @@ def summarize_pass(path, top, calls, kind):
     with open(path) as fh:
         rows = list(csv.DictReader(fh))
     if kind == "trace":
-        recs = sorted((int(_col(r, "Start_Timestamp")), r) for r in rows)
+        recs = sorted(((int(_col(r, "Start_Timestamp")), r) for r in rows), key=lambda t: t[0])
         marks = [i for i, (_, r) in enumerate(recs) if MARKER in _col(r, "Kernel_Name")]
         assert len(marks) >= 2, "marker fills not found"
         inside = [r for _, r in recs[marks[0] + 1:marks[1]] if not any(x in _col(r, "Kernel_Name") for x in EXCLUDE)]
@@ -1375,7 +1437,7 @@ def main():
                 "per_call": {"%s %d" % k: {"calls": r[0], "avg_us": r[1] / r[0] * 1e3,
                                            "tflops": r[2] / (r[1] * 1e-3) / 1e12 if r[1] > 0 else 0.0}
                              for k, r in rp["per"].items()},
-                "call_share_of_step": rp["ms"] / rp["pass_ms"]}
+                "call_ms_per_step": rp["ms"] / args.steps}
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms"] / args.steps, "higher_is_better": True,
