@@ -19,7 +19,9 @@
 // bwd: per step a split-K kernel for dh = Wc_h^T dA_{t+1} (the contraction
 // over the 4 |S| gate rows cut into slices, one partial sum each, so that the
 // small product still fills the chip), then the pointwise backward of step t,
-// which adds the partial sums in a fixed order; then K-batched GEMMs over all
+// which adds the partial sums in a fixed order; for small kept sets instead
+// one kernel per step that runs the whole contraction on 16 x 16 output tiles
+// and the pointwise backward on its outputs. Then K-batched GEMMs over all
 // steps for the weight gradients and one batched GEMM for dX.
 
 #include <hip/hip_runtime.h>
@@ -425,6 +427,101 @@ __global__ void __launch_bounds__(256) lstm_bwd_point_kernel(LstmStep s, const f
   }
 }
 
+// The backward recurrence in one launch per step. A workgroup owns 16 units x
+// 16 samples of dh_rec = Wc_h^T dA[t] and runs the whole contraction over the
+// 4 |S| gate rows itself (on the direct-load pipeline, the four waves on
+// disjoint quarters of each slab, 16x16x4 fp32 MFMAs),
+// adds the waves' sums through LDS in wave order, and the same threads then
+// run the pointwise backward of step t - 1 on their outputs (after step 0:
+// dh0 = dh_rec). Small output tiles give the grid its width in place of a
+// split contraction, so no partial sums leave the workgroup and no second
+// kernel is needed per step. A (m-contiguous): column I + u of Wc's gate rows;
+// B (n-contiguous): dA[t]. Needs 16-byte aligned rows (I, KW and B multiples
+// of 4). 128 gate rows per slab, 4 stages: the deeper 256-row slabs and 3 to
+// 8 stages measured the same or slower.
+using RecStepCfg = FastCfg<float, 16, 16, 128, 4, 1, 1, 4>;  // 64 KB LDS
+
+template <bool FINAL>
+__global__ void __launch_bounds__(RecStepCfg::NT) lstm_bwd_step_fused_kernel(LstmStep s) {
+  using Cfg = RecStepCfg;
+  constexpr int CPR = Cfg::BM * 4 / 16;  // 16-byte chunks per k-row of either operand
+  static_assert(Cfg::BM == 16 && Cfg::BN == 16 && Cfg::NW == 4 && Cfg::KW % 8 == 0, "16 x 16 tile, 4 waves");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int u0 = blockIdx.y * 16, b0 = blockIdx.x * 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nslab = (s.G4 + Cfg::BK - 1) / Cfg::BK;
+  SlabLoader<Cfg, true, true> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(w);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  ld.da.init(s.KW, u0, s.ns, ld.wv);
+  ld.db.init(s.B, b0, s.B, ld.wv);
+  ld.K = s.G4;
+  ld.ik = 0;
+  ld.is = 0;
+  ld.left = nslab - 1;
+  ld.a_step = static_cast<int64_t>(Cfg::BK) * s.KW * 4;
+  ld.b_step = static_cast<int64_t>(Cfg::BK) * s.B * 4;
+  ld.a_wrap = 0;
+  ld.b_wrap = 0;
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.dA + static_cast<int64_t>(s.t) * s.G4 * s.B));
+  // two accumulators on alternate k steps, so that consecutive MFMAs do not
+  // wait for each other's result
+  f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int q = 0; q < Cfg::STAGES - 1; ++q) ld.issue();
+  // MFMA operands: lane l holds A[m][k] and B[k][n] for m = n = l % 16 and
+  // k = l / 16 of each 4-deep step
+  const int mn = lane & 15, kl = lane >> 4;
+  int cs = 0, ck = 0;
+  for (int q = 0; q < nslab; ++q) {
+    wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+    lds_barrier();  // slab q is in LDS; no wave reads slab q - 1 any more
+    const char* st = smem + cs * Cfg::STAGE;
+    if (s.G4 - ck < Cfg::BK) {
+      fast_zero_tail<Cfg, Cfg::BM, true>(smem + cs * Cfg::STAGE, s.G4 - ck);
+      fast_zero_tail<Cfg, Cfg::BN, true>(smem + cs * Cfg::STAGE + Cfg::ABYTES, s.G4 - ck);
+      lds_barrier();
+    }
+    ld.issue();  // slab q + STAGES - 1, into the stage slab q - 1 held
+#pragma unroll
+    for (int j = 0; j < Cfg::KW / 4; j += 2) {
+      const int k0 = w * Cfg::KW + 4 * j + kl;
+      const int o0 = mc_off<CPR, 4>(k0, mn >> 2) + (mn & 3) * 4;
+      const int o1 = mc_off<CPR, 4>(k0 + 4, mn >> 2) + (mn & 3) * 4;
+      const float a0 = *reinterpret_cast<const float*>(st + o0);
+      const float b0v = *reinterpret_cast<const float*>(st + Cfg::ABYTES + o0);
+      const float a1 = *reinterpret_cast<const float*>(st + o1);
+      const float b1v = *reinterpret_cast<const float*>(st + Cfg::ABYTES + o1);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc1, 0, 0, 0);
+    }
+    cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
+    ck += Cfg::BK;
+  }
+  wait_vm<0>();  // no direct load may still write LDS past this point
+  // output (row r, column c) of the 16 x 16 MFMA tile: register r % 4 of lane
+  // 16 (r / 4) + c
+  float* red = reinterpret_cast<float*>(smem);
+  lds_barrier();  // every wave is done with the stages
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[(w * 4 + i) * 64 + lane] = acc0[i] + acc1[i];
+  lds_barrier();
+  const int tm = threadIdx.x >> 4, tn = threadIdx.x & 15;
+  const int src = (tm >> 2) * 16 + tn, reg = tm & 3;
+  float v = 0.0f;
+#pragma unroll
+  for (int ww = 0; ww < 4; ++ww) v += red[(ww * 4 + reg) * 64 + src];
+  const int64_t u = u0 + tm, b = b0 + tn;
+  if (u >= s.ns || b >= s.B) return;
+  const int64_t j = unit_row(s.idx, u);
+  if (FINAL) {
+    if (s.dh0) s.dh0[j * s.B + b] = v;
+  } else {
+    lstm_point_bwd(s, s.t - 1, u, b, s.dHs[(static_cast<int64_t>(s.t - 1) * s.H + j) * s.B + b] + v);
+  }
+}
+
 namespace {
 
 int check_lstm(const ard_lstm_desc* d, int32_t* ns, int32_t* period, int32_t* offset, const int32_t** idx) {
@@ -669,9 +766,41 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   const dim3 rgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32),
                    static_cast<unsigned>(splits));
   const bool vec = L.KW % 4 == 0 && L.Ic % 4 == 0 && L.B % 4 == 0;
+  // One fused launch per step where the direct loads can take the operands
+  // (aligned rows; chunk offsets of a slab below 2^31 bytes) and the operand
+  // stream stays small: 16-wide tiles read each operand twice as often as the
+  // 32-wide tiles of the split path, ns * 4 ns * B / 2 bytes per step. Measured
+  // on MI355X (T 35, batch 64, H 1024, backward per sequence): fused 262 / 329
+  // / 373 / 514 us at |S| = 64 / 128 / 256 / 342 against 408 / 460 / 463 / 600
+  // us split; 650 against 586 us at |S| = 512, where the stream is 32 MB.
+  const bool rec_fused = vec && aligned16(s.Wc) && aligned16(s.dA) &&
+                         int64_t{RecStepCfg::BK} * L.KW * 4 < (int64_t{1} << 31) &&
+                         int64_t{RecStepCfg::BK} * L.B * 4 < (int64_t{1} << 31) &&
+                         static_cast<int64_t>(ns) * L.G4 * L.B / 2 <= (int64_t{16} << 20);
+  if (rec_fused) {
+    static const hipError_t a0 = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(lstm_bwd_step_fused_kernel<false>), hipFuncAttributeMaxDynamicSharedMemorySize,
+        RecStepCfg::LDS);
+    static const hipError_t a1 = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(lstm_bwd_step_fused_kernel<true>), hipFuncAttributeMaxDynamicSharedMemorySize,
+        RecStepCfg::LDS);
+    ARD_HIP_CHECK(a0);
+    ARD_HIP_CHECK(a1);
+  }
+  const dim3 fgrid(static_cast<unsigned>((L.B + 15) / 16), static_cast<unsigned>((ns + 15) / 16));
   for (int t = static_cast<int>(L.T) - 1; t >= 0; --t) {
     if (t == 0 && !dh0) break;
     s.t = t;
+    if (rec_fused) {
+      if (t > 0) {
+        hipLaunchKernelGGL(lstm_bwd_step_fused_kernel<false>, fgrid, dim3(RecStepCfg::NT), RecStepCfg::LDS, sm, s);
+      } else {
+        s.dh0 = static_cast<float*>(dh0);
+        hipLaunchKernelGGL(lstm_bwd_step_fused_kernel<true>, fgrid, dim3(RecStepCfg::NT), RecStepCfg::LDS, sm, s);
+      }
+      ARD_LAUNCH_CHECK();
+      continue;
+    }
     if (rec_fast) {
       gr.b.p = s.dA + static_cast<int64_t>(t) * L.G4 * L.B;
       if (rec_wide)
