@@ -14,8 +14,9 @@
 //
 // fwd: one batched GEMM for the input projection of all steps (bias folded
 // in), then per step a kernel computing Wc_h h_{t-1} for a 32-row x 32-column
-// tile (four waves split the contraction and reduce through LDS) fused with
-// the gate nonlinearities and the state update.
+// tile (four waves split the contraction and reduce through LDS; 16 x 16
+// tiles for small kept sets) fused with the gate nonlinearities and the state
+// update.
 // bwd: per step a split-K kernel for dh = Wc_h^T dA_{t+1} (the contraction
 // over the 4 |S| gate rows cut into slices, one partial sum each, so that the
 // small product still fills the chip), then the pointwise backward of step t,
@@ -321,6 +322,103 @@ __global__ void __launch_bounds__(StepCfg::NT) lstm_fwd_step_fast_kernel(LstmSte
   }
   const int64_t u = r0 / 4 + 2 * w + (lane >> 5);
   const int64_t col = n0 + (lane & 31);
+  if (u >= s.ns || col >= s.B) return;
+  float* Zt = s.Z + static_cast<int64_t>(s.t) * s.G4 * s.B;
+  float gate[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) gate[q] = z[q] + Zt[(4 * u + q) * s.B + col];
+  const float ig = sigm(gate[0]), fg = sigm(gate[1]), gg = tanhf(gate[2]), og = sigm(gate[3]);
+  const float cp = s.Cc[(static_cast<int64_t>(s.t) * s.ns + u) * s.B + col];
+  const float c = fg * cp + ig * gg;
+  const float h = og * tanhf(c);
+  Zt[(4 * u + 0) * s.B + col] = ig;
+  Zt[(4 * u + 1) * s.B + col] = fg;
+  Zt[(4 * u + 2) * s.B + col] = gg;
+  Zt[(4 * u + 3) * s.B + col] = og;
+  s.Cc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = c;
+  s.Hc[(static_cast<int64_t>(s.t + 1) * s.ns + u) * s.B + col] = h;
+  s.Hs[(static_cast<int64_t>(s.t) * s.H + unit_row(s.idx, u)) * s.B + col] = h;
+}
+
+// The same step on 16 x 16 tiles (four units x 16 samples), for kept sets
+// whose 32 x 32 tiles leave most of the chip idle: four times the
+// workgroups, each operand read twice as often. In the 16x16x4 MFMA
+// accumulator layout lane l holds rows 4 (l / 16) .. + 3 of column l % 16,
+// the four gates of one unit, so after the reduction wave 0 updates the
+// cell of (unit l / 16, sample l % 16) in registers. A (k-contiguous): the
+// recurrent columns of Wc; B (n-contiguous): h_{t-1}.
+using StepCfg16 = FastCfg<float, 16, 16, 128, 4, 1, 1, 4>;  // 64 KB LDS
+
+__global__ void __launch_bounds__(StepCfg16::NT) lstm_fwd_step16_kernel(LstmStep s) {
+  using Cfg = StepCfg16;
+  constexpr int ACPR = Cfg::BK * 4 / 16, BCPR = Cfg::BN * 4 / 16;
+  static_assert(Cfg::BM == 16 && Cfg::BN == 16 && Cfg::NW == 4 && Cfg::KW % 8 == 0, "16 x 16 tile, 4 waves");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int r0 = blockIdx.y * 16, n0 = blockIdx.x * 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nslab = (s.ns + Cfg::BK - 1) / Cfg::BK;
+  SlabLoader<Cfg, false, true> ld;
+  ld.wv = __builtin_amdgcn_readfirstlane(w);
+  ld.lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+  ld.da.init(s.KW, r0, s.G4, ld.wv);
+  ld.db.init(s.B, n0, s.B, ld.wv);
+  ld.K = s.ns;
+  ld.ik = 0;
+  ld.is = 0;
+  ld.left = nslab - 1;
+  ld.a_step = Cfg::BK * 4;
+  ld.b_step = static_cast<int64_t>(s.B) * Cfg::BK * 4;
+  ld.a_wrap = 0;
+  ld.b_wrap = 0;
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B));
+  f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int q = 0; q < Cfg::STAGES - 1; ++q) ld.issue();
+  const int mn = lane & 15, kl = lane >> 4;
+  int cs = 0, ck = 0;
+  for (int q = 0; q < nslab; ++q) {
+    wait_vm<(Cfg::STAGES - 2) * Cfg::LPW>();
+    lds_barrier();  // slab q is in LDS; no wave reads slab q - 1 any more
+    const char* st = smem + cs * Cfg::STAGE;
+    if (s.ns - ck < Cfg::BK) {
+      fast_zero_tail<Cfg, Cfg::BM, false>(smem + cs * Cfg::STAGE, s.ns - ck);
+      fast_zero_tail<Cfg, Cfg::BN, true>(smem + cs * Cfg::STAGE + Cfg::ABYTES, s.ns - ck);
+      lds_barrier();
+    }
+    ld.issue();  // slab q + STAGES - 1, into the stage slab q - 1 held
+#pragma unroll
+    for (int j = 0; j < Cfg::KW / 4; j += 2) {
+      const int k0 = w * Cfg::KW + 4 * j + kl;
+      const float a0 = *reinterpret_cast<const float*>(st + kc_off<ACPR>(mn, k0 >> 2) + (k0 & 3) * 4);
+      const float a1 = *reinterpret_cast<const float*>(st + kc_off<ACPR>(mn, (k0 + 4) >> 2) + (k0 & 3) * 4);
+      const float b0v =
+          *reinterpret_cast<const float*>(st + Cfg::ABYTES + mc_off<BCPR, 4>(k0, mn >> 2) + (mn & 3) * 4);
+      const float b1v =
+          *reinterpret_cast<const float*>(st + Cfg::ABYTES + mc_off<BCPR, 4>(k0 + 4, mn >> 2) + (mn & 3) * 4);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0v, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1v, acc1, 0, 0, 0);
+    }
+    cs = cs + 1 == Cfg::STAGES ? 0 : cs + 1;
+    ck += Cfg::BK;
+  }
+  wait_vm<0>();  // no direct load may still write LDS past this point
+  float* red = reinterpret_cast<float*>(smem);
+  lds_barrier();  // every wave is done with the stages
+#pragma unroll
+  for (int i = 0; i < 4; ++i) red[(w * 4 + i) * 64 + lane] = acc0[i] + acc1[i];
+  lds_barrier();
+  if (w != 0) return;
+  float z[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float v = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) v += red[(ww * 4 + q) * 64 + lane];
+    z[q] = v;
+  }
+  const int64_t u = r0 / 4 + (lane >> 4);
+  const int64_t col = n0 + (lane & 15);
   if (u >= s.ns || col >= s.B) return;
   float* Zt = s.Z + static_cast<int64_t>(s.t) * s.G4 * s.B;
   float gate[4];
@@ -651,14 +749,25 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   // direct loads: aligned rows, and every chunk offset of a slab below 2^31 bytes
   const bool step_fast = avec && bvec && aligned16(s.Wc) &&
                          (L.G4 + 1) * L.KW * 4 < (int64_t{1} << 31) && (L.ns + 64) * L.B * 4 < (int64_t{1} << 31);
+  // 16 x 16 tiles where the 32 x 32 grid holds fewer than 128 workgroups
+  // (measured on MI355X, T 35, batch 64, H 1024: 255-269 against 288-290 us per
+  // forward at |S| = 256, 210-218 against 237-244 us at 128, equal at 342 and
+  // 64, slower at 512 and 1024)
+  const bool step16 = step_fast && ((L.G4 + 31) / 32) * ((L.B + 31) / 32) < 128;
   if (step_fast) {
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(lstm_fwd_step_fast_kernel),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, StepCfg::LDS);
+    static const hipError_t attr16 = hipFuncSetAttribute(reinterpret_cast<const void*>(lstm_fwd_step16_kernel),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, StepCfg16::LDS);
     ARD_HIP_CHECK(attr);
+    ARD_HIP_CHECK(attr16);
   }
+  const dim3 sgrid16(static_cast<unsigned>((L.B + 15) / 16), static_cast<unsigned>((L.G4 + 15) / 16));
   for (int t = 0; t < L.T; ++t) {
     s.t = t;
-    if (step_fast)
+    if (step16)
+      hipLaunchKernelGGL(lstm_fwd_step16_kernel, sgrid16, dim3(StepCfg16::NT), StepCfg16::LDS, sm, s);
+    else if (step_fast)
       hipLaunchKernelGGL(lstm_fwd_step_fast_kernel, sgrid, dim3(StepCfg::NT), StepCfg::LDS, sm, s);
     else if (avec && bvec)
       hipLaunchKernelGGL((lstm_fwd_step_kernel<true, true>), sgrid, dim3(256), 0, sm, s);
