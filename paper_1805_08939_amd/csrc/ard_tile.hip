@@ -733,9 +733,12 @@ struct TdpFastCfgs<bf16> {
   using Rows = FastCfg<bf16, 64, 128, 64, 4, 1, 2, 2>;   // 96 KB LDS
   using Group = FastCfg<bf16, 64, 256, 64, 3, 1, 4, 1>;  // 120 KB
 };
+// Narrow: 64 batch columns for batches of at most 64 (the tile-pattern
+// LSTM's steps), so that no half-empty batch tile is loaded and multiplied.
 template <>
 struct TdpFastCfgs<float> {
   using Rows = FastCfg<float, 64, 128, 32, 4, 1, 2, 2>;  // 96 KB
+  using Narrow = FastCfg<float, 64, 64, 32, 4, 1, 2, 2>; // 64 KB
   using Group = FastCfg<float, 64, 256, 32, 3, 1, 4, 1>; // 120 KB
 };
 
@@ -762,6 +765,17 @@ bool tdp_fast_ok(const TdpArgs& a) {
          static_cast<int64_t>(kFastTile + 1) * a.K * es < (int64_t{1} << 31);
 }
 
+// fwd or bwd_data on tile configuration Cfg: batch blocks of Cfg::BN, one
+// workgroup per (tile row or column, batch block, split).
+template <class Cfg, typename T>
+hipError_t launch_rows(int pass, TdpFastArgs& f, int owners, int splits, hipStream_t s) {
+  f.nx = (f.B + Cfg::BN - 1) / Cfg::BN;
+  f.ny = owners;
+  const dim3 grid(static_cast<unsigned>(f.nx * f.ny), static_cast<unsigned>(splits));
+  if (pass == TDP_FWD) return launch_with_lds<Cfg, tdp_fast_kernel<Cfg, TDP_FWD, T>>(grid, f, s);
+  return launch_with_lds<Cfg, tdp_fast_kernel<Cfg, TDP_BWD_DATA, T>>(grid, f, s);
+}
+
 template <typename T>
 hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int owners, int nnz, hipStream_t s) {
   using C = TdpFastCfgs<T>;
@@ -778,11 +792,10 @@ hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int o
     return launch_with_lds<typename C::Group, tdp_fast_dw_kernel<typename C::Group, float>>(
         dim3(static_cast<unsigned>(bound)), f, s);
   }
-  f.nx = (a.B + C::Rows::BN - 1) / C::Rows::BN;
-  f.ny = owners;
-  const dim3 grid(static_cast<unsigned>(f.nx * f.ny));
-  if (pass == TDP_FWD) return launch_with_lds<typename C::Rows, tdp_fast_kernel<typename C::Rows, TDP_FWD, T>>(grid, f, s);
-  return launch_with_lds<typename C::Rows, tdp_fast_kernel<typename C::Rows, TDP_BWD_DATA, T>>(grid, f, s);
+  if constexpr (sizeof(T) == 4) {
+    if (a.B <= C::Narrow::BN) return launch_rows<typename C::Narrow, T>(pass, f, owners, 1, s);
+  }
+  return launch_rows<typename C::Rows, T>(pass, f, owners, 1, s);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -886,7 +899,9 @@ int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan*
   if (!tdp_fast_ok<float>(a)) return single();
   using C = TdpFastCfgs<float>;
   const int owners = fwd ? p->tiles_n : p->tiles_k;
-  const int nx = (a.B + C::Rows::BN - 1) / C::Rows::BN;
+  const bool narrow = a.B <= C::Narrow::BN;
+  const int bn = narrow ? C::Narrow::BN : C::Rows::BN;
+  const int nx = (a.B + bn - 1) / bn;
   int splits = 1;
   while (splits < 8 && static_cast<int64_t>(nx) * owners * splits * 2 <= kTargetBlocks) splits *= 2;
   const int64_t rows = static_cast<int64_t>(owners) * kFastTile;
@@ -894,11 +909,11 @@ int tdp_product_f32_split(bool fwd, const ard_tile_desc* d, const ard_tile_plan*
   TdpFastArgs f = {a.act, nullptr, a.W, a.out, a.B, a.K, nx, owners, a.ptr, a.list, p->d_chunks, a.scale,
                    splits, static_cast<int32_t>(rows), partial};
   hipStream_t sm = static_cast<hipStream_t>(stream);
-  const dim3 grid(static_cast<unsigned>(nx * owners), static_cast<unsigned>(splits));
-  if (fwd)
-    ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_FWD, float>>(grid, f, sm)));
+  const int pass = fwd ? TDP_FWD : TDP_BWD_DATA;
+  if (narrow)
+    ARD_HIP_CHECK((launch_rows<C::Narrow, float>(pass, f, owners, splits, sm)));
   else
-    ARD_HIP_CHECK((launch_with_lds<C::Rows, tdp_fast_kernel<C::Rows, TDP_BWD_DATA, float>>(grid, f, sm)));
+    ARD_HIP_CHECK((launch_rows<C::Rows, float>(pass, f, owners, splits, sm)));
   if (splits_left) {  // the caller adds the partial sums itself (scale 1 only)
     *splits_left = splits;
     return ARD_OK;
