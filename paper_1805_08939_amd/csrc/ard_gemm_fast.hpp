@@ -541,25 +541,56 @@ __device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg:
   constexpr int ROW = Cfg::TN * 4 + 32;
   constexpr int CPRW = Cfg::TN / 4;  // 16-byte pieces per row
   constexpr int RPI = 64 / CPRW;     // rows per read instruction
-  static_assert(Cfg::NW * 32 * ROW <= Cfg::LDS, "epilogue staging exceeds LDS");
+  // the bias of the wave's TM rows sits behind the staging regions
+  static_assert(Cfg::NW * (32 * ROW + Cfg::TM * 4) <= Cfg::LDS, "epilogue staging exceeds LDS");
   lds_barrier();  // every wave is done with the stages
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int lr = lane & 31, lh = lane >> 5;
   char* region = smem + wave * 32 * ROW;
   const int m0w = m0 + wm * Cfg::TM, n0w = n0 + wn * Cfg::TN;
+  // The bias entries of the wave's rows, loaded once with every load in
+  // flight together (a load per accumulator row, each waited for before its
+  // row's values are staged, cost ~4 us per call of a small product), then
+  // read from LDS: the wave reads only what it wrote itself.
+  const bool has_bias = !part && EPI == EPI_FWD && g.c.bias;
+  float* bias_lds = reinterpret_cast<float*>(smem + Cfg::NW * 32 * ROW) + wave * Cfg::TM;
+  if (has_bias) {
+    float bv[(Cfg::TM + 63) / 64];
+#pragma unroll
+    for (int e = 0; e * 64 < Cfg::TM; ++e) {
+      const int m = m0w + e * 64 + lane;
+      bv[e] = (e * 64 + lane < Cfg::TM && m < g.M) ? g.c.bias[bias_row(g.c, m)] : 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e * 64 < Cfg::TM; ++e)
+      if (e * 64 + lane < Cfg::TM) bias_lds[e * 64 + lane] = bv[e];
+  }
 #pragma unroll
   for (int i = 0; i < Cfg::FM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = 8 * (r >> 2) + 4 * lh + (r & 3);
-      const int m = m0w + 32 * i + rl;
-      float bias = 0.0f;
-      if (!part && EPI == EPI_FWD && g.c.bias && m < g.M) bias = g.c.bias[bias_row(g.c, m)];
+      const float bias = has_bias ? bias_lds[32 * i + rl] : 0.0f;
 #pragma unroll
       for (int j = 0; j < Cfg::FN; ++j) {
         float v = acc[i][j][r];
         if (!part) v = epilogue<EPI>(g.c, v, bias);
         *reinterpret_cast<float*>(region + rl * ROW + (32 * j + lr) * 4) = v;
+      }
+    }
+    // the ReLU gate of the rows this lane writes, every load issued before
+    // the first store (the stores may alias the gate as far as the compiler
+    // knows, so loads between them would each wait for the one before)
+    typedef typename std::conditional<sizeof(OutT) == 2, uint2, f32x4>::type GateT;
+    GateT gpre[32 / RPI];
+    if (gate) {
+#pragma unroll
+      for (int t = 0; t < 32 / RPI; ++t) {
+        const int rl = lane / CPRW + RPI * t, ch = lane % CPRW;
+        const int m = m0w + 32 * i + rl, n = n0w + 4 * ch;
+        if (m < g.M && n + 3 < g.N)
+          gpre[t] = *reinterpret_cast<const GateT*>(reinterpret_cast<const OutT*>(gate) +
+                                                    static_cast<int64_t>(m) * ld + n);
       }
     }
 #pragma unroll
@@ -587,10 +618,7 @@ __device__ __forceinline__ void fast_store(const GemmArgs& g, f32x16 (&acc)[Cfg:
         for (int e = 0; e < 4; ++e) w[e] = from_f32<OutT>(v[e]);
         if (gt) {
           OutT gv[4];
-          if constexpr (sizeof(OutT) == 2)
-            *reinterpret_cast<uint2*>(gv) = *reinterpret_cast<const uint2*>(gt);
-          else
-            *reinterpret_cast<f32x4*>(gv) = *reinterpret_cast<const f32x4*>(gt);
+          *reinterpret_cast<GateT*>(gv) = gpre[t];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             if (!(to_f32(gv[e]) > 0.0f)) w[e] = from_f32<OutT>(0.0f);
