@@ -309,6 +309,134 @@ __global__ void __launch_bounds__(kScanThreads)
   }
 }
 
+// The same plan for grids of at most kWideDim tiles per side, spread over
+// tiles_n + tiles_k workgroups of kWideThreads: workgroup r < tiles_n lists
+// tile row r (CSR, flat, its bwd_weight groups), workgroup tiles_n + c lists
+// tile column c (CSC). Every workgroup stages the whole bitmap in LDS
+// (drawing it itself when sampling; workgroup 0 writes it out) and derives
+// its row's (column's) start from the counts of the rows (columns) before
+// it, so no workgroup waits for another. The outputs are those of
+// plan_tiles_kernel, entry for entry.
+constexpr int kWideThreads = 256;
+constexpr int kWideDim = 256;
+constexpr int kWideWords = kWideDim * kWideDim / 32;
+
+__global__ void __launch_bounds__(kWideThreads)
+    plan_tiles_wide_kernel(uint32_t* bits, TileSampler smp, int32_t tiles_n, int32_t tiles_k,
+                           int32_t* __restrict__ row_ptr, int32_t* __restrict__ row_cols,
+                           int32_t* __restrict__ col_ptr, int32_t* __restrict__ col_rows,
+                           int32_t* __restrict__ flat, int32_t* __restrict__ chunks) {
+  __shared__ uint32_t sbits[kWideWords];
+  __shared__ int32_t red[2][kWideThreads / 64];
+  __shared__ int32_t wpre[kWideThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t nbits = static_cast<int64_t>(tiles_n) * tiles_k;
+  const int nwords = static_cast<int>((nbits + 31) / 32);
+  if (smp.enabled) {
+    for (int64_t base = 0; base < nbits; base += kWideThreads) {
+      const int64_t t = base + tid;
+      bool keep = false;
+      if (t < nbits)
+        keep = static_cast<double>(splitmix_draw(smp.s0, static_cast<uint64_t>(t)) >> 11) * 0x1.0p-53 >= smp.p;
+      const uint64_t m = __ballot(keep);
+      const int64_t w0 = (base + 64 * wave) / 32;
+      if (lane < 2 && w0 + lane < nwords) {
+        const uint32_t x = static_cast<uint32_t>(m >> (32 * lane));
+        sbits[w0 + lane] = x;
+        if (blockIdx.x == 0) bits[w0 + lane] = x;
+      }
+    }
+  } else {
+    for (int w = tid; w < nwords; w += kWideThreads) sbits[w] = bits[w];
+  }
+  __syncthreads();
+  BitSrc src = {nullptr, sbits};
+  const bool is_row = static_cast<int>(blockIdx.x) < tiles_n;
+  const int own = is_row ? static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x) - tiles_n;
+  const int len = is_row ? tiles_k : tiles_n;     // entries of the own row (column)
+  const int nown = is_row ? tiles_n : tiles_k;    // rows (columns) in all
+  // counts of the rows (columns) before this one (and groups, for rows):
+  // thread i counts row (column) i
+  int32_t c_before = 0, g_before = 0, c_total = 0, g_total = 0;
+  {
+    int32_t c = 0;
+    if (tid < nown) {
+      if (is_row) {
+        c = src.count(static_cast<int64_t>(tid) * tiles_k, static_cast<int64_t>(tid + 1) * tiles_k);
+      } else {
+        for (int r = 0; r < tiles_n; ++r) c += src.bit(static_cast<int64_t>(r) * tiles_k + tid);
+      }
+    }
+    const int32_t g = (c + kTdpChunk - 1) / kTdpChunk;
+    int32_t cb = tid < own ? c : 0, gb = tid < own ? g : 0;
+    int32_t ct = c, gt = g;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      cb += __shfl_xor(cb, d, 64);
+      gb += __shfl_xor(gb, d, 64);
+      ct += __shfl_xor(ct, d, 64);
+      gt += __shfl_xor(gt, d, 64);
+    }
+    __shared__ int32_t tot[2][kWideThreads / 64];
+    if (lane == 0) {
+      red[0][wave] = cb;
+      red[1][wave] = gb;
+      tot[0][wave] = ct;
+      tot[1][wave] = gt;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < kWideThreads / 64; ++v) {
+      c_before += red[0][v];
+      g_before += red[1][v];
+      c_total += tot[0][v];
+      g_total += tot[1][v];
+    }
+  }
+  // the own row's (column's) entries: thread i takes entry i, its rank among
+  // the kept ones from a ballot per wave and the kept counts of the waves before
+  const bool kept = tid < len && (is_row ? src.bit(static_cast<int64_t>(own) * tiles_k + tid)
+                                         : src.bit(static_cast<int64_t>(tid) * tiles_k + own));
+  const uint64_t m = __ballot(kept);
+  if (lane == 0) wpre[wave] = __popcll(m);
+  __syncthreads();
+  int32_t rank = __popcll(m & ((uint64_t{1} << lane) - 1));
+  int32_t nkept = 0;
+#pragma unroll
+  for (int v = 0; v < kWideThreads / 64; ++v) {
+    if (v < wave) rank += wpre[v];
+    nkept += wpre[v];
+  }
+  if (is_row) {
+    if (tid == 0) row_ptr[own] = c_before;
+    if (own == tiles_n - 1 && tid == 0) {
+      row_ptr[tiles_n] = c_total;
+      chunks[0] = g_total;
+      chunks[1] = chunks[2] = chunks[3] = 0;
+    }
+    if (kept) {
+      const int32_t pos = c_before + rank;
+      row_cols[pos] = tid;
+      flat[pos] = own * tiles_k + tid;
+      int32_t* rec = chunks + 4 + static_cast<int64_t>(g_before + rank / kTdpChunk) * kTdpRec;
+      const int slot = rank % kTdpChunk;
+      if (slot == 0) {
+        rec[0] = own;
+        rec[1] = pos;
+        rec[2] = nkept - rank < kTdpChunk ? nkept - rank : kTdpChunk;
+        rec[3] = 0;
+      }
+      rec[4 + slot] = tid;
+      if (rank == nkept - 1)  // the row's last tile pads its group
+        for (int i = slot + 1; i < kTdpChunk; ++i) rec[4 + i] = tid;
+    }
+  } else {
+    if (tid == 0) col_ptr[own] = c_before;
+    if (own == tiles_k - 1 && tid == 0) col_ptr[tiles_k] = c_total;
+    if (kept) col_rows[c_before + rank] = tid;
+  }
+}
+
 enum TdpPass { TDP_FWD = 0, TDP_BWD_DATA = 1, TDP_BWD_WEIGHT = 2 };
 
 struct TdpArgs {
@@ -866,9 +994,14 @@ int plan_tiles(int32_t n, int32_t k, int32_t tile, uint32_t* d_bits, int32_t nnz
   plan->d_flat = reinterpret_cast<int32_t*>(w);
   w += align256(4 * full);
   plan->d_chunks = reinterpret_cast<int32_t*>(w);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, static_cast<hipStream_t>(stream),
-                     d_bits, smp, tn, tk, plan->d_row_ptr, plan->d_row_cols, plan->d_col_ptr,
-                     plan->d_col_rows, plan->d_flat, plan->d_chunks);
+  if (tn <= kWideDim && tk <= kWideDim)
+    hipLaunchKernelGGL(plan_tiles_wide_kernel, dim3(static_cast<unsigned>(tn + tk)), dim3(kWideThreads), 0,
+                       static_cast<hipStream_t>(stream), d_bits, smp, tn, tk, plan->d_row_ptr, plan->d_row_cols,
+                       plan->d_col_ptr, plan->d_col_rows, plan->d_flat, plan->d_chunks);
+  else
+    hipLaunchKernelGGL(plan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, static_cast<hipStream_t>(stream),
+                       d_bits, smp, tn, tk, plan->d_row_ptr, plan->d_row_cols, plan->d_col_ptr,
+                       plan->d_col_rows, plan->d_flat, plan->d_chunks);
   ARD_LAUNCH_CHECK();
   return ARD_OK;
 }

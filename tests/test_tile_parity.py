@@ -182,8 +182,20 @@ def test_plan_lists_of_large_grids(grid):
     tile_plan(tn * 32, tk * 32, 32, words)
 
 
+@pytest.mark.parametrize("grid", [(256, 256), (256, 1), (1, 256), (200, 37), (64, 64)])
+def test_plan_lists_up_to_256_tiles_per_side(grid):
+    """Grids of at most 256 tiles per side are planned by one workgroup per
+    tile row and one per tile column: every list against the oracle, for a
+    Bernoulli bitmap, the tile pattern, every tile kept and none kept."""
+    tn, tk = grid
+    for words in (oprng.tile_bitmap_bernoulli(tn, tk, 0.6, 23, 1, 2), oprng.tile_bitmap_tdp(tn, tk, 3, 1),
+                  oprng.tile_bitmap_tdp(tn, tk, 1, 0), oprng.tile_bitmap_bernoulli(tn, tk, 1.0, 1, 0, 0)):
+        tile_plan(tn * 32, tk * 32, 32, words)
+
+
 @pytest.mark.parametrize("grid,p", [((64, 64), 0.5), ((3, 5), 0.4), ((70, 66), 0.02), ((260, 260), 0.6),
-                                    ((33, 1100), 0.3), ((4, 4), 0.0), ((4, 4), 1.0)])
+                                    ((33, 1100), 0.3), ((4, 4), 0.0), ((4, 4), 1.0), ((256, 256), 0.5),
+                                    ((256, 1), 0.3)])
 def test_device_sampled_bitmap_and_lists(grid, p):
     tn, tk = grid
     sampled_plan(tn * 32, tk * 32, 32, p, 8939, 0, 5)
