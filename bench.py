@@ -1194,7 +1194,7 @@ def summarize_trace(path, top, last=0, tail=0):
 
 MARKER = "FillFunctor<short>"
 # per-step work outside the layer calls, and the pass's spin kernel
-EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel", "plan_rows_kernel", "spin_kernel")
+EXCLUDE = ("compact_weights_kernel", "plan_tiles_kernel", "plan_tiles_wide_kernel", "plan_rows_kernel", "spin_kernel")
 
 
 def summarize_pass(path, top, calls, kind):
