@@ -239,3 +239,33 @@ def test_stacked_lstm_full_width():
         if l > 0:
             _normwise(st.dX[l].double().cpu().numpy().transpose(0, 2, 1), dX, f"dX{l}")
         dH = dX
+
+
+@pytest.mark.parametrize("period", [3, 8])
+def test_lstm_full_width_small_kept_sets(period):
+    """The 1024/1024 LSTM at batch 64 (4 steps instead of 35) with hidden
+    period 3 (342 kept units) and 8 (128): the kept sets whose backward steps
+    run the fused one-kernel recurrence and whose forward steps run on 16 x 16
+    tiles. Hs, hT, cT, dX, dW, db, dh0 and dc0 against the oracle."""
+    import bench
+    wl = bench.Lstm("lstm-t4", T=4, batch=64, inputs=1024, hidden=1024, dtype="f32", seed=1811)
+    api = wl.api
+    api.ard_plan_rows(wl.H, period, 1, wl.idx, wl.stream, plan=wl.plan)
+    d = wl.desc
+    api.ard_lstm_fwd(d, wl.X, wl.W, wl.b, None, None, wl.Hs, wl.hT, wl.cT, wl.ws, wl.stream)
+    api.ard_lstm_bwd(d, wl.X, wl.dHs, None, None, wl.ws, wl.dX, wl.dW, wl.db, wl.dh0, wl.dc0, wl.stream)
+    torch.cuda.synchronize()
+    wl.host_copies()
+    X, W, b, dHs = wl._host
+    m = opat.row_mask(wl.H, period, 1)
+    Hs, hT, cT, cache = olstm.lstm_forward(X, W, b, m)
+    dX, dW, db, dh0, dc0 = olstm.lstm_backward(X, W, m, cache, dHs)
+    t = lambda a: a.double().cpu().numpy()
+    _normwise(t(wl.Hs).transpose(0, 2, 1), Hs, "Hs")
+    _normwise(t(wl.hT).T, hT, "hT")
+    _normwise(t(wl.cT).T, cT, "cT")
+    _normwise(t(wl.dX).transpose(0, 2, 1), dX, "dX")
+    _normwise(t(wl.dW), dW, "dW")
+    _normwise(t(wl.db), db, "db")
+    _normwise(t(wl.dh0).T, dh0, "dh0")
+    _normwise(t(wl.dc0).T, dc0, "dc0")
