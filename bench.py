@@ -962,8 +962,8 @@ def roofline_pass(wl, steps, warmup, it0):
 def _roofline_pass(wl, steps, warmup, it0):
     """The same steps once more with every layer call bracketed by a HIP event
     pair on the step stream. Returns, per call key and in total, the number of
-    calls, the summed event time and the summed kept FLOPs, plus the whole
-    pass's GPU time. A one-element int16 fill before and after the timed steps
+    calls, the summed event time, the summed kept FLOPs and the algorithmic
+    bytes of the calls. A one-element int16 fill before and after the timed steps
     marks their kernels in a rocprofv3 trace or counter run of this command
     (--summarize-pass)."""
     import torch
