@@ -1092,9 +1092,37 @@ def cpu_baseline(wl, p, budget_s):
             "sample": f"{n} steps of the same workload at p={p} (fp64 masked dense layers, numpy), {t:.1f} s"}
 
 
+def code_text(src):
+    """C/C++/HIP source text without its comments, with every run of blanks
+    within a line made one space and blank lines dropped (string and character
+    literals kept as they are): what the compiler sees of the code, up to
+    layout."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif src[i] in "\"'":
+            q, j = src[i], i + 1
+            while j < n and src[j] != q:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(src[i])
+            i += 1
+    lines = (" ".join(line.split()) for line in "".join(out).split("\n"))
+    return "\n".join(line for line in lines if line)
+
+
 def source_digest():
-    """sha256 over the kernel sources and the header: a stored counter reading
-    holds only for the code it was taken on."""
+    """sha256 over the code of the kernel sources and the header (comments and
+    layout left out): a stored counter reading holds only for the code it was
+    taken on."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1805_08939_amd", "csrc")
@@ -1102,8 +1130,8 @@ def source_digest():
     files.append(os.path.join(ROOT, "include", "ard.h"))
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(code_text(fh.read()).encode())
     return h.hexdigest()
 
 

@@ -257,7 +257,11 @@ typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
  *                             ard_fc_sgd_momentum takes dW in this layout too.
  * With FULL weights and a gathered input side, fwd and bwd_data build the
  * compact copy in their workspace themselves; a training step that compacts
- * once and passes COMPACT to both saves one pass over W.
+ * once and passes COMPACT to both saves one pass over W. With an ungathered
+ * input side FULL reads the kept rows of W in place, and where those rows do
+ * not start on a 16-byte boundary the products run on the general kernel:
+ * Y and dX of FULL and COMPACT then agree up to the order of rounding, not
+ * bit for bit.
  */
 typedef enum {
   ARD_WEIGHTS_FULL = 0,

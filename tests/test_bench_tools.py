@@ -98,6 +98,18 @@ def test_traffic_record_follows_the_source_digest(tmp_path, monkeypatch):
     assert bench.traffic_record("w", 0.7, 100) is None  # only the stale record is left
 
 
+def test_digest_ignores_comments_and_layout():
+    """Comments, blank lines and runs of blanks do not change the code a
+    record was taken on; a change of the code does."""
+    a = "int f(int x) {  // one\n  return x + 1; /* two */\n}\n"
+    b = "/* header\n   lines */\nint f(int x) {\n\n  return  x + 1;\n}  // end\n"
+    c = "int f(int x) {\n  return x + 2;\n}\n"
+    assert bench.code_text(a) == bench.code_text(b) == "int f(int x) {\nreturn x + 1;\n}"
+    assert bench.code_text(c) != bench.code_text(a)
+    s = 'const char* s = "/* kept */ // kept"; char q = \'"\';'
+    assert bench.code_text(s) == s
+
+
 def test_committed_traffic_records_parse():
     """Every committed profile carries one parsable traffic record with the
     fields the benchmark reads."""

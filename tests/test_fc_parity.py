@@ -70,8 +70,13 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
     api.ard_fc_bwd(desc, Xt, dYt, Yst, Wd, dXt2, dW2, db2, ws)
     torch.cuda.synchronize()
     assert torch.equal(dXt2, dXt) and torch.equal(dW2, dW) and torch.equal(db2, db)
+    # Y and dX of the compact layouts, checked against the oracle below: equal
+    # to the full layout's up to the rounding order (a full-layout view that the
+    # direct-load kernels cannot read takes the general kernel)
+    alt = {"Y": [], "dX": []}
     if pin != (1, 0) and not poison:
-        # the same layer with the caller compacting W once: bitwise identical
+        # the same layer with the caller compacting W once (with a gathered
+        # input side the full layout compacts W itself: bitwise identical)
         cdesc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, out_plan, scale, ACTS[act], dropped,
                             api.ARD_WEIGHTS_COMPACT)
         Wc = torch.empty(max(api.ard_fc_compact_bytes(cdesc), 16) // 2, dtype=torch.int16, device=device())
@@ -82,6 +87,8 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
         api.ard_fc_bwd_data(cdesc, dYt, Yst, Wc, dXt2, cws)
         torch.cuda.synchronize()
         assert torch.equal(Yt2, Yt) and torch.equal(dXt2, dXt)
+        alt["Y"].append(Yt2)
+        alt["dX"].append(dXt2)
     if not poison:
         # the compact weight gradient: dWc[i][j] = dW[S_out(i)][S_in(j)] bit
         # for bit, through bwd_weight and through the one-call backward
@@ -95,16 +102,18 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
         nc = len(Sout) * ldc
         dWc_buf = torch.full((max(nc, 4),), 7.0, device=device())  # never a null pointer
         dWc2_buf, db3, dXt3 = dWc_buf.clone(), torch.full_like(db, fill), torch.full_like(dXt, fill)
-        db4 = torch.full_like(db, fill)
+        db4, dXt4 = torch.full_like(db, fill), torch.full_like(dXt, fill)
         api.ard_fc_bwd_weight(gdesc, Xt, dYt, Yst, dWc_buf, db3, gws)
         api.ard_fc_bwd(gdesc, Xt, dYt, Yst, Wc, dXt3, dWc2_buf, db4, gws)
+        api.ard_fc_bwd_data(gdesc, dYt, Yst, Wc, dXt4, gws)
         torch.cuda.synchronize()
         dWc, dWc2 = dWc_buf[:nc].view(len(Sout), ldc), dWc2_buf[:nc].view(len(Sout), ldc)
         want_c = dW[torch.tensor(Sout, dtype=torch.long, device=device())][:, torch.tensor(Sin, dtype=torch.long,
                                                                                               device=device())]
         assert torch.equal(dWc[:, :len(Sin)], want_c) and torch.equal(dWc2_buf, dWc_buf)
         assert (dWc[:, len(Sin):] == 7.0).all(), "padding columns were written"
-        assert torch.equal(db3, db) and torch.equal(db4, db) and torch.equal(dXt3, dXt)
+        assert torch.equal(db3, db) and torch.equal(db4, db) and torch.equal(dXt3, dXt4)
+        alt["dX"].append(dXt3)
 
     Xa, Wa = np.abs(f64(X) * m_in[None, :]), np.abs(f64(W))
     G = ofc.fc_output_grad(f64(Ys), f64(dY), m_out, scale, act)
@@ -119,13 +128,14 @@ def run_layer(dtype, X, W, b, dY, pin, pout, act, scale, dropped, use_null_plans
             "dW": np.outer(m_out, m_in) > 0, "db": m_out > 0}
     want = {"Y": Y64, "dX": dX64, "dW": dW64, "db": db64}
     norm = {"Y": nY, "dX": ndX, "dW": ndW, "db": ndb}
-    for k in got:
+    checks = [(k, v) for k, v in got.items()] + [(k, f64(v).T) for k, vs in alt.items() for v in vs]
+    for k, v in checks:
         if dropped == api.ARD_DROPPED_SKIP:
             # untouched: bit-identical sentinel outside the kept sets
-            assert (got[k][~keep[k]] == fill).all(), f"{k}: dropped entries were written"
-            compare(got[k][keep[k]], want[k][keep[k]], norm[k][keep[k]], t, k)
+            assert (v[~keep[k]] == fill).all(), f"{k}: dropped entries were written"
+            compare(v[keep[k]], want[k][keep[k]], norm[k][keep[k]], t, k)
         else:
-            compare(got[k], want[k], norm[k], t, k)
+            compare(v, want[k], norm[k], t, k)
     return Yt, dXt, dW, db
 
 
@@ -149,6 +159,36 @@ def test_multi_tile_ragged(dtype, shape):
                                           ((4, 2), (1, 0), "relu"), ((7, 0), (3, 1), "none")]):
         run_layer(dtype, X, W, b, dY, pin, pout, act, 1.25, api.ARD_DROPPED_ZERO,
                   use_null_plans=False, lists=i % 2 == 1)
+
+
+def random_cases(dtype, n, seed):
+    """n seeded layer shapes and patterns spread over the planner's choices:
+    batch from 1 to 600, sides from 1 to 3000 (the long contractions take a
+    k split), periods 1 to 16 with any offset, both activations and modes."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        B = int(rng.choice([1, 16, 64, 96, 128, 200, 256, 512, 600]))
+        K = int(rng.integers(1, 3001))
+        N = int(rng.integers(1, 3001))
+        pin = (1, 0) if rng.random() < 0.3 else (lambda q: (q, int(rng.integers(0, q))))(int(rng.integers(2, 17)))
+        pout = (1, 0) if rng.random() < 0.3 else (lambda q: (q, int(rng.integers(0, q))))(int(rng.integers(2, 17)))
+        act = "relu" if rng.random() < 0.5 else "none"
+        dropped = api.ARD_DROPPED_SKIP if rng.random() < 0.5 else api.ARD_DROPPED_ZERO
+        cases.append((B, K, N, pin, pout, act, dropped))
+    return cases
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_random_shapes_and_patterns(dtype):
+    """Every product of 12 random layers (see random_cases) against the oracle,
+    with the sentinel checks of SKIP mode; the case is printed before it runs."""
+    for i, (B, K, N, pin, pout, act, dropped) in enumerate(random_cases(dtype, 12, 8939 + (dtype == "bf16"))):
+        print(f"case {i}: {dtype} B={B} K={K} N={N} pin={pin} pout={pout} act={act} dropped={dropped}", flush=True)
+        X, W, b, dY = make_inputs(dtype, B, K, N, seed=1805 + i)
+        sentinel = -3.25 if dropped == api.ARD_DROPPED_SKIP else None
+        run_layer(dtype, X, W, b, dY, pin, pout, act, 1.0 / 0.7, dropped, use_null_plans=i % 3 != 0,
+                  sentinel=sentinel, lists=i % 2 == 0)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
