@@ -115,6 +115,36 @@ def test_all_units_kept_wide_recurrence_tiles(shape):
     run_lstm(*shape, (1, 0), seed=sum(shape), with_state=True)
 
 
+def random_lstm_cases(n, seed):
+    """n seeded layer shapes: 1-5 steps, batch 1-100, input and hidden sizes
+    1-700, a hidden pattern of period 1-16 and (in a third of the cases) an
+    input pattern, each keeping at least one unit; initial state and final
+    gradients present or absent."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        T = int(rng.integers(1, 6))
+        B = int(rng.choice([1, 2, 5, 8, 16, 20, 33, 64, 100]))
+        I, H = int(rng.integers(1, 701)), int(rng.integers(1, 701))
+        q = 1 if rng.random() < 0.25 else int(rng.integers(2, 17))
+        pat = (q, int(rng.integers(0, q)))
+        qi = int(rng.integers(2, 9)) if rng.random() < 0.33 else 1
+        ipat = (qi, int(rng.integers(0, qi)))
+        if opat.row_kept_count(H, *pat) < 1 or opat.row_kept_count(I, *ipat) < 1:
+            continue
+        out.append((T, B, I, H, pat, ipat, bool(rng.random() < 0.5), bool(rng.random() < 0.5)))
+    return out
+
+
+def test_random_shapes_and_patterns():
+    """Forward and backward of 10 random layers (see random_lstm_cases) against
+    the oracle; the case is printed before it runs."""
+    for i, (T, B, I, H, pat, ipat, state, finals) in enumerate(random_lstm_cases(10, 1805)):
+        print(f"case {i}: T={T} B={B} I={I} H={H} pattern={pat} input={ipat} state={state} finals={finals}",
+              flush=True)
+        run_lstm(T, B, I, H, pat, seed=100 + i, with_state=state, with_final_grads=finals, in_pattern=ipat)
+
+
 def test_full_config_lstm_1024():
     """Single LSTM layer fp32, input 1024, hidden 1024, 35 steps, batch 64, hidden
     units dropped with period 2 (seeded offset), inputs ~ U(-0.1, 0.1)."""

@@ -136,6 +136,36 @@ def test_lists_longer_than_64_tiles(dtype):
         run_tile(dtype, 16, tn * 64, tk * 64, 64, words, scale=0.5)
 
 
+def random_tile_cases(n, seed):
+    """n seeded layers: 32- or 64-tiles, 1-40 tiles per side, batch 1-512, a
+    Bernoulli bitmap (drop rate 0-0.95) or the tile pattern of a period and
+    offset, either dropped mode and a scale."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        tile = int(rng.choice([32, 64]))
+        tn, tk = int(rng.integers(1, 41)), int(rng.integers(1, 41))
+        B = int(rng.choice([1, 8, 16, 64, 72, 128, 131, 200, 256, 512]))
+        if rng.random() < 0.5:
+            words = oprng.tile_bitmap_bernoulli(tn, tk, float(rng.uniform(0.0, 0.95)), int(rng.integers(1, 1000)), 0, 0)
+        else:
+            q = int(rng.integers(1, 9))
+            words = oprng.tile_bitmap_tdp(tn, tk, q, int(rng.integers(0, q)))
+        dropped = api.ARD_DROPPED_SKIP if rng.random() < 0.5 else api.ARD_DROPPED_ZERO
+        out.append((tile, tn, tk, B, words, dropped, float(rng.choice([1.0, 1.25, 2.0]))))
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_random_grids_and_patterns(dtype):
+    """fwd, bwd_data and bwd_weight of 8 random layers (see random_tile_cases)
+    against the oracle; the case is printed before it runs."""
+    for i, (tile, tn, tk, B, words, dropped, scale) in enumerate(random_tile_cases(8, 64 + (dtype == "bf16"))):
+        print(f"case {i}: {dtype} tile={tile} grid={tn}x{tk} B={B} dropped={dropped} scale={scale}", flush=True)
+        run_tile(dtype, B, tn * tile, tk * tile, tile, words, scale=scale, dropped=dropped, seed=i,
+                 sentinel=-1.5 if dropped == api.ARD_DROPPED_SKIP else 0.0)
+
+
 def test_full_config_bf16_4096():
     """One 4096x4096 layer, batch 512, bf16, 64x64 tiles kept by a seeded
     Bernoulli bitmap at p = 0.5: sampled output rows against the oracle."""
