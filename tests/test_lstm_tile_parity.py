@@ -96,6 +96,29 @@ def test_larger_layer():
         with_state=False)
 
 
+def test_random_shapes_and_patterns():
+    """8 random layers: 32- or 64-tiles, 1-4 steps, batch 1-64, input and hidden
+    sizes of 1-8 and 1-6 tiles, a Bernoulli bitmap (drop rate 0-0.9) or the
+    tile pattern of a period and offset; the case is printed before it runs."""
+    rng = np.random.default_rng(1805)
+    for i in range(8):
+        tile = int(rng.choice([32, 64]))
+        T, B = int(rng.integers(1, 5)), int(rng.choice([1, 8, 16, 20, 64]))
+        I, H = tile * int(rng.integers(1, 9)), tile * int(rng.integers(1, 7))
+        if rng.random() < 0.5:
+            p, seed = float(rng.uniform(0.0, 0.9)), int(rng.integers(1, 1000))
+            words_of = lambda tn, tk, p=p, seed=seed: oprng.tile_bitmap_bernoulli(tn, tk, p, seed, 0, 0)
+            what = f"bernoulli p={p:.2f}"
+        else:
+            q = int(rng.integers(1, 6))
+            off = int(rng.integers(0, q))
+            words_of = lambda tn, tk, q=q, off=off: oprng.tile_bitmap_tdp(tn, tk, q, off)
+            what = f"tdp ({q}, {off})"
+        state = bool(rng.random() < 0.5)
+        print(f"case {i}: tile={tile} T={T} B={B} I={I} H={H} {what} state={state}", flush=True)
+        run(T, B, I, H, tile, words_of, seed=40 + i, with_state=state)
+
+
 def test_invalid():
     d = device()
     words = oprng.tile_bitmap_tdp(4, 3, 1, 0)
