@@ -44,6 +44,7 @@ using RecWideCfg = FastCfg<float, 32, 64, 128, 3, 1, 2, 4>;
 struct Layout {
   int64_t T, B, I, H, ns, G4, KW, S;
   int64_t Ic, ip, io;  // kept inputs (compact input width) and their pattern
+  int64_t R;           // first recurrent column of a compact row: Ic rounded up to 16 bytes
   size_t wc, bc, rowmap, z, cc, hc, da, dc, part, total;
 };
 
@@ -72,7 +73,11 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
   L.Ic = in_all ? L.I : d->input_plan->kept;
   L.ip = in_all ? 1 : d->input_plan->period;
   L.io = in_all ? 0 : d->input_plan->offset;
-  L.KW = (L.Ic + ns + 3) / 4 * 4;  // compact rows padded to 16 bytes (zeros past Ic + |S|)
+  // compact rows [Ic inputs][zeros to R][|S| recurrent][zeros to KW]: the
+  // recurrent part starts on a 16-byte boundary whatever the input pattern
+  // keeps, so the step kernels' direct loads can read it
+  L.R = (L.Ic + 3) / 4 * 4;
+  L.KW = (L.R + ns + 3) / 4 * 4;
   L.S = bwd_splits(ns, L.B);
   size_t off = 0;
   L.wc = off;     off += al256(4 * L.G4 * L.KW);
@@ -93,10 +98,11 @@ Layout make_layout(const ard_lstm_desc* d, int32_t ns) {
 __device__ __forceinline__ int64_t unit_row(const int32_t* idx, int64_t u) { return idx ? idx[u] : u; }
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
 
-// Compact weights (rows of KW >= I + |S| entries, zero past I + |S|), bias
-// and row map; one block per compact row 4u + g.
+// Compact weights (rows of KW entries: the Ic kept inputs, zeros up to R,
+// the |S| kept recurrent columns from R on, zeros after), bias and row map;
+// one block per compact row 4u + g.
 __global__ void lstm_prepare_kernel(const float* __restrict__ W, const float* __restrict__ bias,
-                                    const int32_t* __restrict__ idx, int32_t I, int32_t Ic, int32_t ip,
+                                    const int32_t* __restrict__ idx, int32_t I, int32_t Ic, int32_t R, int32_t ip,
                                     int32_t io, int32_t H, int32_t ns, int32_t KW, float* __restrict__ Wc,
                                     float* __restrict__ bc, int32_t* __restrict__ rowmap) {
   const int r = blockIdx.x;
@@ -105,7 +111,9 @@ __global__ void lstm_prepare_kernel(const float* __restrict__ W, const float* __
   const float* wrow = W + src * (I + H);
   float* crow = Wc + static_cast<int64_t>(r) * KW;
   for (int c = threadIdx.x; c < KW; c += blockDim.x)
-    crow[c] = c < Ic ? wrow[io + static_cast<int64_t>(ip) * c] : c < Ic + ns ? wrow[I + unit_row(idx, c - Ic)] : 0.0f;
+    crow[c] = c < Ic                  ? wrow[io + static_cast<int64_t>(ip) * c]
+              : c >= R && c < R + ns ? wrow[I + unit_row(idx, c - R)]
+                                     : 0.0f;
   if (threadIdx.x == 0) {
     bc[r] = bias ? bias[src] : 0.0f;
     rowmap[r] = static_cast<int32_t>(src);
@@ -196,6 +204,7 @@ struct LstmStep {
   const float* dHs;     // [T][H][B]
   float* dh0;           // [H][B] or NULL (final backward step)
   int32_t t, B, I, H, ns, G4, KW;
+  int32_t R;            // first recurrent column of a Wc row (16-byte aligned)
 };
 
 constexpr int kStepBK = 64;
@@ -253,7 +262,7 @@ __global__ void __launch_bounds__(256) lstm_fwd_step_kernel(LstmStep s) {
   b.ld = s.B;
   const float* hprev = s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B;
   float z[4];
-  splitk_32x32<AVEC ? KC_VEC : KC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I, b, hprev, r0, n0, s.G4, s.B,
+  splitk_32x32<AVEC ? KC_VEC : KC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.R, b, hprev, r0, n0, s.G4, s.B,
                                                                   s.ns, z);
   const int64_t u = r0 / 4 + 2 * w + (lane >> 5);
   const int64_t col = n0 + (lane & 31);
@@ -303,7 +312,7 @@ __global__ void __launch_bounds__(StepCfg::NT) lstm_fwd_step_fast_kernel(LstmSte
   ld.b_step = static_cast<int64_t>(s.B) * Cfg::BK * 4;
   ld.a_wrap = 0;
   ld.b_wrap = 0;
-  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.R));
   ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B));
   run_slabs<Cfg, false, true, true>(ld, nslab, s.ns, 0, acc, 0, 0, w * Cfg::KW, smem);
   // wave v's registers 4 w' .. 4 w' + 3 (rows 8 w' + 4 (lane / 32) + q) go to wave w'
@@ -370,7 +379,7 @@ __global__ void __launch_bounds__(StepCfg16::NT) lstm_fwd_step16_kernel(LstmStep
   ld.b_step = static_cast<int64_t>(s.B) * Cfg::BK * 4;
   ld.a_wrap = 0;
   ld.b_wrap = 0;
-  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.R));
   ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.Hc + static_cast<int64_t>(s.t) * s.ns * s.B));
   f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -480,7 +489,7 @@ __global__ void __launch_bounds__(256) lstm_bwd_rec_kernel(LstmStep s, float* __
   b.ld = s.B;
   const float* dAt = s.dA + static_cast<int64_t>(s.t) * s.G4 * s.B;
   float z[4];
-  splitk_32x32<AVEC ? MC_VEC : MC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.I + k0 * s.KW, b, dAt + k0 * s.B, m0,
+  splitk_32x32<AVEC ? MC_VEC : MC_ELEM, BVEC ? MC_VEC : MC_ELEM>(a, s.Wc + s.R + k0 * s.KW, b, dAt + k0 * s.B, m0,
                                                                   n0, s.ns, s.B, klen, z);
   const int64_t col = n0 + (lane & 31);
   if (col >= s.B) return;
@@ -561,7 +570,7 @@ __global__ void __launch_bounds__(RecStepCfg::NT) lstm_bwd_step_fused_kernel(Lst
   ld.b_step = static_cast<int64_t>(Cfg::BK) * s.B * 4;
   ld.a_wrap = 0;
   ld.b_wrap = 0;
-  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.I));
+  ld.na = uniform_ptr(reinterpret_cast<const char*>(s.Wc + s.R));
   ld.nb = uniform_ptr(reinterpret_cast<const char*>(s.dA + static_cast<int64_t>(s.t) * s.G4 * s.B));
   // two accumulators on alternate k steps, so that consecutive MFMAs do not
   // wait for each other's result
@@ -663,7 +672,8 @@ LstmStep step_args(const Layout& L, char* w, const int32_t* idx) {
   s.dA = reinterpret_cast<float*>(w + L.da);
   s.dc = reinterpret_cast<float*>(w + L.dc);
   s.B = static_cast<int32_t>(L.B);
-  s.I = static_cast<int32_t>(L.Ic);  // compact input width: the recurrent columns of Wc start here
+  s.I = static_cast<int32_t>(L.Ic);  // compact input width
+  s.R = static_cast<int32_t>(L.R);   // the recurrent columns of Wc start here
   s.H = static_cast<int32_t>(L.H);
   s.ns = static_cast<int32_t>(L.ns);
   s.G4 = static_cast<int32_t>(L.G4);
@@ -715,7 +725,7 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   }
 
   hipLaunchKernelGGL(lstm_prepare_kernel, dim3(static_cast<unsigned>(L.G4)), dim3(256), 0, sm,
-                     static_cast<const float*>(W), bias, idx, static_cast<int32_t>(L.I), s.I,
+                     static_cast<const float*>(W), bias, idx, static_cast<int32_t>(L.I), s.I, s.R,
                      static_cast<int32_t>(L.ip), static_cast<int32_t>(L.io), s.H, ns, s.KW, const_cast<float*>(s.Wc),
                      reinterpret_cast<float*>(w + L.bc), reinterpret_cast<int32_t*>(w + L.rowmap));
   ARD_LAUNCH_CHECK();
@@ -745,7 +755,7 @@ int ard_lstm_fwd(const ard_lstm_desc* desc, const void* X, const void* W, const 
   }
 
   const dim3 sgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((L.G4 + 31) / 32));
-  const bool avec = kw_vec && L.Ic % 4 == 0, bvec = L.B % 4 == 0;
+  const bool avec = kw_vec, bvec = L.B % 4 == 0;  // the recurrent columns start aligned (R)
   // direct loads: aligned rows, and every chunk offset of a slab below 2^31 bytes
   const bool step_fast = avec && bvec && aligned16(s.Wc) &&
                          (L.G4 + 1) * L.KW * 4 < (int64_t{1} << 31) && (L.ns + 64) * L.B * 4 < (int64_t{1} << 31);
@@ -863,7 +873,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
     gr.M = ns;
     gr.N = s.B;
     gr.K = static_cast<int32_t>(L.G4 / fs);
-    gr.a = {s.Wc + L.Ic, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
+    gr.a = {s.Wc + L.R, nullptr, L.KW, nullptr, nullptr, gr.K * L.KW, 0, 1.0f, 0};
     gr.b = {s.dA, nullptr, L.B, nullptr, nullptr, gr.K * L.B, 0, 1.0f, 0};
     gr.c = {part, L.B, nullptr, nullptr, nsB, nullptr, 0, 1.0f};
     rec_fast = fast_ok<true, true>(gr, sizeof(float));
@@ -874,7 +884,7 @@ int ard_lstm_bwd(const ard_lstm_desc* desc, const void* X, const void* dHs, cons
   }
   const dim3 rgrid(static_cast<unsigned>((L.B + 31) / 32), static_cast<unsigned>((ns + 31) / 32),
                    static_cast<unsigned>(splits));
-  const bool vec = L.KW % 4 == 0 && L.Ic % 4 == 0 && L.B % 4 == 0;
+  const bool vec = L.KW % 4 == 0 && L.B % 4 == 0;
   // One fused launch per step where the direct loads can take the operands
   // (aligned rows; chunk offsets of a slab below 2^31 bytes) and the operand
   // stream stays small: 16-wide tiles read each operand twice as often as the
