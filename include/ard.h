@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define ARD_VERSION 2
+#define ARD_VERSION 3
 
 typedef enum {
   ARD_OK = 0,
@@ -255,6 +255,15 @@ typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
  *                             with a strided input side, a full-layout dW
  *                             leaves every 32-byte sector partly written.
  *                             ard_fc_sgd_momentum takes dW in this layout too.
+ *   ARD_WEIGHTS_INPUT_MAJOR : W stored input-major, W^T[K][N] (row k holds
+ *                             the weights of input k to every output), dW
+ *                             likewise dW^T[K][N], V of ard_fc_sgd_momentum
+ *                             too. Every output must be kept (out_plan NULL
+ *                             or of period 1, else ARD_ERR_UNSUPPORTED); a
+ *                             dropped input is then a skipped row, so no
+ *                             compact copy is built or accepted (the compact
+ *                             calls return ARD_ERR_INVALID_ARG). For a last
+ *                             layer, whose outputs carry no pattern.
  * With FULL weights and a gathered input side, fwd and bwd_data build the
  * compact copy in their workspace themselves; a training step that compacts
  * once and passes COMPACT to both saves one pass over W. With an ungathered
@@ -266,7 +275,8 @@ typedef enum { ARD_DROPPED_ZERO = 0, ARD_DROPPED_SKIP = 1 } ard_dropped;
 typedef enum {
   ARD_WEIGHTS_FULL = 0,
   ARD_WEIGHTS_COMPACT = 1,
-  ARD_WEIGHTS_COMPACT_GRAD = 2
+  ARD_WEIGHTS_COMPACT_GRAD = 2,
+  ARD_WEIGHTS_INPUT_MAJOR = 3
 } ard_weight_layout;
 
 typedef struct {
@@ -354,8 +364,9 @@ int ard_fc_bwd(const ard_fc_desc* desc, const void* Xt, const void* dYt, const v
  * and for the kept rows' bias entries the same with Vb, dbias. W is the full
  * [N][K] matrix of the descriptor's dtype, V [N][K] fp32, dW [N][K] fp32, or
  * the compact dWc[kept_out][ldc] when the descriptor's weight_layout is
- * ARD_WEIGHTS_COMPACT_GRAD, bias, Vb, dbias [N] fp32 (all three given or all
- * NULL).
+ * ARD_WEIGHTS_COMPACT_GRAD; with ARD_WEIGHTS_INPUT_MAJOR W, V and dW are all
+ * input-major [K][N] and the kept input rows are updated whole. bias, Vb,
+ * dbias [N] fp32 (all three given or all NULL).
  * Dropped weights, their momentum and their bias entries are left untouched:
  * they are frozen for the step (the reading of an update restricted to the
  * kept rows). All device, caller-owned.

@@ -17,7 +17,7 @@ ARD_F32, ARD_BF16 = 0, 1
 ARD_SEARCH_PLAIN, ARD_SEARCH_MIRROR = 0, 1
 ARD_ACT_NONE, ARD_ACT_RELU = 0, 1
 ARD_DROPPED_ZERO, ARD_DROPPED_SKIP = 0, 1
-ARD_WEIGHTS_FULL, ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_COMPACT_GRAD = 0, 1, 2
+ARD_WEIGHTS_FULL, ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_COMPACT_GRAD, ARD_WEIGHTS_INPUT_MAJOR = 0, 1, 2, 3
 
 
 class ard_search_opts(ctypes.Structure):

@@ -12,7 +12,7 @@ import numpy as np
 from . import _ffi
 from ._ffi import (ARD_ACT_NONE, ARD_ACT_RELU, ARD_BF16, ARD_DROPPED_SKIP, ARD_DROPPED_ZERO,  # noqa: F401
                    ARD_ERR_INVALID_ARG, ARD_ERR_NOT_CONVERGED, ARD_F32, ARD_SEARCH_MIRROR, ARD_SEARCH_PLAIN,
-                   ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_COMPACT_GRAD, ARD_WEIGHTS_FULL,
+                   ARD_WEIGHTS_COMPACT, ARD_WEIGHTS_COMPACT_GRAD, ARD_WEIGHTS_FULL, ARD_WEIGHTS_INPUT_MAJOR,
                    ard_fc_desc, ard_lstm_desc, ard_lstm_tile_desc, ard_row_plan, ard_search_info, ard_search_opts,
                    ard_tile_desc, ard_tile_plan)
 

@@ -210,6 +210,7 @@ struct FcShape {
   bool compact_given;                // W argument is the compact matrix
   bool grad_compact;                 // dW is written as the compact dWc[kout][ldc]
   bool needs_compact;                // fwd / bwd_data gather W through a compact copy
+  bool input_major;                  // W is stored W^T[K][N] (every output kept), dW as dW^T[K][N]
 };
 
 int check_desc(const ard_fc_desc* d, FcShape* s) {
@@ -224,7 +225,7 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   if (d->dropped != ARD_DROPPED_ZERO && d->dropped != ARD_DROPPED_SKIP)
     return fail(ARD_ERR_INVALID_ARG, "unknown dropped-output mode %d", d->dropped);
   if (d->weight_layout != ARD_WEIGHTS_FULL && d->weight_layout != ARD_WEIGHTS_COMPACT &&
-      d->weight_layout != ARD_WEIGHTS_COMPACT_GRAD)
+      d->weight_layout != ARD_WEIGHTS_COMPACT_GRAD && d->weight_layout != ARD_WEIGHTS_INPUT_MAJOR)
     return fail(ARD_ERR_INVALID_ARG, "unknown weight layout %d", d->weight_layout);
   if (!(d->scale == d->scale) || d->scale == __builtin_inff() || d->scale == -__builtin_inff())
     return fail(ARD_ERR_INVALID_ARG, "scale must be finite");
@@ -245,9 +246,13 @@ int check_desc(const ard_fc_desc* d, FcShape* s) {
   s->out_offset = out_all ? 0 : d->out_plan->offset;
   s->esize = d->dtype == ARD_BF16 ? 2 : 4;
   s->ldc = (static_cast<int64_t>(s->kin) + 7) / 8 * 8;
-  s->compact_given = d->weight_layout != ARD_WEIGHTS_FULL;
+  s->compact_given = d->weight_layout == ARD_WEIGHTS_COMPACT || d->weight_layout == ARD_WEIGHTS_COMPACT_GRAD;
   s->grad_compact = d->weight_layout == ARD_WEIGHTS_COMPACT_GRAD;
-  s->needs_compact = !s->compact_given && s->in_period > 1;
+  s->input_major = d->weight_layout == ARD_WEIGHTS_INPUT_MAJOR;
+  // input-major rows are the inputs: the kept ones are whole rows, read in place
+  s->needs_compact = !s->compact_given && !s->input_major && s->in_period > 1;
+  if (s->input_major && !out_all)
+    return fail(ARD_ERR_UNSUPPORTED, "input-major weights need every output kept (out_plan NULL or period 1)");
   return ARD_OK;
 }
 
@@ -365,8 +370,9 @@ GemmOutput strided_out(void* p, int64_t ld, size_t esize, int32_t period, int32_
   return c;
 }
 
-// The view of W used by fwd / bwd_data: either the full matrix's kept output
-// rows (no input gather), or a compact copy (given, or built into ws).
+// The view of W used by fwd / bwd_data: the full matrix's kept output rows (no
+// input gather), a compact copy (given, or built into ws), or the kept input
+// rows of an input-major W^T.
 struct WeightView {
   GemmOperand op;
   float* partial;  // split-K partial sums in ws, or NULL
@@ -377,6 +383,8 @@ int weight_view(const FcShape& s, const void* W, void* ws, hipStream_t stream, W
   char* w = static_cast<char*>(ws);
   if (s.compact_given) {
     v->op = kept_rows(W, nullptr, s.ldc, 1, 0, sizeof(T), 0);
+  } else if (s.input_major) {  // the kept input rows of W^T[K][N]
+    v->op = kept_rows(W, nullptr, s.N, s.in_period, s.in_offset, sizeof(T), 0);
   } else if (s.needs_compact) {
     ARD_HIP_CHECK(launch_compact<T>(s, W, w, stream));
     v->op = kept_rows(w, nullptr, s.ldc, 1, 0, sizeof(T), 0);
@@ -404,7 +412,14 @@ int fc_fwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
                     nullptr);
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok<false, true>(g, sizeof(T))) {
+  if (s.input_major) {  // A(m, k) = W^T[in(k)][m]: m-contiguous
+    if (fast_ok<true, true>(g, sizeof(T))) {
+      ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
+    } else {
+      ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+          g, 1, a_vec, b_vec, stream, wv.partial)));
+    }
+  } else if (fast_ok<false, true>(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, wv.partial)));
   } else {
     ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
@@ -439,15 +454,26 @@ GemmArgs bwd_data_args(const ard_fc_desc* d, const FcShape& s, const void* dYt, 
   return g;
 }
 
-// bwd_weight as a GEMM: dW[S_out][S_in] = G X^T over the batch.
+// bwd_weight as a GEMM: dW[S_out][S_in] = G X^T over the batch (input-major:
+// dW^T[S_in][:] = X G^T).
 template <typename T>
 GemmArgs bwd_weight_args(const ard_fc_desc* d, const FcShape& s, const void* Xt, const void* dYt,
                          const void* Yt, float* dW) {
   GemmArgs g = {};
+  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
+  if (s.input_major) {
+    // dW^T[S_in][n] = X G^T over the batch: whole rows of N outputs
+    g.M = s.kin;
+    g.N = s.N;
+    g.K = s.B;
+    g.a = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
+    g.b = kept_rows(dYt, gated ? Yt : nullptr, s.B, 1, 0, sizeof(T), gated);
+    g.c = strided_out(dW, s.N, sizeof(float), s.in_period, s.in_offset, 1, 0, nullptr, 0, d->scale, nullptr);
+    return g;
+  }
   g.M = s.kout;
   g.N = s.kin;
   g.K = s.B;
-  const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   g.a = kept_rows(dYt, gated ? Yt : nullptr, s.B, s.out_period, s.out_offset, sizeof(T), gated);
   g.b = kept_rows(Xt, nullptr, s.B, s.in_period, s.in_offset, sizeof(T), 0);
   if (s.grad_compact)  // dWc[i][j]: contiguous rows of ldc
@@ -483,6 +509,12 @@ int finish_bwd_weight(const ard_fc_desc* d, const FcShape& s, const void* dYt, c
                        s.out_offset, d->scale, gated ? 1 : 0, vec, dbias);
     ARD_LAUNCH_CHECK();
   }
+  if (d->dropped == ARD_DROPPED_ZERO && s.input_major && s.in_period > 1) {  // the dropped input rows of dW^T
+    hipLaunchKernelGGL(zero_dropped_rows_kernel<float>, dim3(s.K), dim3(256), 0, stream, dW,
+                       static_cast<int64_t>(s.N), s.N, s.in_period, s.in_offset);
+    ARD_LAUNCH_CHECK();
+    return ARD_OK;
+  }
   if (d->dropped == ARD_DROPPED_ZERO && (s.out_period > 1 || s.in_period > 1)) {
     if (!s.grad_compact) {  // a compact gradient has no dropped entries
       hipLaunchKernelGGL(zero_dropped_weights_kernel, dim3(s.N), dim3(256), 0, stream, dW, s.K,
@@ -504,7 +536,17 @@ int run_bwd_data(const ard_fc_desc* d, const FcShape& s, const GemmArgs& g, cons
   const bool gated = d->act == ARD_ACT_RELU && Yt != nullptr;
   const bool a_vec = vec_rows(g.a.ld, sizeof(T));
   const bool b_vec = vec_rows(s.B, sizeof(T));
-  if (fast_ok<true, true>(g, sizeof(T))) {
+  if (s.input_major) {  // A(m, t) = W^T[in(m)][t]: k-contiguous rows
+    if (fast_ok<false, true>(g, sizeof(T))) {
+      ARD_HIP_CHECK((run_fast_gemm<T, false, true, T, EPI_FWD>(g, 1, stream, partial)));
+    } else if (gated) {
+      ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
+          g, 1, a_vec, b_vec, stream, partial)));
+    } else {
+      ARD_HIP_CHECK((run_gemm<T, T, KC_VEC, KC_ELEM, MC_VEC, MC_ELEM, false, false, EPI_FWD>(
+          g, 1, a_vec, b_vec, stream, partial)));
+    }
+  } else if (fast_ok<true, true>(g, sizeof(T))) {
     ARD_HIP_CHECK((run_fast_gemm<T, true, true, T, EPI_FWD>(g, 1, stream, partial)));
   } else if (gated) {
     ARD_HIP_CHECK((run_gemm<T, T, MC_VEC, MC_ELEM, MC_VEC, MC_ELEM, false, true, EPI_FWD>(
@@ -535,7 +577,17 @@ int fc_bwd_weight_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, c
                                                  (s.needs_compact ? al256(compact_bytes(s)) : 0))
                       : nullptr;
   bool dbias_done = false;
-  if (fast_ok<false, false>(g, sizeof(T))) {
+  if (s.input_major) {  // the bias gradient from dbias_kernel (G is the B operand here)
+    if (fast_ok<false, false>(g, sizeof(T))) {
+      ARD_HIP_CHECK((run_fast_gemm<T, false, false, float, EPI_FWD>(g, 1, stream, partial)));
+    } else if (gated) {
+      ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, true, EPI_FWD>(
+          g, 1, v, v, stream, partial)));
+    } else {
+      ARD_HIP_CHECK((run_gemm<T, float, KC_VEC, KC_ELEM, KC_VEC, KC_ELEM, false, false, EPI_FWD>(
+          g, 1, v, v, stream, partial)));
+    }
+  } else if (fast_ok<false, false>(g, sizeof(T))) {
     // dbias = scale * G 1: the row sums of A, taken by the same kernel
     if (dbias) {
       g.rsum = dbias + s.out_offset;
@@ -566,7 +618,8 @@ int fc_bwd_impl(const ard_fc_desc* d, const FcShape& s, const void* Xt, const vo
   if (st != ARD_OK) return st;
   const GemmArgs gd = bwd_data_args<T>(d, s, dYt, Yt, wv.op, dXt, Xgate);
   GemmArgs gw = bwd_weight_args<T>(d, s, Xt, dYt, Yt, dW);
-  if (fast_ok<true, true>(gd, sizeof(T)) && fast_ok<false, false>(gw, sizeof(T)) && fast_pair_ok<T>(gd, gw)) {
+  if (!s.input_major && fast_ok<true, true>(gd, sizeof(T)) && fast_ok<false, false>(gw, sizeof(T)) &&
+      fast_pair_ok<T>(gd, gw)) {
     if (dbias) {
       gw.rsum = dbias + s.out_offset;
       gw.rsum_ld = s.out_period;
@@ -684,6 +737,7 @@ int ard_fc_compact_weights(const ard_fc_desc* desc, const void* W, void* Wc, voi
   FcShape s;
   int st = check_desc(desc, &s);
   if (st != ARD_OK) return st;
+  if (s.input_major) return fail(ARD_ERR_INVALID_ARG, "input-major weights have no compact copy");
   if ((st = check_ptr(W, "W")) || (st = check_ptr(Wc, "Wc"))) return st;
   hipStream_t sm = static_cast<hipStream_t>(stream);
   if (desc->dtype == ARD_BF16) {
@@ -708,6 +762,7 @@ int ard_fc_compact_weights_batch(int32_t count, const ard_fc_desc* const* descs,
     int st = check_desc(descs[q], &s);
     if (st != ARD_OK) return st;
     if (descs[q]->dtype != dtype) return fail(ARD_ERR_INVALID_ARG, "descs[%d]: dtypes differ", q);
+    if (s.input_major) return fail(ARD_ERR_INVALID_ARG, "descs[%d]: input-major weights have no compact copy", q);
     if ((st = check_ptr(W[q], "W")) || (st = check_ptr(Wc[q], "Wc"))) return st;
     jf.job[q] = compact_job<float>(s, W[q], Wc[q]);
     jb.job[q] = compact_job<bf16>(s, W[q], Wc[q]);
@@ -737,6 +792,27 @@ int ard_fc_sgd_momentum(const ard_fc_desc* desc, void* W, float* V, const float*
   if (!(lr == lr) || !(momentum == momentum)) return fail(ARD_ERR_INVALID_ARG, "lr and momentum must be numbers");
   if (s.kout == 0) return ARD_OK;
   hipStream_t sm = static_cast<hipStream_t>(stream);
+  if (s.input_major) {
+    // the kept input rows of W^T, V^T and dW^T, whole (every output kept);
+    // the bias of every output as one more row
+    if (s.kin > 0) {
+      if (desc->dtype == ARD_BF16)
+        hipLaunchKernelGGL(sgd_momentum_kernel<bf16>, dim3(s.kin), dim3(256), 0, sm, static_cast<bf16*>(W), V, dW,
+                           s.N, int64_t{0}, s.in_period, s.in_offset, 1, 0, s.N, nullptr, nullptr, nullptr, lr,
+                           momentum);
+      else
+        hipLaunchKernelGGL(sgd_momentum_kernel<float>, dim3(s.kin), dim3(256), 0, sm, static_cast<float*>(W), V,
+                           dW, s.N, int64_t{0}, s.in_period, s.in_offset, 1, 0, s.N, nullptr, nullptr, nullptr, lr,
+                           momentum);
+      ARD_LAUNCH_CHECK();
+    }
+    if (bias) {
+      hipLaunchKernelGGL(sgd_momentum_kernel<float>, dim3(1), dim3(256), 0, sm, bias, Vb, dbias, s.N, int64_t{0}, 1,
+                         0, 1, 0, s.N, nullptr, nullptr, nullptr, lr, momentum);
+      ARD_LAUNCH_CHECK();
+    }
+    return ARD_OK;
+  }
   const int64_t ldg = s.grad_compact ? s.ldc : 0;
   if (desc->dtype == ARD_BF16)
     hipLaunchKernelGGL(sgd_momentum_kernel<bf16>, dim3(s.kout), dim3(256), 0, sm, static_cast<bf16*>(W), V, dW, s.K,

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert api.ard_version() == 2
+    assert api.ard_version() == 3
     assert api.ard_status_string(0) == "ARD_OK"
     assert api.ard_status_string(4) == "ARD_ERR_NOT_CONVERGED"
 

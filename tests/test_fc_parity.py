@@ -192,6 +192,79 @@ def test_random_shapes_and_patterns(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape,pin", [((64, 96, 520), (3, 1)), ((200, 1000, 260), (2, 0)), ((128, 2048, 1024), (7, 4)),
+                                       ((8, 130, 70), (1, 0)), ((256, 600, 2048), (16, 15))])
+def test_input_major_weights(dtype, shape, pin):
+    """A last layer (every output kept) with W stored input-major, W^T[K][N]:
+    fwd, bwd_data, bwd_weight (dW^T), the one-call backward and the momentum
+    update against the oracle on W, in both dropped modes; dropped input rows
+    of dW^T keep a sentinel in SKIP mode and are 0 in ZERO mode."""
+    B, K, N = shape
+    X, W, b, dY = make_inputs(dtype, B, K, N, seed=sum(shape) + pin[0])
+    m_in = opat.row_mask(K, *pin)
+    m_out = np.ones(N)
+    in_plan = row_plan(K, *pin, with_list=False) if pin != (1, 0) else None
+    Y64 = ofc.fc_forward(f64(X), f64(W), f64(b), m_in, m_out, 1.25, "relu")
+    Ys = synth.to_storage(torch.from_numpy(Y64).float(), dtype)
+    dX64, dW64, db64 = ofc.fc_backward(f64(X), f64(W), f64(Ys), f64(dY), m_in, m_out, 1.25, "relu")
+    Xa, Wa = np.abs(f64(X) * m_in[None, :]), np.abs(f64(W))
+    G = ofc.fc_output_grad(f64(Ys), f64(dY), m_out, 1.25, "relu")
+    t = tol(dtype)
+    Xt, WTd, dYt, Yst = to_dev(X.T), to_dev(W.T.contiguous()), to_dev(dY.T), to_dev(Ys.T)
+    sdt = synth.storage_dtype(dtype)
+    for dropped, fill in ((api.ARD_DROPPED_SKIP, -3.25), (api.ARD_DROPPED_ZERO, 0.0)):
+        desc = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, None, 1.25, api.ARD_ACT_RELU, dropped,
+                           api.ARD_WEIGHTS_INPUT_MAJOR)
+        ws = workspace(api.ard_fc_workspace_bytes(desc))
+        Yt = torch.full((N, B), 9.0, dtype=sdt, device=device())
+        dXt = torch.full((K, B), fill, dtype=sdt, device=device())
+        dWT = torch.full((K, N), fill, dtype=torch.float32, device=device())
+        db = torch.full((N,), fill, dtype=torch.float32, device=device())
+        api.ard_fc_fwd(desc, Xt, WTd, to_dev(b), Yt, ws)
+        api.ard_fc_bwd_data(desc, dYt, Yst, WTd, dXt, ws)
+        api.ard_fc_bwd_weight(desc, Xt, dYt, Yst, dWT, db, ws)
+        dXt2, dWT2, db2 = (torch.full_like(x, fill) for x in (dXt, dWT, db))
+        api.ard_fc_bwd(desc, Xt, dYt, Yst, WTd, dXt2, dWT2, db2, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(dXt2, dXt) and torch.equal(dWT2, dWT) and torch.equal(db2, db)
+        compare(f64(Yt).T, Y64, 1.25 * (Xa @ Wa.T + np.abs(f64(b))[None, :]), t, "Y")
+        keep = m_in > 0
+        got_dX, got_dW = f64(dXt).T, f64(dWT).T
+        compare(got_dX[:, keep], dX64[:, keep], 1.25 * (np.abs(G) @ Wa)[:, keep], t, "dX")
+        compare(got_dW[:, keep], dW64[:, keep], 1.25 * (np.abs(G).T @ Xa)[:, keep], t, "dW")
+        compare(f64(db), db64, 1.25 * np.abs(G).sum(0), t, "db")
+        assert (got_dX[:, ~keep] == fill).all() and (got_dW[:, ~keep] == fill).all(), "dropped inputs"
+        if dropped == api.ARD_DROPPED_SKIP:
+            # the momentum update on the kept input rows of W^T (all outputs)
+            V = torch.full((K, N), 0.5, device=device())
+            Vb = torch.full((N,), 0.25, device=device())
+            bias = to_dev(b)
+            W0, V0, bias0, Vb0 = WTd.clone(), V.clone(), bias.clone(), Vb.clone()
+            api.ard_fc_sgd_momentum(desc, WTd, V, dWT, bias, Vb, db, 0.01, 0.9)
+            torch.cuda.synchronize()
+            Wn, Vn, bn, Vbn = ofc.sgd_momentum(f64(W0).T, f64(V0).T, f64(dWT).T, m_out, m_in, 0.01, 0.9,
+                                               f64(bias0), f64(Vb0), f64(db))
+            kw = np.outer(m_out, m_in) > 0
+            compare(f64(V).T[kw], Vn[kw], (0.9 * np.abs(f64(V0).T) + np.abs(f64(dWT).T) + 1.0)[kw], F32_TOL_UPD,
+                    "V")
+            compare(f64(WTd).T[kw], Wn[kw], (np.abs(Wn) + 0.01 * np.abs(Vn) + 1e-3)[kw], t, "W")
+            compare(f64(Vb), Vbn, 0.9 * np.abs(f64(Vb0)) + np.abs(f64(db)) + 1.0, F32_TOL_UPD, "Vb")
+            compare(f64(bias), bn, np.abs(bn) + 0.01 * np.abs(Vbn) + 1e-3, F32_TOL_UPD, "b")
+            assert np.array_equal(f64(WTd).T[~kw], f64(W0).T[~kw]) and np.array_equal(f64(V).T[~kw], f64(V0).T[~kw])
+            WTd.copy_(W0)
+    # an output pattern cannot be read from input-major rows; no compact copy exists
+    bad = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, row_plan(N, 2, 1, with_list=False), 1.0,
+                      api.ARD_ACT_NONE, api.ARD_DROPPED_SKIP, api.ARD_WEIGHTS_INPUT_MAJOR)
+    with pytest.raises(RuntimeError, match="UNSUPPORTED|every output"):
+        api.ard_fc_fwd(bad, Xt, WTd, None, torch.empty((N, B), dtype=sdt, device=device()),
+                       workspace(1 << 20))
+    good = api.fc_desc(ard_dtype(dtype), B, K, N, in_plan, None, 1.0, api.ARD_ACT_NONE, api.ARD_DROPPED_SKIP,
+                       api.ARD_WEIGHTS_INPUT_MAJOR)
+    with pytest.raises(RuntimeError, match="compact"):
+        api.ard_fc_compact_weights(good, WTd, torch.empty(K * N, dtype=sdt, device=device()))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_skip_mode_leaves_dropped_entries_untouched(dtype):
     X, W, b, dY = make_inputs(dtype, 96, 160, 144, seed=7)
     run_layer(dtype, X, W, b, dY, (3, 0), (2, 1), "relu", 2.0, api.ARD_DROPPED_SKIP, sentinel=-7.5)
@@ -248,7 +321,7 @@ def test_invalid_arguments_are_rejected_before_launch():
         api.ard_fc_fwd(big_k, Xk, Wk, None, Y)
     assert e.value.status == 5
     with pytest.raises(api.ArdError):
-        api.ard_fc_fwd(api.fc_desc(api.ARD_F32, 8, 16, 8, weight_layout=3), X, W, None, Y)
+        api.ard_fc_fwd(api.fc_desc(api.ARD_F32, 8, 16, 8, weight_layout=7), X, W, None, Y)
     with pytest.raises(api.ArdError):
         api.ard_fc_fwd(good, X[:, 1:].contiguous().view(-1)[1:], W, None, Y)  # misaligned
     relu = api.fc_desc(api.ARD_F32, 8, 16, 8, act=api.ARD_ACT_RELU)
