@@ -39,9 +39,13 @@ PATTERN_SEED = 8939
 
 class Mlp:
     """An MLP whose hidden layers take row-based dropout patterns sampled per
-    step from K(p). Layers are FC: Xt[K][B] -> Yt[N][B]."""
+    step from K(p). Layers are FC: Xt[K][B] -> Yt[N][B]. With
+    last_input_major the last layer, whose outputs carry no pattern, stores its
+    weights (and their gradient and momentum) input-major, W^T[K][N]: its kept
+    inputs are then whole rows, read in place, and no step compacts it."""
 
-    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False, dropped="skip", streams=1):
+    def __init__(self, name, dims, batch, dtype, init, seed, relu_last=False, dropped="skip", streams=1,
+                 last_input_major=False):
         import torch
         from paper_1805_08939_amd import api, synth
         self.api, self.torch = api, torch
@@ -53,22 +57,26 @@ class Mlp:
         L = len(dims) - 1
         self.L = L
         self.X0 = synth.to_storage(synth.normal(g, (dims[0], batch)), dtype).to(dev)
+        self.input_major = [last_input_major and l == L - 1 for l in range(L)]
         self.W = []
         for l in range(L):
             w = synth.xavier(g, dims[l + 1], dims[l]) if init == "xavier" else synth.he(g, dims[l + 1], dims[l])
-            self.W.append(synth.to_storage(w, dtype).to(dev))
+            w = synth.to_storage(w, dtype).to(dev)
+            self.W.append(w.t().contiguous() if self.input_major[l] else w)
         self.bias = [torch.zeros(dims[l + 1], device=dev) for l in range(L)]
         self.Y = [torch.zeros(dims[l + 1], batch, dtype=sdt, device=dev) for l in range(L)]
         self.dY = [torch.zeros(dims[l + 1], batch, dtype=sdt, device=dev) for l in range(L)]
         self.dY[-1].copy_(synth.to_storage(synth.normal(g, (dims[-1], batch)), dtype).to(dev))
-        self.dW = [torch.zeros(dims[l + 1], dims[l], device=dev) for l in range(L)]
+        self.dW = [torch.zeros(*((dims[l], dims[l + 1]) if self.input_major[l] else (dims[l + 1], dims[l])),
+                               device=dev) for l in range(L)]
         self.db = [torch.zeros(dims[l + 1], device=dev) for l in range(L)]
         self.plans = [api.ard_row_plan() for _ in range(L - 1)]
         # compact weights of the layers whose inputs are dropped (built once per
         # step, shared by fwd and bwd_data) and one workspace for split-K sums:
         # at most two rounds of 256 output tiles of 256 x 256 fp32
-        self.Wc = [None] + [torch.zeros(dims[l + 1] * ((dims[l] + 7) // 8 * 8), dtype=sdt, device=dev)
-                            for l in range(1, L)]
+        self.comp_layers = [l for l in range(1, L) if not self.input_major[l]]
+        self.Wc = [torch.zeros(dims[l + 1] * ((dims[l] + 7) // 8 * 8), dtype=sdt, device=dev)
+                   if l in self.comp_layers else None for l in range(L)]
         self.ws = torch.empty(2 * 256 * 256 * 256, dtype=torch.float32, device=dev)
         # streams == 2: the step runs the compaction and the weight-gradient
         # products of the hidden layers on a second stream (same priority),
@@ -88,7 +96,8 @@ class Mlp:
         self.stream = torch.cuda.current_stream().cuda_stream
         self.ptr = {
             "X0": self.X0.data_ptr(), "W": [w.data_ptr() for w in self.W],
-            "Wc": [None] + [w.data_ptr() for w in self.Wc[1:]], "bias": [b.data_ptr() for b in self.bias],
+            "Wc": [w.data_ptr() if w is not None else None for w in self.Wc],
+            "bias": [b.data_ptr() for b in self.bias],
             "Y": [y.data_ptr() for y in self.Y], "dY": [d.data_ptr() for d in self.dY],
             "dW": [w.data_ptr() for w in self.dW], "db": [b.data_ptr() for b in self.db]}
 
@@ -104,6 +113,10 @@ class Mlp:
             act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
             args = (self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], in_plan, out_plan, 1.0, act,
                     self.dropped)
+            if self.input_major[l]:
+                self.descs.append(api.fc_desc(*args, api.ARD_WEIGHTS_INPUT_MAJOR))
+                self.cdescs.append(self.descs[-1])
+                continue
             self.descs.append(api.fc_desc(*args))
             # a layer whose inputs are dropped reads the compact weights and
             # writes the compact weight gradient dWc[kept_out][ldc] into dW
@@ -132,8 +145,8 @@ class Mlp:
                                                                     P["db"][l], ws, st), {})
             return calls
 
-        self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l > 0 else None}
-                            for l in range(self.L)]
+        self.layer_calls = [{False: layer_calls(l, False), True: layer_calls(l, True) if l in self.comp_layers
+                             else None} for l in range(self.L)]
 
         def split_calls(l, compact):
             """The layer's products as separate calls: fwd and bwd_data on the
@@ -152,14 +165,14 @@ class Mlp:
             return calls
 
         if self.streams == 2:
-            self.split_calls = [{False: split_calls(l, False), True: split_calls(l, True) if l > 0 else None}
-                                for l in range(self.L)]
+            self.split_calls = [{False: split_calls(l, False), True: split_calls(l, True) if l in self.comp_layers
+                                 else None} for l in range(self.L)]
         # one compaction launch per step for the layers whose inputs are
         # dropped: the marshalled arguments of every subset, built once
         import itertools
         self.compact_batches = {}
-        for r in range(1, self.L):
-            for sub in itertools.combinations(range(1, self.L), r):
+        for r in range(1, len(self.comp_layers) + 1):
+            for sub in itertools.combinations(self.comp_layers, r):
                 self.compact_batches[sub] = api.CompactBatch([self.cdescs[l] for l in sub],
                                                              [P["W"][l] for l in sub], [P["Wc"][l] for l in sub])
         self.order = [("fwd", l) for l in range(self.L)]
@@ -184,8 +197,9 @@ class Mlp:
         self.dense = []
         for l in range(self.L):
             act = api.ARD_ACT_RELU if l < self.L - 1 else api.ARD_ACT_NONE
+            layout = api.ARD_WEIGHTS_INPUT_MAJOR if self.input_major[l] else api.ARD_WEIGHTS_FULL
             self.dense.append(api.fc_desc(self.ard_dtype, self.B, self.dims[l], self.dims[l + 1], None, None, 1.0, act,
-                                          api.ARD_DROPPED_SKIP))
+                                          api.ARD_DROPPED_SKIP, layout))
 
     def sgd_step(self, dense):
         """Momentum SGD on every layer (lr 1e-6, momentum 0.9; the cost does not
@@ -268,7 +282,7 @@ class Mlp:
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, None, st, plan=self.plans[l])
         calls = dict(self.layer_calls[0][False])
-        sub = tuple(l for l in range(1, self.L) if pats[l - 1][0] > 1)
+        sub = tuple(l for l in self.comp_layers if pats[l - 1][0] > 1)
         self.step_compact = sub  # layers whose dW holds the compact gradient this step
         if sub:
             api.ard_fc_compact_weights_batch(self.compact_batches[sub], st)
@@ -290,7 +304,7 @@ class Mlp:
         pats = self.patterns(it)
         for l, (per, off) in enumerate(pats):
             api.ard_plan_rows(self.dims[l + 1], per, off, None, st, plan=self.plans[l])
-        sub = tuple(l for l in range(1, self.L) if pats[l - 1][0] > 1)
+        sub = tuple(l for l in self.comp_layers if pats[l - 1][0] > 1)
         self.step_compact = sub
         calls = [self.split_calls[l][l in sub] for l in range(self.L)]
 
@@ -369,9 +383,13 @@ class Mlp:
             dY = dX
         return np.abs(dW).sum()
 
+    def full_weight(self, l):
+        """Layer l's weights as W[N][K] (a view of the stored tensor)."""
+        return self.W[l].t() if self.input_major[l] else self.W[l]
+
     def host_copies(self):
         self._host = {"X0": self.X0.double().cpu().numpy().T.copy(),
-                      "W": [w.double().cpu().numpy() for w in self.W],
+                      "W": [self.full_weight(l).double().cpu().numpy() for l in range(self.L)],
                       "dY": self.dY[-1].double().cpu().numpy().T.copy()}
 
 
@@ -909,7 +927,7 @@ WORKLOADS = {
     "lstm1024tile": dict(cls="LstmTile", name="lstm-t35-b64-i1024-h1024-fp32-tile64", T=35, batch=64, inputs=1024,
                          hidden=1024, tile=64, dtype="f32", seed=1805 + 3),
     "mlp8192": dict(cls="Mlp", name="mlp-8192x4-bf16-b2048", dims=[8192, 8192, 8192, 8192], batch=2048,
-                    dtype="bf16", init="he", seed=1805 + 4, streams=2),
+                    dtype="bf16", init="he", seed=1805 + 4, streams=2, last_input_major=True),
 }
 
 

@@ -79,7 +79,10 @@ def full_weight_grad(mlp, l, pats, fill):
     """Layer l's weight gradient after a step of the benchmark's MLP, as a
     full [N][K] fp64 array: a layer whose inputs were dropped that step wrote
     the compact gradient dWc[kept_out][ldc] into its dW buffer; its entries are
-    placed at [S_out][S_in] and every other entry gets fill."""
+    placed at [S_out][S_in] and every other entry gets fill. An input-major
+    layer's buffer holds dW^T[K][N], returned transposed."""
+    if getattr(mlp, "input_major", None) and mlp.input_major[l]:  # dW^T[K][N]
+        return mlp.dW[l].t().double().cpu().numpy()
     dW = mlp.dW[l].double().cpu().numpy()
     if l not in mlp.step_compact:
         return dW

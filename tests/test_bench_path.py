@@ -54,7 +54,7 @@ def test_mlp784_step_against_oracle(mlp, p):
         masks = [np.ones(dims[0])] + [opat.row_mask(dims[l + 1], *pats[l]) for l in range(L - 1)] + \
                 [np.ones(dims[-1])]
         acts = [_host(mlp.X0)] + [_host(y) for y in mlp.Y]
-        W = [w.double().cpu().numpy() for w in mlp.W]
+        W = [mlp.full_weight(l).double().cpu().numpy() for l in range(mlp.L)]
         for l in range(L):
             act = "relu" if l < L - 1 else "none"
             m_in, m_out = masks[l], masks[l + 1]

@@ -62,7 +62,8 @@ def check_mlp_step(mlp, it, tol):
         keep_in = m_in > 0
         X = _host(mlp.X0) if l == 0 else _host(mlp.Y[l - 1])
         Xm = np.where(keep_in[None, :], X, 0.0)  # dropped input rows hold NaN: never read
-        W = mlp.W[l][torch.from_numpy(Sout).to(mlp.W[l].device)].double().cpu().numpy()
+        Wl = mlp.full_weight(l)
+        W = Wl[torch.from_numpy(Sout).to(Wl.device)].double().cpu().numpy()
         ones = np.ones(len(Sout))
         # forward on the kept outputs: the oracle layer with those rows of W
         want = ofc.fc_forward(Xm, W, None, m_in, ones, 1.0, act)
