@@ -15,14 +15,16 @@ pytestmark = pytest.mark.gpu
 SCRATCH_BYTES = 32 << 20
 
 
-def layer(dtype, B, K, N, pin, pout, seed):
+def layer(dtype, B, K, N, pin, pout, seed, layout=api.ARD_WEIGHTS_FULL):
     g = synth.generator(seed)
     X = synth.to_storage(synth.normal(g, (B, K)), dtype)
     W = synth.to_storage(synth.normal(g, (N, K), 0.05), dtype)
     b = synth.normal(g, (N,), 0.1)
     desc = api.fc_desc(api.ARD_F32 if dtype == "f32" else api.ARD_BF16, B, K, N,
                        row_plan(K, *pin, with_list=False), row_plan(N, *pout, with_list=False), 1.25,
-                       api.ARD_ACT_RELU, api.ARD_DROPPED_ZERO)
+                       api.ARD_ACT_RELU, api.ARD_DROPPED_ZERO, layout)
+    if layout == api.ARD_WEIGHTS_INPUT_MAJOR:
+        W = W.T.contiguous()
     return desc, to_dev(X.T), to_dev(W), to_dev(b), synth.storage_dtype(dtype)
 
 
@@ -34,11 +36,14 @@ def test_noalloc_forward_matches_workspace_forward():
         # a smaller layer next: a tiny output grid whose contraction is split,
         # partial sums in the scratch
         ("f32", 8, 4096, 8, (1, 0), (1, 0)),
+        # input-major weights (a last layer): the kept inputs are read in place
+        ("bf16", 64, 4096, 1024, (2, 1), (1, 0), api.ARD_WEIGHTS_INPUT_MAJOR),
     ]
-    for i, (dtype, B, K, N, pin, pout) in enumerate(cases):
-        desc, Xt, W, b, sdt = layer(dtype, B, K, N, pin, pout, seed=100 + i)
+    for i, (dtype, B, K, N, pin, pout, *layout) in enumerate(cases):
+        desc, Xt, W, b, sdt = layer(dtype, B, K, N, pin, pout, seed=100 + i, layout=layout[0] if layout else
+                                    api.ARD_WEIGHTS_FULL)
         need = api.ard_fc_workspace_bytes(desc)
-        assert 0 < need <= SCRATCH_BYTES
+        assert need <= SCRATCH_BYTES and (need > 0 or layout)
         ref = torch.full((N, B), 3.0, dtype=sdt, device=device())
         got = torch.full((N, B), -3.0, dtype=sdt, device=device())
         api.ard_fc_fwd(desc, Xt, W, b, ref, workspace(need))
