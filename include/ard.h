@@ -422,6 +422,15 @@ int ard_tile_bwd_data(const ard_tile_desc* desc, const ard_tile_plan* plan, cons
                       const void* W, void* dXt, void* stream);
 int ard_tile_bwd_weight(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt,
                         const void* dYt, float* dW, void* stream);
+/*
+ * The layer's backward in one call: ard_tile_bwd_data and
+ * ard_tile_bwd_weight on the same arguments, with the same results bit for
+ * bit. Where both products take the direct-load kernels they run as one
+ * launch, the weight-gradient work starting on each compute unit as soon as
+ * its bwd_data tile is done; otherwise the two calls one after the other.
+ */
+int ard_tile_bwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt, const void* dYt,
+                 const void* W, void* dXt, float* dW, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* LSTM layer with hidden-unit row pattern fixed per sequence (device).     */

@@ -112,6 +112,8 @@ SIGNATURES = {
                                          c_vp, c_vp, c_vp, c_vp]),
     "ard_tile_bwd_weight": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
                                            c_vp, c_vp, c_vp, c_vp]),
+    "ard_tile_bwd": (ctypes.c_int, [ctypes.POINTER(ard_tile_desc), ctypes.POINTER(ard_tile_plan),
+                                    c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "ard_lstm_workspace_bytes": (c_size, [ctypes.POINTER(ard_lstm_desc)]),
     "ard_lstm_tile_workspace_bytes": (c_size, [ctypes.POINTER(ard_lstm_tile_desc)]),
     "ard_lstm_tile_fwd": (ctypes.c_int, [ctypes.POINTER(ard_lstm_tile_desc), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,

@@ -287,6 +287,12 @@ def ard_tile_bwd_weight(desc, plan, Xt, dYt, dW, stream=None):
                                           _ptr(dW), _stream(stream)))
 
 
+def ard_tile_bwd(desc, plan, Xt, dYt, W, dXt, dW, stream=None):
+    """ard_tile_bwd_data and ard_tile_bwd_weight in one call (one launch on the fast path)."""
+    _check(_ffi.lib().ard_tile_bwd(ctypes.byref(desc), ctypes.byref(plan), _ptr(Xt), _ptr(dYt), _ptr(W),
+                                   _ptr(dXt), _ptr(dW), _stream(stream)))
+
+
 # --------------------------------------------------------------------------- LSTM layer
 
 def lstm_desc(dtype, seq_len, batch, input_size, hidden_size, hidden_plan=None, input_plan=None):

@@ -606,20 +606,20 @@ constexpr int kFastTile = 64;
 // fwd:       Yt[tn block][n0 ..] = scale * sum over kept tk of row tn: W(tn, tk) Xt[tk block][n0 ..]
 // bwd_data:  dXt[tk block][n0 ..] = scale * sum over kept tn of column tk: W(tn, tk)^T dYt[tn block][n0 ..]
 // A tile row (column) without kept tiles gets zeros.
+// One workgroup of the fwd / bwd_data product: position bid of the grid of
+// nx x ny (batch block, tile row or column), split sp.
 template <class Cfg, int PASS, typename OutT>
-__global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
+__device__ __forceinline__ void tdp_rows_tile(const TdpFastArgs& a, int bid, int sp, char* smem) {
   constexpr int TT = kFastTile, ES = Cfg::ES, SPT = TT / Cfg::BK;
   constexpr bool AMC = PASS == TDP_BWD_DATA;
   static_assert(Cfg::BM == TT && TT % Cfg::BK == 0, "one tile row per workgroup");
-  extern __shared__ __attribute__((aligned(16))) char smem[];
   const int wave = threadIdx.x >> 6;
   const int ks = wave / (Cfg::WGM * Cfg::WGN), wmn = wave % (Cfg::WGM * Cfg::WGN);
   const int wm = wmn / Cfg::WGN, wn = wmn % Cfg::WGN;
   int own, col;
-  grouped_tile(blockIdx.x, a.nx, a.ny, own, col);
+  grouped_tile(bid, a.nx, a.ny, own, col);
   const int n0 = col * Cfg::BN;
   const int splits = a.splits > 1 ? a.splits : 1;
-  const int sp = splits > 1 ? static_cast<int>(blockIdx.y) : 0;
   const int pa = __builtin_amdgcn_readfirstlane(a.ptr[own]);
   const int nall = __builtin_amdgcn_readfirstlane(a.ptr[own + 1]) - pa;
   const int p0 = pa + nall * sp / splits;  // this split's share of the list
@@ -708,6 +708,13 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
   fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, n0, wm, wn, 0, 0, smem);
 }
 
+template <class Cfg, int PASS, typename OutT>
+__global__ void __launch_bounds__(Cfg::NT) tdp_fast_kernel(TdpFastArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  tdp_rows_tile<Cfg, PASS, OutT>(a, static_cast<int>(blockIdx.x), a.splits > 1 ? static_cast<int>(blockIdx.y) : 0,
+                                 smem);
+}
+
 // out[e] = scale * sum over the splits of partial[split][e], in split order
 // (the loads of up to eight splits issued together).
 __global__ void __launch_bounds__(256) tdp_split_reduce_kernel(const float* __restrict__ partial, int32_t splits,
@@ -731,21 +738,22 @@ __global__ void __launch_bounds__(256) tdp_split_reduce_kernel(const float* __re
 // wave column wn computes the group's tile wn. Each workgroup takes the groups
 // t, t + gridDim.x, ... of the list (t its position in the XCD-aware order),
 // so the grid can stay at what the chip holds at once.
+// Workgroup bid of nw walking the weight-gradient groups bid', bid' + nw, ...
+// (bid' its position in the XCD-aware order).
 template <class Cfg, typename OutT>
-__global__ void __launch_bounds__(Cfg::NT) tdp_fast_dw_kernel(TdpFastArgs a) {
+__device__ __forceinline__ void tdp_dw_walk(const TdpFastArgs& a, int bid, int nw, char* smem) {
   constexpr int TT = kFastTile, ES = Cfg::ES;
   static_assert(Cfg::BM == TT && Cfg::TN == TT && Cfg::BN == TT * kTdpChunk && Cfg::KSPLIT == 1,
                 "one kept tile per wave column");
-  extern __shared__ __attribute__((aligned(16))) char smem[];
   int unused, c0;
-  grouped_tile(blockIdx.x, gridDim.x, 1, unused, c0);
+  grouped_tile(bid, nw, 1, unused, c0);
   const int count = __builtin_amdgcn_readfirstlane(a.chunks[0]);
   const int wave = threadIdx.x >> 6;
   const int wm = wave / Cfg::WGN, wn = wave % Cfg::WGN;
   const int64_t B = a.B, K = a.K;
   const int nslab = (a.B + Cfg::BK - 1) / Cfg::BK;
 
-  for (int c = c0; c < count; c += gridDim.x) {
+  for (int c = c0; c < count; c += nw) {
     const int32_t* rec = a.chunks + 4 + static_cast<int64_t>(c) * kTdpRec;
     const int tn = __builtin_amdgcn_readfirstlane(rec[0]);
     const int cnt = __builtin_amdgcn_readfirstlane(rec[2]);
@@ -790,6 +798,30 @@ __global__ void __launch_bounds__(Cfg::NT) tdp_fast_dw_kernel(TdpFastArgs a) {
     fast_store<OutT, Cfg, EPI_FWD>(g, acc, 0, 0, wm, wn, 0, 0, smem);
     lds_barrier();  // the next group's loads overwrite the epilogue's staging
   }
+}
+
+template <class Cfg, typename OutT>
+__global__ void __launch_bounds__(Cfg::NT) tdp_fast_dw_kernel(TdpFastArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  tdp_dw_walk<Cfg, OutT>(a, static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), smem);
+}
+
+// The layer's backward in one launch: workgroups 0 .. nd - 1 run bwd_data
+// (one per tile column and batch block), the nw after them walk the
+// weight-gradient groups. A compute unit that finishes its bwd_data tile
+// takes up weight-gradient work at once, with no kernel boundary between the
+// two products; every output is computed by the same code as in the separate
+// kernels, so the results are theirs bit for bit.
+template <class CfgD, class CfgW, typename T>
+__global__ void __launch_bounds__(CfgD::NT) tdp_fast_bwd_kernel(TdpFastArgs d, TdpFastArgs w, int32_t nd,
+                                                                int32_t nw) {
+  static_assert(CfgD::NT == CfgW::NT, "one block size");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < nd)
+    tdp_rows_tile<CfgD, TDP_BWD_DATA, T>(d, b, 0, smem);
+  else
+    tdp_dw_walk<CfgW, float>(w, b - nd, nw, smem);
 }
 
 // ZERO mode: clears every dropped tile of dW.
@@ -924,6 +956,41 @@ hipError_t run_tdp_fast(int pass, const TdpArgs& a, const int32_t* chunks, int o
     if (a.B <= C::Narrow::BN) return launch_rows<typename C::Narrow, T>(pass, f, owners, 1, s);
   }
   return launch_rows<typename C::Rows, T>(pass, f, owners, 1, s);
+}
+
+// bwd_data and bwd_weight as one launch of tdp_fast_bwd_kernel (both on the
+// fast path): the bwd_data workgroups first, then the weight-gradient walkers.
+template <class CfgD, typename T>
+hipError_t launch_tdp_fast_bwd(const TdpArgs& ad, const TdpArgs& aw, const int32_t* chunks, int tiles_n,
+                               int tiles_k, int nnz, hipStream_t s) {
+  using CfgW = typename TdpFastCfgs<T>::Group;
+  constexpr int LDS = CfgD::LDS > CfgW::LDS ? CfgD::LDS : CfgW::LDS;
+  auto kern = tdp_fast_bwd_kernel<CfgD, CfgW, T>;
+  static const hipError_t attr =
+      hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+  if (attr != hipSuccess) return attr;
+  TdpFastArgs d = {ad.act, nullptr, ad.W, ad.out, ad.B, ad.K, 0, 0, ad.ptr, ad.list, chunks, ad.scale};
+  d.nx = (d.B + CfgD::BN - 1) / CfgD::BN;
+  d.ny = tiles_k;
+  TdpFastArgs w = {aw.act, aw.act2, aw.W, aw.out, aw.B, aw.K, 0, 0, aw.ptr, aw.list, chunks, aw.scale};
+  const int64_t rows = tiles_n < nnz ? tiles_n : nnz;
+  int64_t nw = nnz > 0 ? (nnz + (kTdpChunk - 1) * rows) / kTdpChunk
+                       : nnz == 0 ? 0 : static_cast<int64_t>(tiles_n) * ((tiles_k + kTdpChunk - 1) / kTdpChunk);
+  if (nw > kTargetBlocks) nw = kTargetBlocks;
+  const int64_t nd = static_cast<int64_t>(d.nx) * d.ny;
+  hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(nd + nw)), dim3(CfgD::NT), LDS, s, d, w,
+                     static_cast<int32_t>(nd), static_cast<int32_t>(nw));
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t run_tdp_fast_bwd(const TdpArgs& ad, const TdpArgs& aw, const int32_t* chunks, int tiles_n, int tiles_k,
+                            int nnz, hipStream_t s) {
+  using C = TdpFastCfgs<T>;
+  if constexpr (sizeof(T) == 4) {
+    if (ad.B <= C::Narrow::BN) return launch_tdp_fast_bwd<typename C::Narrow, T>(ad, aw, chunks, tiles_n, tiles_k, nnz, s);
+  }
+  return launch_tdp_fast_bwd<typename C::Rows, T>(ad, aw, chunks, tiles_n, tiles_k, nnz, s);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -1136,6 +1203,37 @@ int ard_tile_bwd_data(const ard_tile_desc* desc, const ard_tile_plan* plan, cons
       ARD_HIP_CHECK(run_tdp_fast<float>(TDP_BWD_DATA, a, plan->d_chunks, plan->tiles_k, plan->nnz, s));
     else
       ARD_HIP_CHECK(run_tdp<float>(TDP_BWD_DATA, a, plan->tiles_k, plan->nnz, full, s));
+  }
+  return ARD_OK;
+}
+
+int ard_tile_bwd(const ard_tile_desc* desc, const ard_tile_plan* plan, const void* Xt, const void* dYt,
+                 const void* W, void* dXt, float* dW, void* stream) {
+  clear_error();
+  int st = check_tile_call(desc, plan);
+  if (st != ARD_OK) return st;
+  if ((st = check_dev_ptr(Xt, "Xt")) || (st = check_dev_ptr(dYt, "dYt")) || (st = check_dev_ptr(W, "W")) ||
+      (st = check_dev_ptr(dXt, "dXt")) || (st = check_dev_ptr(dW, "dW")))
+    return st;
+  const TdpArgs ad = {dYt, nullptr, W, dXt, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
+                      plan->d_col_ptr, plan->d_col_rows, desc->scale, plan->d_row_ptr + plan->tiles_n};
+  const TdpArgs aw = {Xt, dYt, nullptr, dW, desc->batch, plan->n, plan->k, plan->tile, plan->tiles_k,
+                      plan->d_row_ptr, plan->d_row_cols, desc->scale, plan->d_row_ptr + plan->tiles_n};
+  const bool bf = desc->dtype == ARD_BF16;
+  if (!(bf ? tdp_fast_ok<bf16>(ad) : tdp_fast_ok<float>(ad))) {  // the two calls one after the other
+    if ((st = ard_tile_bwd_data(desc, plan, dYt, W, dXt, stream)) != ARD_OK) return st;
+    return ard_tile_bwd_weight(desc, plan, Xt, dYt, dW, stream);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (bf)
+    ARD_HIP_CHECK(run_tdp_fast_bwd<bf16>(ad, aw, plan->d_chunks, plan->tiles_n, plan->tiles_k, plan->nnz, s));
+  else
+    ARD_HIP_CHECK(run_tdp_fast_bwd<float>(ad, aw, plan->d_chunks, plan->tiles_n, plan->tiles_k, plan->nnz, s));
+  const int full = plan->tiles_n * plan->tiles_k;
+  if (desc->dropped == ARD_DROPPED_ZERO && plan->nnz != full) {
+    hipLaunchKernelGGL(zero_dropped_tiles_kernel, dim3(plan->tiles_k, plan->tiles_n), dim3(256), 0, s,
+                       plan->d_bits, dW, plan->k, plan->tile, plan->tiles_k);
+    ARD_LAUNCH_CHECK();
   }
   return ARD_OK;
 }

@@ -88,7 +88,11 @@ def run_tile(dtype, B, N, K, tile, words, scale=1.0, dropped=api.ARD_DROPPED_ZER
     api.ard_tile_fwd(desc, plan, Xt, Wd, Yt)
     api.ard_tile_bwd_data(desc, plan, dYt, Wd, dXt)
     api.ard_tile_bwd_weight(desc, plan, Xt, dYt, dW)
+    # the backward in one call (one launch on the fast path): bit for bit the separate calls
+    dXt2, dW2 = torch.full_like(dXt, 5.0), torch.full_like(dW, sentinel)
+    api.ard_tile_bwd(desc, plan, Xt, dYt, Wd, dXt2, dW2)
     torch.cuda.synchronize()
+    assert torch.equal(dXt2, dXt) and torch.equal(dW2, dW), "ard_tile_bwd differs from the separate calls"
     Xa, Wm, dYa = np.abs(f64(X)), np.abs(f64(W)) * M, np.abs(f64(dY))
     t = tol(dtype)
     compare(f64(Yt).T, Y64, abs(scale) * Xa @ Wm.T, t, "Y")
@@ -184,7 +188,11 @@ def test_full_config_bf16_4096():
     api.ard_tile_fwd(desc, plan, Xt, Wd, Yt)
     api.ard_tile_bwd_data(desc, plan, dYt, Wd, dXt)
     api.ard_tile_bwd_weight(desc, plan, Xt, dYt, dW)
+    # the backward in one call (one launch on the fast path): bit for bit the separate calls
+    dXt2, dW2 = torch.full_like(dXt, 5.0), torch.full_like(dW, -1.0)  # ZERO mode writes every entry
+    api.ard_tile_bwd(desc, plan, Xt, dYt, Wd, dXt2, dW2)
     torch.cuda.synchronize()
+    assert torch.equal(dXt2, dXt) and torch.equal(dW2, dW), "ard_tile_bwd differs from the separate calls"
     rng = np.random.default_rng(0)
     rows = np.sort(rng.choice(N, 48, replace=False))
     cols = np.sort(rng.choice(K, 48, replace=False))
