@@ -483,10 +483,11 @@ class TileLayer:
     """One layer under a tile-based pattern: each step draws a Bernoulli(1 - p)
     keep bitmap over the 64 x 64 tiles of W[N][K] on the device together with
     the kept-tile lists (one kernel; the same draws as the host sampler, which
-    the FLOP count and the oracle use), then runs fwd, bwd_data and bwd_weight,
-    reading and writing only kept tiles."""
+    the FLOP count and the oracle use), then runs the forward and the backward
+    (bwd_data and bwd_weight in one launch), reading and writing only kept
+    tiles."""
 
-    def __init__(self, name, n, k, batch, tile, dtype, seed, w_std):
+    def __init__(self, name, n, k, batch, tile, dtype, seed, w_std, fused_bwd=True):
         import torch
         from paper_1805_08939_amd import api, synth
         self.api, self.torch = api, torch
@@ -517,7 +518,10 @@ class TileLayer:
         self.desc = api.tile_desc(api.ARD_BF16 if dtype == "bf16" else api.ARD_F32, batch, k, n, 1.0,
                                   api.ARD_DROPPED_SKIP)
         self.stream = torch.cuda.current_stream().cuda_stream
-        self.order = [("fwd", 0), ("bwd_data", 0), ("bwd_weight", 0)]
+        # the backward as one call (bwd_data and bwd_weight in one launch), or
+        # the two calls one after the other
+        self.fused_bwd = fused_bwd
+        self.order = [("fwd", 0), ("bwd", 0)] if fused_bwd else [("fwd", 0), ("bwd_data", 0), ("bwd_weight", 0)]
         self.config = {"workload": name, "global_batch": batch, "layer": [k, n], "tile": tile,
                        "patterns": "Bernoulli tile bitmap per step, keep probability 1 - p", "dropped": "skip"}
 
@@ -537,6 +541,7 @@ class TileLayer:
     def layer_calls(self, plan):
         api, d, st = self.api, self.desc, self.stream
         return {("fwd", 0): (api.ard_tile_fwd, (d, plan, self.Xt, self.W, self.Yt, st), {}),
+                ("bwd", 0): (api.ard_tile_bwd, (d, plan, self.Xt, self.dYt, self.W, self.dXt, self.dW, st), {}),
                 ("bwd_data", 0): (api.ard_tile_bwd_data, (d, plan, self.dYt, self.W, self.dXt, st), {}),
                 ("bwd_weight", 0): (api.ard_tile_bwd_weight, (d, plan, self.Xt, self.dYt, self.dW, st), {})}
 
@@ -565,7 +570,7 @@ class TileLayer:
         if isinstance(pats, int):  # a step number: its pattern from the host sampler
             pats = self.patterns(pats)
         f = 2.0 * self.B * self.tile * self.tile * pats[1]
-        per = {key: f for key in self.order}
+        per = {key: (2 * f if key[0] == "bwd" else f) for key in self.order}
         return sum(per.values()), per
 
     def kept_bytes(self, pats):
@@ -576,7 +581,9 @@ class TileLayer:
         es = 2 if self.dtype == "bf16" else 4
         wt = pats[1] * self.tile * self.tile
         x, y = self.K * self.B * es, self.N * self.B * es
-        return {("fwd", 0): wt * es + x + y, ("bwd_data", 0): wt * es + y + x, ("bwd_weight", 0): y + x + 4 * wt}
+        per = {("fwd", 0): wt * es + x + y, ("bwd_data", 0): wt * es + y + x, ("bwd_weight", 0): y + x + 4 * wt}
+        per[("bwd", 0)] = per[("bwd_data", 0)] + per[("bwd_weight", 0)]
+        return {key: per[key] for key in self.order}
 
     def prepare(self, it):
         self.planned = {}
