@@ -1371,7 +1371,7 @@ def main():
         return summarize_counters(args.summarize_counters, args.top, args.last, args.tail)
     if args.summarize_pass:
         spec = WORKLOADS[args.workload]
-        per_step = {"Mlp": 2 * (len(spec.get("dims", ())) - 1), "TileLayer": 3, "TileLayerTdp": 3}.get(spec["cls"], 2)
+        per_step = {"Mlp": 2 * (len(spec.get("dims", ())) - 1)}.get(spec["cls"], 2)  # fwd and bwd per layer
         return summarize_pass(args.summarize_pass, args.top, args.steps * per_step, args.pass_kind)
     if args.digest:
         return print(source_digest())
