@@ -163,3 +163,56 @@ def test_sampler_argument_errors():
         api.ard_tile_bitmap_tdp(2, 2, 3, 3)
     with pytest.raises(api.ArdError):
         api.ard_tile_bitmap_bernoulli(2, 2, 1.5, 0, 0, 0)
+
+
+def test_tile_call_validation_on_host():
+    """Every tile-layer entry point rejects a bad descriptor, plan or operand
+    on the host, before anything is launched (no GPU needed): each case below
+    must fail validation, with the status its header states."""
+    fake = 1 << 20  # 16-byte aligned, never dereferenced: every case fails before a launch
+
+    def plan(**kw):
+        p = dict(n=256, k=128, tile=64, tiles_n=4, tiles_k=2, nnz=3, d_bits=fake, d_row_ptr=fake,
+                 d_row_cols=fake, d_col_ptr=fake, d_col_rows=fake, d_flat=fake, d_chunks=fake)
+        p.update(kw)
+        return _ffi.ard_tile_plan(**p)
+
+    def desc(**kw):
+        d = dict(dtype=api.ARD_BF16, batch=64, in_features=128, out_features=256, scale=1.0,
+                 dropped=api.ARD_DROPPED_SKIP)
+        d.update(kw)
+        return _ffi.ard_tile_desc(**d)
+
+    calls = {
+        "fwd": lambda d, p, x=fake: api.ard_tile_fwd(d, p, x, fake, fake),
+        "bwd_data": lambda d, p, x=fake: api.ard_tile_bwd_data(d, p, x, fake, fake),
+        "bwd_weight": lambda d, p, x=fake: api.ard_tile_bwd_weight(d, p, x, fake, fake),
+        "bwd": lambda d, p, x=fake: api.ard_tile_bwd(d, p, x, fake, fake, fake, fake),
+    }
+    bad = [
+        (desc(dtype=7), plan(), _ffi.ARD_ERR_UNSUPPORTED, "dtype"),
+        (desc(batch=0), plan(), _ffi.ARD_ERR_INVALID_ARG, "batch"),
+        (desc(dropped=5), plan(), _ffi.ARD_ERR_INVALID_ARG, "dropped"),
+        (desc(scale=float("nan")), plan(), _ffi.ARD_ERR_INVALID_ARG, "scale"),
+        (desc(scale=float("inf")), plan(), _ffi.ARD_ERR_INVALID_ARG, "scale"),
+        (desc(), plan(tile=48), _ffi.ARD_ERR_INVALID_ARG, "tile"),
+        (desc(in_features=192), plan(), _ffi.ARD_ERR_INVALID_ARG, "does not match"),
+        (desc(), plan(tiles_n=3), _ffi.ARD_ERR_INVALID_ARG, "grid"),
+        (desc(), plan(nnz=9), _ffi.ARD_ERR_INVALID_ARG, "nnz"),
+        (desc(), plan(nnz=-2), _ffi.ARD_ERR_INVALID_ARG, "nnz"),
+        (desc(), plan(d_chunks=None), _ffi.ARD_ERR_INVALID_ARG, "NULL lists"),
+    ]
+    for name, call in calls.items():
+        for d, p, status, msg in bad:
+            with pytest.raises(api.ArdError) as e:
+                call(d, p)
+            assert e.value.status == status, (name, msg, e.value.message)
+            assert msg in e.value.message, (name, msg, e.value.message)
+        for x, msg in ((None, "is NULL"), (fake + 8, "aligned")):
+            with pytest.raises(api.ArdError) as e:
+                call(desc(), plan(), x)
+            assert e.value.status == _ffi.ARD_ERR_INVALID_ARG and msg in e.value.message, (name, e.value.message)
+        fn = getattr(_ffi.lib(), f"ard_tile_{name}")
+        nargs = 6 if name == "bwd" else 4
+        assert fn(None, ctypes.byref(plan()), *([None] * nargs)) == _ffi.ARD_ERR_INVALID_ARG  # NULL descriptor
+        assert fn(ctypes.byref(desc()), None, *([None] * nargs)) == _ffi.ARD_ERR_INVALID_ARG  # NULL plan
