@@ -866,10 +866,11 @@ struct FastCfgs<float> {
   using Wide = Huge;
   using Tall = Huge;
   using Big = FastCfg<float, 64, 64, 64, 3, 2, 2, 2>;     // 96 KB, 8 waves on 32-deep k shares
+  using Narrow = FastCfg<float, 128, 32, 32, 4, 2, 1, 2>; // 80 KB, 4 waves on 16-deep k shares
   using Small = FastCfg<float, 32, 32, 128, 4, 1, 1, 8>;  // 128 KB, 8 waves on 16-deep k shares
 };
 
-enum FastKind { FAST_HUGE, FAST_WIDE, FAST_TALL, FAST_BIG, FAST_SMALL };
+enum FastKind { FAST_HUGE, FAST_WIDE, FAST_TALL, FAST_BIG, FAST_SMALL, FAST_NARROW };
 
 struct FastPlan {
   int kind;    // FastKind
@@ -894,6 +895,15 @@ inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
   FastPlan p;
   int bk;
   int64_t tiles;
+  const int64_t kb = kbatch > 0 ? kbatch : 1;
+  // at most 32 columns (an LSTM's per-step products at a small batch): 128 x
+  // 32 tiles, so that most of each tile is not zero padding of the columns
+  if (N <= C::Narrow::BN && tiles_of(C::Narrow::BM, C::Narrow::BN) >= kTargetBlocks * 5 / 8) {
+    p.kind = FAST_NARROW;
+    tiles = tiles_of(C::Narrow::BM, C::Narrow::BN);
+    p.splits = kb * K >= 8192 ? fast_splits(tiles, kb * ((K + C::Narrow::BK - 1) / C::Narrow::BK)) : 1;
+    return p;
+  }
   if (M > C::Big::BM && N > C::Big::BN && tiles_of(C::Huge::BM, C::Huge::BN) >= kTargetBlocks * 5 / 8) {
     p.kind = FAST_HUGE;
     bk = C::Huge::BK;
@@ -907,7 +917,6 @@ inline FastPlan plan_fast_f32(int M, int N, int K, int kbatch, int batch) {
     bk = C::Small::BK;
     tiles = tiles_of(C::Small::BM, C::Small::BN);
   }
-  const int64_t kb = kbatch > 0 ? kbatch : 1;
   const int64_t slabs = kb * ((K + bk - 1) / bk);
   if (p.kind == FAST_SMALL) {
     // A 32x32 workgroup takes about 0.9 us per 128-deep slab however many run
@@ -1055,6 +1064,9 @@ inline hipError_t launch_planned(const GemmArgs& g, int kind, int batch, hipStre
       return launch_fast<typename C::Tall, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
     case FAST_BIG:
       return launch_fast<typename C::Big, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+    case FAST_NARROW:  // fp32 only
+      if constexpr (sizeof(T) == 4) return launch_fast<typename C::Narrow, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
+      else return hipErrorNotSupported;
     default:
       return launch_fast<typename C::Small, AMC, BMC, OutT, EPI, RSUM>(g, batch, stream);
   }

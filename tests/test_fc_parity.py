@@ -161,6 +161,16 @@ def test_multi_tile_ragged(dtype, shape):
                   use_null_plans=False, lists=i % 2 == 1)
 
 
+@pytest.mark.parametrize("B", [16, 20, 32])
+def test_small_batch_tall_layer_fp32(B):
+    """At most 32 batch columns and 161 row tiles of 128 rows: the fp32
+    forward runs on 128 x 32 tiles (ragged rows and columns)."""
+    K, N = 264, 128 * 160 + 37
+    X, W, b, dY = make_inputs("f32", B, K, N, seed=B)
+    for pin, act in (((1, 0), "relu"), ((2, 1), "none")):
+        run_layer("f32", X, W, b, dY, pin, (1, 0), act, 1.25, api.ARD_DROPPED_ZERO, use_null_plans=False)
+
+
 def random_cases(dtype, n, seed):
     """n seeded layer shapes and patterns spread over the planner's choices:
     batch from 1 to 600, sides from 1 to 3000 (the long contractions take a

@@ -115,6 +115,15 @@ def test_all_units_kept_wide_recurrence_tiles(shape):
     run_lstm(*shape, (1, 0), seed=sum(shape), with_state=True)
 
 
+@pytest.mark.parametrize("shape,pattern,in_pattern", [((35, 20, 640, 320), (2, 1), (1, 0)),
+                                                      ((35, 20, 768, 320), (2, 0), (2, 1))])
+def test_small_batch_steps_on_narrow_tiles(shape, pattern, in_pattern):
+    """Batch 20 over 35 steps: the step-batched input projection (and, with
+    every input kept, the input gradient) has 20 columns per step and at
+    least 160 row tiles of 128, so it runs on 128 x 32 tiles."""
+    run_lstm(*shape, pattern, seed=sum(shape), in_pattern=in_pattern)
+
+
 def random_lstm_cases(n, seed):
     """n seeded layer shapes: 1-5 steps, batch 1-100, input and hidden sizes
     1-700, a hidden pattern of period 1-16 and (in a third of the cases) an
